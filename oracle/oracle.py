@@ -1,0 +1,145 @@
+"""ctypes wrapper over the C oracle (``stacklstm_oracle.c``). Test infrastructure only.
+
+``run`` executes the branching StackLSTM (paper, section 2 definitions of Push and
+Pop, section 3 hold op) and its exact reverse-mode gradient (section 5) on the
+selected batch elements; ``alg1`` executes Algorithm 1 literally (forward only).
+Arrays come straight from ``paper_1904_03409_amd.workloads`` (or any caller) as
+float32 / int8; results are float64 (``mode="f64"``) or float32 (``mode="f32"``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "stacklstm_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+ERRORS = {1: "EINVAL", 2: "EOPS", 3: "EUNDERFLOW"}
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle status {code} ({ERRORS.get(code, '?')})")
+        self.code = code
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain -O3, OpenMP over batch elements)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-shared", "-fPIC", "-Wall", "-o", tmp, _SRC, "-lm"],
+                              cwd=_HERE)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i = ctypes.c_int
+        for sfx in ("f64", "f32"):
+            f = getattr(lib, f"oracle_run_{sfx}")
+            f.restype = i
+            f.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, P, P, i, i, i] + [P] * 12
+            g = getattr(lib, f"oracle_alg1_{sfx}")
+            g.restype = i
+            g.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i] + [P] * 6
+        lib.oracle_round_bf16.restype = None
+        lib.oracle_round_bf16.argtypes = [P, P, ctypes.c_long]
+        lib.oracle_max_threads.restype = i
+        _lib = lib
+    return _lib
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f32(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float32)
+
+
+def round_bf16(a: np.ndarray) -> np.ndarray:
+    a = _f32(a)
+    out = np.empty_like(a)
+    _load().oracle_round_bf16(_p(a), _p(out), a.size)
+    return out
+
+
+def _unpack(wl, kw):
+    if wl is not None:
+        d = dict(T=wl.T, B=wl.B, I=wl.I, H=wl.H, x=wl.x, ops=wl.ops, W=wl.W, U=wl.U, b=wl.b, h0=wl.h0, c0=wl.c0,
+                 dh_top=wl.dh_top, dc_top=wl.dc_top)
+        d.update(kw)
+        return d
+    return kw
+
+
+def run(wl=None, sel: Optional[Sequence[int]] = None, mode: str = "f64", bf16: bool = False,
+        threads: Optional[int] = None, backward: bool = True, **kw) -> dict:
+    """Branching StackLSTM forward + backward on the batch elements ``sel``.
+
+    Returns h_top, c_top, h_cell, c_cell ([T, n, H]; h_cell/c_cell NaN on non-push
+    steps), ptr [T+1, n], top [T, n], and with ``backward``: dx [T, n, I], dW, dU,
+    db (summed over the selected elements), dh0, dc0 [n, H].
+    """
+    a = _unpack(wl, kw)
+    T, B, I, H = int(a["T"]), int(a["B"]), int(a["I"]), int(a["H"])
+    sel = np.arange(B, dtype=np.int32) if sel is None else np.ascontiguousarray(sel, dtype=np.int32)
+    n = int(sel.size)
+    dt = np.float64 if mode == "f64" else np.float32
+    x, W, U, b, h0, c0 = (_f32(a[k]) for k in ("x", "W", "U", "b", "h0", "c0"))
+    ops = np.ascontiguousarray(a["ops"], dtype=np.int8)
+    dh_top = _f32(a.get("dh_top")) if backward else None
+    dc_top = _f32(a.get("dc_top")) if backward else None
+    o = dict(h_top=np.empty((T, n, H), dt), c_top=np.empty((T, n, H), dt),
+             h_cell=np.full((T, n, H), np.nan, dt), c_cell=np.full((T, n, H), np.nan, dt),
+             ptr=np.zeros((T + 1, n), np.int32), top=np.zeros((T, n), np.int32))
+    if backward:
+        o.update(dx=np.zeros((T, n, I), dt), dW=np.zeros((I, 4 * H), dt), dU=np.zeros((H, 4 * H), dt),
+                 db=np.zeros(4 * H, dt), dh0=np.zeros((n, H), dt), dc0=np.zeros((n, H), dt))
+    th = max_threads() if threads is None else int(threads)
+    f = getattr(_load(), f"oracle_run_{mode}")
+    rc = f(T, B, I, H, _p(x), _p(ops), _p(W), _p(U), _p(b), _p(h0), _p(c0), _p(dh_top), _p(dc_top), _p(sel), n,
+           int(bool(bf16)), th, _p(o["h_top"]), _p(o["c_top"]), _p(o["h_cell"]), _p(o["c_cell"]), _p(o["ptr"]),
+           _p(o["top"]), _p(o.get("dx")), _p(o.get("dW")), _p(o.get("dU")), _p(o.get("db")), _p(o.get("dh0")),
+           _p(o.get("dc0")))
+    if rc:
+        raise OracleError(rc)
+    o["threads"] = th
+    return o
+
+
+def alg1(wl=None, sel: Optional[Sequence[int]] = None, bf16: bool = False, threads: Optional[int] = None,
+         mode: str = "f64", **kw) -> dict:
+    """Algorithm 1 executed literally: h_cell/c_cell on every step, h_top/c_top, ptr, top."""
+    a = _unpack(wl, kw)
+    T, B, I, H = int(a["T"]), int(a["B"]), int(a["I"]), int(a["H"])
+    sel = np.arange(B, dtype=np.int32) if sel is None else np.ascontiguousarray(sel, dtype=np.int32)
+    n = int(sel.size)
+    dt = np.float64 if mode == "f64" else np.float32
+    x, W, U, b, h0, c0 = (_f32(a[k]) for k in ("x", "W", "U", "b", "h0", "c0"))
+    ops = np.ascontiguousarray(a["ops"], dtype=np.int8)
+    o = dict(h_top=np.empty((T, n, H), dt), c_top=np.empty((T, n, H), dt), h_cell=np.empty((T, n, H), dt),
+             c_cell=np.empty((T, n, H), dt), ptr=np.zeros((T + 1, n), np.int32), top=np.zeros((T, n), np.int32))
+    th = max_threads() if threads is None else int(threads)
+    f = getattr(_load(), f"oracle_alg1_{mode}")
+    rc = f(T, B, I, H, _p(x), _p(ops), _p(W), _p(U), _p(b), _p(h0), _p(c0), _p(sel), n, int(bool(bf16)), th,
+           _p(o["h_top"]), _p(o["c_top"]), _p(o["h_cell"]), _p(o["c_cell"]), _p(o["ptr"]), _p(o["top"]))
+    if rc:
+        raise OracleError(rc)
+    return o
