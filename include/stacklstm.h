@@ -1,0 +1,121 @@
+/*
+ * stacklstm.h -- C ABI of the MI355X (gfx950) parallelised StackLSTM step.
+ *
+ * Method: Ding & Koehn, "Parallelizable Stack Long Short-Term Memory" (2019).
+ * Each batch element carries its own stack of (h, c) states and its own op stream,
+ * op in {+1 push, -1 pop, 0 hold} (section 2 defines Push and Pop, section 3 the
+ * unified pointer update p <- p + op and the hold op). Algorithm 1 (section 3) is run
+ * for every element at every step with no op-dependent branch: read the state at the
+ * pointer p, run one LSTM cell on (x_t, h_p), write the result to slot p + 1, move p
+ * by op, return the state at the new p. The cell-state stack is handled exactly like
+ * the hidden-state stack (footnote of section 2). Backward is BPTT through the stack
+ * reads (section 5: gradient reaches popped and overwritten states).
+ *
+ * LSTM cell (the paper names the standard LSTM without equations): gates i, f, g, o,
+ * a = x W + h_prev U + b, i = sig(a_i), f = sig(a_f), g = tanh(a_g), o = sig(a_o),
+ * c = f c_prev + i g, h = o tanh(c). Gate k of hidden unit u is column k*H + u of W, U
+ * and b (torch.nn.LSTMCell order: weight_ih = W^T, weight_hh = U^T, bias_ih = b,
+ * bias_hh = 0).
+ *
+ * Conventions for every entry point:
+ *  - All array arguments are DEVICE pointers, owned by the caller; the library keeps
+ *    none of them after the call returns. Shapes are row-major, time-major.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream), except
+ *    that stacklstm_fwd reads back one status word after validating the ops (the only
+ *    host synchronisation), and that a positive dims->spin_limit (debug) makes both
+ *    calls synchronise at the end to report SLSTM_ETIMEOUT.
+ *  - Gradient outputs are overwritten, not accumulated.
+ *  - On an error status nothing further is launched; output contents are unspecified.
+ *  - No exception crosses the ABI. The functions keep no mutable global state apart
+ *    from cached device properties; calls on different work spaces may overlap.
+ *  - Supported sizes: T >= 0, B >= 1, I >= 1, 1 <= H <= 512 (SLSTM_FP32) or
+ *    H <= 1024 (SLSTM_BF16_GEMM); B up to 8 groups of 128 rows per XCC pass
+ *    (SLSTM_ENORESIDENT beyond what one launch can hold).
+ */
+#ifndef STACKLSTM_H
+#define STACKLSTM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SLSTM_OK = 0,
+  SLSTM_EINVAL = 1,        /* bad dims, NULL required pointer, unsupported size */
+  SLSTM_EOPS = 2,          /* an op outside {-1, 0, 1} */
+  SLSTM_EUNDERFLOW = 3,    /* a pop while only the initial state is on the stack */
+  SLSTM_EWORKSPACE = 4,    /* ws_bytes < stacklstm_workspace_bytes(dims) */
+  SLSTM_ENORESIDENT = 5,   /* the persistent kernels cannot be made co-resident */
+  SLSTM_EDEVICE = 6,       /* a HIP runtime error */
+  SLSTM_ETIMEOUT = 7       /* a group barrier exceeded dims->spin_limit polls */
+} slstm_status;
+
+typedef enum {
+  SLSTM_FP32 = 0,          /* fp32 operands, fp32 accumulation */
+  SLSTM_BF16_GEMM = 1      /* operands of every matrix product rounded to bf16 (nearest
+                              even): x, W, U, h_prev, dA; fp32 accumulation, fp32 h/c,
+                              fp32 nonlinearities */
+} slstm_precision;
+
+typedef struct {
+  int32_t T;               /* steps */
+  int32_t B;               /* batch elements */
+  int32_t I;               /* input size */
+  int32_t H;               /* hidden size */
+  int32_t precision;       /* slstm_precision */
+  int32_t spin_limit;      /* 0 = default barrier spin limit; > 0 = debug limit + final sync */
+} slstm_dims;
+
+/* Bytes of device work space that stacklstm_fwd / stacklstm_bwd need for `d`
+ * (0 for invalid dims). The work space carries the forward's gate activations and
+ * stack to the backward; pass the same buffer, untouched, to both calls. */
+size_t stacklstm_workspace_bytes(const slstm_dims* d);
+
+/* Forward over T steps (Algorithm 1 for every element and step).
+ *  x      [T, B, I]   inputs x_t                                 (read)
+ *  ops    [T, B]      int8 ops, +1 push / -1 pop / 0 hold         (read)
+ *  W [I, 4H], U [H, 4H], b [4H], h0 [B, H], c0 [B, H]             (read)
+ *  h_cell, c_cell [T, B, H]   the LSTM output of step t, i.e. the state Algorithm 1
+ *                             writes to slot p + 1 at step t      (written)
+ *  h_top, c_top   [T, B, H]   Algorithm 1's return value: the state at the pointer
+ *                             after step t; may be NULL           (written)
+ *  ptr    [T + 1, B]  int32 pointer before step t (ptr[T] = after the last step)
+ *  top    [T, B]      int32 step that produced the returned state of step t, -1 for the
+ *                     initial state (h0, c0)                      (written)
+ * Returns SLSTM_EOPS / SLSTM_EUNDERFLOW after validating ops (before any other work). */
+int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                  const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
+                  float* c_top, int32_t* ptr, int32_t* top, void* workspace, size_t ws_bytes, void* stream);
+
+/* Backward of L given dL/dh_top and dL/dc_top (section 5), after stacklstm_fwd on the
+ * same inputs and work space.
+ *  x, ops, W, U, h0, c0       as given to stacklstm_fwd          (read)
+ *  h_cell, c_cell, top        as written by stacklstm_fwd        (read)
+ *  dh_top [T, B, H]           gradient w.r.t. h_top              (read)
+ *  dc_top [T, B, H] or NULL   gradient w.r.t. c_top (NULL = 0)   (read)
+ *  dx [T, B, I], dW [I, 4H], dU [H, 4H], db [4H], dh0 [B, H], dc0 [B, H]  (written)
+ * dx is exactly 0 on steps whose op is not push. */
+int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                  const float* h0, const float* c0, const float* h_cell, const float* c_cell, const int32_t* top,
+                  void* workspace, size_t ws_bytes, const float* dh_top, const float* dc_top, float* dx, float* dW,
+                  float* dU, float* db, float* dh0, float* dc0, void* stream);
+
+/* Synchronises `stream` and reports SLSTM_ETIMEOUT if a persistent kernel of the last
+ * call on `workspace` gave up on a group barrier, SLSTM_OK otherwise. */
+int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream);
+
+/* Static text for a status code. */
+const char* stacklstm_status_string(int status);
+
+/* Launch configuration chosen for `d`: fills groups, workgroups per group, rows per
+ * group and K chunks; returns a status like the entry points. Informational. */
+int stacklstm_plan(const slstm_dims* d, int32_t* groups, int32_t* wg_per_group, int32_t* rows_per_group,
+                   int32_t* k_chunks);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STACKLSTM_H */

@@ -1,0 +1,365 @@
+// Host side of the StackLSTM library: argument checks, work-space layout, launch
+// configuration and the launch order of the forward and backward passes.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+#include <algorithm>
+#include <mutex>
+
+#include "../../include/stacklstm.h"
+#include "common.h"
+#include "gemm.h"
+#include "rec_config.h"
+#include "recurrent.h"
+
+__global__ void k_init_ctl(uint32_t* ctl);
+__global__ void k_scan(const int8_t* ops, int T, int B, int32_t* ptr, uint32_t* ctl);
+__global__ void k_gather_top(const int32_t* top, const float* cellv, const float* init, float* out, int T, int B,
+                             int H);
+__global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
+__global__ void k_fill_f32(float* p, size_t n, float v);
+__global__ void k_zero_u32(uint32_t* p, int n);
+template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
+__global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
+                                float* out);
+
+namespace {
+
+constexpr int kDefaultSpin = 1 << 22;
+constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 32;
+
+struct DevInfo { int cus; bool ok; };
+
+int device_cus() {
+  static std::mutex mu;
+  static DevInfo info[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!info[dev].ok) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) != hipSuccess) return 0;
+    info[dev].cus = p.multiProcessorCount;
+    info[dev].ok = true;
+  }
+  return info[dev].cus;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Plan {
+  int prec, KS, ks_eff, NT, G, NW, per_xcc;
+  int splits_w, splits_u;
+};
+
+struct Layout {
+  size_t ctl, stack, wp, r1, stash, hx, dh, dc, dbp, part, total;
+};
+
+bool dims_ok(const slstm_dims* d) {
+  if (!d) return false;
+  if (d->T < 0 || d->B < 1 || d->I < 1 || d->H < 1) return false;
+  if (d->precision != SLSTM_FP32 && d->precision != SLSTM_BF16_GEMM) return false;
+  if (d->H > (d->precision == SLSTM_FP32 ? 512 : 1024)) return false;
+  if ((int64_t)d->T * d->B > ((int64_t)1 << 28)) return false;
+  // the persistent kernels address T*B*4H fp32 (fp32 mode) or bf16 values with 32-bit byte offsets
+  const int64_t esz = d->precision == SLSTM_FP32 ? 4 : 2;
+  if ((int64_t)d->T * d->B * 4 * d->H * esz >= ((int64_t)1 << 32)) return false;
+  if ((int64_t)d->T * d->B * d->H * 4 >= ((int64_t)1 << 32)) return false;
+  return true;
+}
+
+int ks_bucket(int prec, int ks_eff) {
+  const int lo = prec ? 2 : 4;
+  int ks = lo;
+  while (ks < ks_eff) ks *= 2;
+  return ks <= 32 ? ks : -1;
+}
+
+int splits_for(int M, int N, int K) {
+  int tiles = ((M + kGemmBM - 1) / kGemmBM) * ((N + kGemmBN - 1) / kGemmBN);
+  int s = std::max(1, 1024 / std::max(1, tiles));
+  int max_s = std::max(1, (K + kGemmBK - 1) / kGemmBK);
+  return std::min(std::min(s, 64), max_s);
+}
+
+// Chooses rows per group (16*NT) so that every group's workgroups fit on one XCC.
+int make_plan(const slstm_dims* d, Plan* p) {
+  if (!dims_ok(d)) return SLSTM_EINVAL;
+  const int prec = d->precision;
+  const int KC = rec_kc(prec);
+  p->prec = prec;
+  p->ks_eff = (d->H + KC - 1) / KC;
+  p->KS = ks_bucket(prec, p->ks_eff);
+  if (p->KS < 0) return SLSTM_EINVAL;
+  p->NW = (d->H + 15) / 16;
+  const int cus = device_cus();
+  const int cu_per_xcc = cus > 0 ? cus / 8 : 32;
+  for (int NT = 1; NT <= 8; NT *= 2) {
+    int G = (d->B + 16 * NT - 1) / (16 * NT);
+    if (G > MAX_GROUPS) continue;
+    int per_xcc = p->NW * ((G + 7) / 8);
+    int occ_f = 0, occ_b = 0;
+    RecArgs dummy;
+    memset(&dummy, 0, sizeof(dummy));
+    if (launch_fwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ_f) != hipSuccess) return SLSTM_EDEVICE;
+    if (launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ_b) != hipSuccess) return SLSTM_EDEVICE;
+    int occ = std::min(occ_f, occ_b);
+    if (per_xcc <= cu_per_xcc * occ) {
+      p->NT = NT;
+      p->G = G;
+      p->per_xcc = per_xcc;
+      int64_t K = (int64_t)d->T * d->B;
+      p->splits_w = splits_for(d->I, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
+      p->splits_u = splits_for(d->H, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
+      return SLSTM_OK;
+    }
+  }
+  return SLSTM_ENORESIDENT;
+}
+
+// Work-space layout; splits are bounded by 64 so the layout does not depend on the device.
+Layout layout(const slstm_dims* d) {
+  const size_t T = d->T, B = d->B, I = d->I, H = d->H;
+  const bool bf = d->precision == SLSTM_BF16_GEMM;
+  Layout L;
+  size_t o = 0;
+  L.ctl = o; o += align256(CTL_WORDS * 4);
+  L.stack = o; o += align256(B * (T + 1) * 4);
+  L.wp = o; o += align256(I * 4 * H * 4);
+  L.r1 = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));   // XW (forward), dA (backward)
+  L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
+  L.hx = o; o += bf ? align256(T * B * H * 2) : 0;
+  L.dh = o; o += align256((T + 1) * B * H * 4);
+  L.dc = o; o += align256((T + 1) * B * H * 4);
+  L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
+  L.part = o; o += align256((size_t)64 * std::max(I, H) * 4 * H * 4);
+  L.total = o;
+  return L;
+}
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return SLSTM_OK;
+  if (e == hipErrorCooperativeLaunchTooLarge) return SLSTM_ENORESIDENT;
+  return SLSTM_EDEVICE;
+}
+
+int grid1d(size_t n) { return (int)std::min<size_t>((n + 255) / 256, 8192); }
+
+int launch_gemm(int prec, int AL, int BL, const GemmArgs& g, int splits, hipStream_t st) {
+  dim3 grid((g.N + kGemmBN - 1) / kGemmBN, (g.M + kGemmBM - 1) / kGemmBM, splits);
+#define GCASE(P, A, B_)                                                       \
+  if (prec == P && AL == A && BL == B_) {                                     \
+    hipLaunchKernelGGL((k_gemm<P, A, B_>), grid, dim3(256), 0, st, g);        \
+    return hip_status(hipGetLastError());                                     \
+  }
+  GCASE(0, GEMM_MK, GEMM_KN) GCASE(0, GEMM_MK, GEMM_NK) GCASE(0, GEMM_KM, GEMM_KN) GCASE(0, GEMM_KM_GATHER, GEMM_KN)
+  GCASE(1, GEMM_MK, GEMM_KN) GCASE(1, GEMM_MK, GEMM_NK) GCASE(1, GEMM_KM, GEMM_KN) GCASE(1, GEMM_KM_GATHER, GEMM_KN)
+#undef GCASE
+  return SLSTM_EINVAL;
+}
+
+int check_timeout(const uint32_t* ctl, hipStream_t st) {
+  uint32_t v = 0;
+  if (hipMemcpyAsync(&v, ctl + CTL_TIMEOUT, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
+  if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
+  return v ? SLSTM_ETIMEOUT : SLSTM_OK;
+}
+
+RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L) {
+  RecArgs a;
+  memset(&a, 0, sizeof(a));
+  a.T = d->T; a.B = d->B; a.I = d->I; a.H = d->H;
+  a.G = p.G; a.NW = p.NW; a.ks_eff = p.ks_eff;
+  a.spin_limit = d->spin_limit > 0 ? d->spin_limit : kDefaultSpin;
+  a.ctl = (uint32_t*)(ws + L.ctl);
+  a.stack = (int32_t*)(ws + L.stack);
+  a.stash = (float*)(ws + L.stash);
+  a.hx = d->precision == SLSTM_BF16_GEMM ? (uint16_t*)(ws + L.hx) : nullptr;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t stacklstm_workspace_bytes(const slstm_dims* d) {
+  if (!dims_ok(d)) return 0;
+  return layout(d).total;
+}
+
+const char* stacklstm_status_string(int s) {
+  switch (s) {
+    case SLSTM_OK: return "ok";
+    case SLSTM_EINVAL: return "invalid argument (dims, null pointer or unsupported size)";
+    case SLSTM_EOPS: return "op outside {-1, 0, 1}";
+    case SLSTM_EUNDERFLOW: return "pop with only the initial state on the stack";
+    case SLSTM_EWORKSPACE: return "work space too small";
+    case SLSTM_ENORESIDENT: return "persistent kernels cannot be co-resident";
+    case SLSTM_EDEVICE: return "HIP runtime error";
+    case SLSTM_ETIMEOUT: return "group barrier spin limit exceeded";
+    default: return "unknown status";
+  }
+}
+
+int stacklstm_plan(const slstm_dims* d, int32_t* groups, int32_t* wg_per_group, int32_t* rows_per_group,
+                   int32_t* k_chunks) {
+  Plan p;
+  int rc = make_plan(d, &p);
+  if (rc) return rc;
+  if (groups) *groups = p.G;
+  if (wg_per_group) *wg_per_group = p.NW;
+  if (rows_per_group) *rows_per_group = 16 * p.NT;
+  if (k_chunks) *k_chunks = p.ks_eff;
+  return SLSTM_OK;
+}
+
+int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                  const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
+                  float* c_top, int32_t* ptr, int32_t* top, void* workspace, size_t ws_bytes, void* stream) {
+  if (!dims_ok(d)) return SLSTM_EINVAL;
+  if (!ptr || !workspace ||
+      (d->T > 0 && (!ops || !x || !W || !U || !b || !h0 || !c0 || !h_cell || !c_cell || !top)))
+    return SLSTM_EINVAL;
+  const Layout L = layout(d);
+  if (ws_bytes < L.total) return SLSTM_EWORKSPACE;
+  Plan p;
+  int rc = make_plan(d, &p);
+  if (rc) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  uint32_t* ctl = (uint32_t*)(ws + L.ctl);
+  const int T = d->T, B = d->B, I = d->I, H = d->H;
+
+  // a1: validate ops and scan the pointer (the call's one host synchronisation)
+  hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl);
+  hipLaunchKernelGGL(k_scan, dim3((B + 15) / 16), dim3(256), 0, st, ops, T, B, ptr, ctl);
+  uint32_t hs[2] = {0, 0};
+  if (hipMemcpyAsync(hs, ctl + CTL_STATUS, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
+  if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
+  if (hs[0] != 0x7fffffffu) return (int)(hs[0] & 7u);
+  if (T == 0) return SLSTM_OK;
+
+  // a2: XW = x Wp + b for all steps (Wp = W with gate-interleaved columns)
+  const bool bf = p.prec == SLSTM_BF16_GEMM;
+  void* wp = ws + L.wp;
+  hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W,
+                     bf ? nullptr : (float*)wp, bf ? (bf16_t*)wp : nullptr, I, H);
+  float* xw = (float*)(ws + L.r1);
+  GemmArgs g;
+  memset(&g, 0, sizeof(g));
+  g.M = T * B; g.N = 4 * H; g.K = I;
+  g.A = x; g.lda = I; g.a_bf16 = 0; g.a_vec = (I % 4 == 0);
+  g.Bm = wp; g.ldb = 4 * H; g.b_bf16 = bf; g.b_vec = 1;
+  g.C = xw; g.ldc = 4 * H; g.bias = b; g.bias_H = H;
+  g.k_chunk = ((I + kGemmBK - 1) / kGemmBK) * kGemmBK; g.split_stride = 0;
+  if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_KN, g, 1, st))) return rc;
+
+  // a3-a6: persistent recurrent kernel
+  RecArgs a = rec_args(d, p, ws, L);
+  a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
+  if ((rc = hip_status(launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
+
+  // a7: Algorithm 1's return values
+  size_t n = (size_t)T * B * H;
+  if (h_top) hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H);
+  if (c_top) hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, c_top, T, B, H);
+  if ((rc = hip_status(hipGetLastError()))) return rc;
+  if (d->spin_limit > 0) return check_timeout(ctl, st);
+  return SLSTM_OK;
+}
+
+int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                  const float* h0, const float* c0, const float* h_cell, const float* c_cell, const int32_t* top,
+                  void* workspace, size_t ws_bytes, const float* dh_top, const float* dc_top, float* dx, float* dW,
+                  float* dU, float* db, float* dh0, float* dc0, void* stream) {
+  (void)W;
+  if (!dims_ok(d)) return SLSTM_EINVAL;
+  if (!workspace || !dW || !dU || !db || !dh0 || !dc0) return SLSTM_EINVAL;
+  if (d->T > 0 && (!x || !ops || !U || !h0 || !c0 || !h_cell || !c_cell || !top || !dh_top || !dx))
+    return SLSTM_EINVAL;
+  const Layout L = layout(d);
+  if (ws_bytes < L.total) return SLSTM_EWORKSPACE;
+  Plan p;
+  int rc = make_plan(d, &p);
+  if (rc) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  uint32_t* ctl = (uint32_t*)(ws + L.ctl);
+  const int T = d->T, B = d->B, I = d->I, H = d->H;
+  const bool bf = p.prec == SLSTM_BF16_GEMM;
+  if (T == 0) {
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, dW, (size_t)I * 4 * H, 0.f);
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)H * 4 * H)), dim3(256), 0, st, dU, (size_t)H * 4 * H, 0.f);
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)4 * H)), dim3(256), 0, st, db, (size_t)4 * H, 0.f);
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, dh0, (size_t)B * H, 0.f);
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, dc0, (size_t)B * H, 0.f);
+    return hip_status(hipGetLastError());
+  }
+
+  // a8: persistent reverse loop
+  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_XCC_SLOT_B, 16);
+  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_BAR_B, 16 * MAX_GROUPS);
+  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_ABORT, 2);
+  RecArgs a = rec_args(d, p, ws, L);
+  a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0;
+  a.hcell = const_cast<float*>(h_cell); a.ccell = const_cast<float*>(c_cell); a.top = const_cast<int32_t*>(top);
+  a.dh_top = dh_top; a.dc_top = dc_top;
+  a.dA = ws + L.r1;
+  a.dh_acc = (float*)(ws + L.dh); a.dc_acc = (float*)(ws + L.dc);
+  a.db_part = (float*)(ws + L.dbp);
+  a.dh0 = dh0; a.dc0 = dc0;
+  if ((rc = hip_status(launch_bwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
+
+  // a9: post-loop gradients
+  const int H4 = 4 * H;
+  float* part = (float*)(ws + L.part);
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H4)), dim3(256), 0, st, a.db_part, p.G, (size_t)H4, 1, H4,
+                     H, db);
+  const int K = T * B;
+  GemmArgs g;
+  // dW = x^T dA
+  memset(&g, 0, sizeof(g));
+  g.M = I; g.N = H4; g.K = K;
+  g.A = x; g.lda = I; g.a_bf16 = 0; g.a_vec = (I % 4 == 0);
+  g.Bm = a.dA; g.ldb = H4; g.b_bf16 = bf; g.b_vec = 1;
+  g.C = part; g.ldc = H4;
+  g.k_chunk = ((K + p.splits_w - 1) / p.splits_w + kGemmBK - 1) / kGemmBK * kGemmBK;
+  int sw = (K + g.k_chunk - 1) / g.k_chunk;
+  g.split_stride = (size_t)I * H4;
+  if ((rc = launch_gemm(p.prec, GEMM_KM, GEMM_KN, g, sw, st))) return rc;
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, sw, g.split_stride, I,
+                     H4, H, dW);
+  // dU = Hprev^T dA, Hprev rows gathered through the producer table
+  memset(&g, 0, sizeof(g));
+  g.M = H; g.N = H4; g.K = K;
+  g.A = nullptr; g.a_bf16 = 0; g.a_vec = (H % 4 == 0);
+  g.gtop = top; g.gh0 = h0; g.gcell = bf ? (const void*)(ws + L.hx) : (const void*)h_cell; g.gcell_bf16 = bf;
+  g.gB = B; g.gH = H;
+  g.Bm = a.dA; g.ldb = H4; g.b_bf16 = bf; g.b_vec = 1;
+  g.C = part; g.ldc = H4;
+  g.k_chunk = ((K + p.splits_u - 1) / p.splits_u + kGemmBK - 1) / kGemmBK * kGemmBK;
+  int su = (K + g.k_chunk - 1) / g.k_chunk;
+  g.split_stride = (size_t)H * H4;
+  if ((rc = launch_gemm(p.prec, GEMM_KM_GATHER, GEMM_KN, g, su, st))) return rc;
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, su, g.split_stride, H,
+                     H4, H, dU);
+  // dx = dA Wp^T
+  memset(&g, 0, sizeof(g));
+  g.M = K; g.N = I; g.K = H4;
+  g.A = a.dA; g.lda = H4; g.a_bf16 = bf; g.a_vec = 1;
+  g.Bm = ws + L.wp; g.ldb = H4; g.b_bf16 = bf; g.b_vec = 1;
+  g.C = dx; g.ldc = I;
+  g.k_chunk = ((H4 + kGemmBK - 1) / kGemmBK) * kGemmBK;
+  if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, 1, st))) return rc;
+  if ((rc = hip_status(hipGetLastError()))) return rc;
+  if (d->spin_limit > 0) return check_timeout(ctl, st);
+  return SLSTM_OK;
+}
+
+int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream) {
+  if (!workspace || ws_bytes < align256(CTL_WORDS * 4)) return SLSTM_EINVAL;
+  return check_timeout((const uint32_t*)workspace, (hipStream_t)stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,138 @@
+// Shared device helpers for the StackLSTM HIP library (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;  // raw bfloat16 bits in memory
+
+// Status codes shared with the C-ABI (values fixed by include/stacklstm.h).
+enum {
+  ST_OK = 0, ST_EINVAL = 1, ST_EOPS = 2, ST_EUNDERFLOW = 3, ST_EWORKSPACE = 4,
+  ST_ENORESIDENT = 5, ST_EDEVICE = 6, ST_ETIMEOUT = 7
+};
+
+// Work-space word offsets (uint32 units) of the control block at the start of the work space.
+enum {
+  CTL_STATUS = 0,        // lowest (element * 8 + code) of a failing element, or 0x7fffffff
+  CTL_MAXDEPTH = 1,
+  CTL_ABORT = 2,         // set when a group barrier ran out of spins
+  CTL_TIMEOUT = 3,
+  CTL_XCC_SLOT = 16,     // 16 per-XCC slot counters (forward kernel)
+  CTL_XCC_SLOT_B = 32,   // 16 per-XCC slot counters (backward kernel)
+  CTL_BAR_F = 64,        // forward group barrier counters, one 64-byte line per group
+  CTL_BAR_B = 64 + 16 * 64,   // backward group barrier counters
+  CTL_WORDS = 64 + 2 * 16 * 64
+};
+#define MAX_GROUPS 64
+
+// Gate-interleaved ("permuted") column order used inside the library: column 4*u + k
+// holds gate k (0=i, 1=f, 2=g, 3=o) of hidden unit u. The caller's order is k*H + u.
+__device__ __forceinline__ int perm_to_orig(int np, int H) { return (np & 3) * H + (np >> 2); }
+
+__device__ __forceinline__ float bf16_bits_to_f32(bf16_t v) {
+  return __uint_as_float(((uint32_t)v) << 16);
+}
+// Round to bfloat16, nearest-even (the hardware conversion on gfx950).
+__device__ __forceinline__ __bf16 f32_to_bf16(float f) { return static_cast<__bf16>(f); }
+__device__ __forceinline__ bf16_t f32_to_bf16_bits(float f) {
+  __bf16 h = static_cast<__bf16>(f);
+  return __builtin_bit_cast(bf16_t, h);
+}
+
+__device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_bf16_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float sigmoidf_(float z) {
+  // logistic, in the form that cannot overflow
+  if (z >= 0.f) return 1.f / (1.f + expf(-z));
+  float e = expf(z);
+  return e / (1.f + e);
+}
+
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 0xf;
+}
+
+// Loads of data that another CU wrote earlier in the same kernel. They go through a
+// buffer descriptor (bounds-checked: an offset past `bytes` reads 0 instead of faulting)
+// with the sc1 cache policy, which bypasses this CU's L1 and reads the XCC's L2, so a
+// line that L1 cached before the other CU's write is never returned stale.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, size_t bytes) {
+  uint32_t n = bytes > 0xffffffffu ? 0xffffffffu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+constexpr int kSc1 = 16;  // cache-policy bit SC1 of gfx94x/gfx950 memory instructions
+__device__ __forceinline__ uint4 ld_coh_b128(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kSc1));
+}
+__device__ __forceinline__ uint32_t ld_coh_b32(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSc1);
+}
+__device__ __forceinline__ uint16_t ld_coh_b16(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kSc1);
+}
+
+// Group barrier for workgroups that all run on one XCC (one shared L2).
+// Each wave waits until its own stores are acknowledged by L2, the workgroup meets at
+// s_barrier, one lane adds to the group counter and polls it with L1-bypassing loads.
+// Data written by other workgroups before the barrier must then be read with the
+// ld_coh_* loads above. Returns true when the spin limit ran out (or another group's
+// did): the caller must then leave its loop so that every wave of the grid exits.
+__device__ __forceinline__ bool group_barrier(uint32_t* ctr, uint32_t target, uint32_t* ctl, int spin_limit,
+                                              int* s_flag) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int spins = 0, bad = 0;
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      ++spins;
+      if ((spins & 255) == 0 && __hip_atomic_load(&ctl[CTL_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+        bad = 1;
+        break;
+      }
+      if (spins > spin_limit) {
+        __hip_atomic_store(&ctl[CTL_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&ctl[CTL_TIMEOUT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        bad = 1;
+        break;
+      }
+    }
+    *s_flag = bad;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// Claims this workgroup's (group, member) slot from the XCC it runs on, so that every
+// group's members share one XCC. Groups are dealt to XCCs round-robin (group g on XCC
+// g % 8); a workgroup with nothing to do gets group -1 and must exit.
+__device__ __forceinline__ void claim_group_slot(uint32_t* slot_ctrs, int G, int NW, int* s_g, int* s_w) {
+  if (threadIdx.x == 0) {
+    unsigned x = xcc_id();
+    int g = -1, w = 0;
+    if (x < 8) {
+      unsigned slot = __hip_atomic_fetch_add(&slot_ctrs[x], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      int per_xcc = NW * ((G + 7) / 8);
+      if ((int)slot < per_xcc) {
+        int lg = (int)slot / NW;
+        w = (int)slot % NW;
+        g = lg * 8 + (int)x;
+        if (g >= G) g = -1;
+      }
+    }
+    *s_g = g;
+    *s_w = w;
+  }
+  __syncthreads();
+}

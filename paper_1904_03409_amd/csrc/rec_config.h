@@ -1,0 +1,36 @@
+// Compile-time configuration table of the persistent recurrent kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+
+// K per chunk of the register-resident U slice: 16 (fp32 MFMA, 4 k per lane x 4 steps)
+// or 32 (bf16 MFMA, 8 k per lane).
+constexpr int rec_kc(int prec) { return prec ? 32 : 16; }
+constexpr int rec_lds_ld(int prec, int ks) { return ks * rec_kc(prec) + (prec ? 8 : 4); }
+// Row tiles staged in LDS per pass: as many as fit in about 68 KB, so two workgroups
+// can share a CU when the configuration needs it.
+constexpr int rec_ntb(int prec, int nt, int ks) {
+  int per_tile = 16 * rec_lds_ld(prec, ks) * (prec ? 2 : 4);
+  int cap = 69632 / per_tile;
+  int ntb = 1;
+  while (ntb * 2 <= nt && ntb * 2 <= cap) ntb *= 2;
+  return ntb;
+}
+constexpr size_t rec_lds_bytes(int prec, int ntb, int ks) {
+  return (size_t)16 * ntb * rec_lds_ld(prec, ks) * (prec ? 2 : 4);
+}
+// Workgroups per CU the kernel is compiled for: 2 for the bf16 H > 512 case (64
+// workgroups per group), 1 otherwise.
+constexpr int rec_occ(int prec, int ks) { return (prec == 1 && ks == 32) ? 2 : 1; }
+
+#define REC_CASES(X) \
+  X(0, 1, 4) X(0, 1, 8) X(0, 1, 16) X(0, 1, 32) \
+  X(0, 2, 4) X(0, 2, 8) X(0, 2, 16) X(0, 2, 32) \
+  X(0, 4, 4) X(0, 4, 8) X(0, 4, 16) X(0, 4, 32) \
+  X(0, 8, 4) X(0, 8, 8) X(0, 8, 16) X(0, 8, 32) \
+  X(1, 1, 2) X(1, 1, 4) X(1, 1, 8) X(1, 1, 16) X(1, 1, 32) \
+  X(1, 2, 2) X(1, 2, 4) X(1, 2, 8) X(1, 2, 16) X(1, 2, 32) \
+  X(1, 4, 2) X(1, 4, 4) X(1, 4, 8) X(1, 4, 16) X(1, 4, 32) \
+  X(1, 8, 2) X(1, 8, 4) X(1, 8, 8) X(1, 8, 16) X(1, 8, 32)
+
+hipError_t launch_fwd(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);
+hipError_t launch_bwd(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);

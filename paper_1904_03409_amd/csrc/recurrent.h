@@ -1,0 +1,30 @@
+// Launch descriptions of the persistent recurrent kernels (forward and backward).
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+struct RecArgs {
+  int T, B, I, H;
+  int G, NW, ks_eff, spin_limit;   // batch groups, workgroups per group, K chunks in use, barrier spin limit
+  const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
+  const int8_t* ops;     // [T][B]
+  const float* U;        // [H][4H] caller layout (gate-major columns)
+  const float* h0;       // [B][H]
+  const float* c0;       // [B][H]
+  float* hcell;          // [T][B][H]  state computed at step t (written to slot p+1)
+  float* ccell;          // [T][B][H]
+  uint16_t* hx;          // [T][B][H]  bf16 copy of hcell (bf16-GEMM mode)
+  float* stash;          // [T][B][4H] gate activations i, f, g, o, gate-interleaved
+  int32_t* top;          // [T][B]     producer step of the state returned at step t (-1 = initial)
+  int32_t* stack;        // [B][T+1]   step index written to each stack slot
+  uint32_t* ctl;         // control block (status, barrier counters)
+  // backward
+  const float* dh_top;   // [T][B][H]
+  const float* dc_top;   // [T][B][H] or null
+  void* dA;              // [T][B][4H] fp32 or bf16: gradient w.r.t. the gate pre-activations
+  float* dh_acc;         // [T+1][B][H] gradient w.r.t. each produced state (slot 0 = initial)
+  float* dc_acc;         // [T+1][B][H]
+  float* db_part;        // [G][4H] per-group bias gradient (gate-interleaved)
+  float* dh0;            // [B][H]
+  float* dc0;            // [B][H]
+};

@@ -1,0 +1,98 @@
+// Op validation and stack-pointer scan (paper, section 3: the unified update p <- p + op
+// with op in {+1 push, -1 pop, 0 hold}). ptr[t][b] is the pointer before step t;
+// ptr[T][b] the pointer after the last step. A pop while only the initial state is on
+// the stack (p would become -1) is reported as EUNDERFLOW, an op outside {-1, 0, 1} as
+// EOPS; the reported element is the lowest failing batch index, and within it the
+// earliest failing step decides the code.
+#include "common.h"
+
+__global__ void __launch_bounds__(256) k_init_ctl(uint32_t* ctl) {
+  for (int i = threadIdx.x; i < CTL_WORDS; i += blockDim.x) ctl[i] = (i == CTL_STATUS) ? 0x7fffffffu : 0u;
+}
+
+// Block of 256 threads = 16 columns x 16 time segments. Two passes over each segment:
+// segment sums, a scan of the 16 sums per column in LDS, then the pointer values.
+__global__ void __launch_bounds__(256) k_scan(const int8_t* __restrict__ ops, int T, int B, int32_t* __restrict__ ptr,
+                                              uint32_t* ctl) {
+  __shared__ int s_sum[16][17];
+  __shared__ int s_first_bad[16], s_first_uf[16], s_maxd;
+  const int c = threadIdx.x & 15, seg = threadIdx.x >> 4;
+  const int b = blockIdx.x * 16 + c;
+  const int L = (T + 15) / 16;
+  const int t0 = seg * L, t1 = min(T, t0 + L);
+  if (threadIdx.x < 16) { s_first_bad[threadIdx.x] = 0x7fffffff; s_first_uf[threadIdx.x] = 0x7fffffff; }
+  if (threadIdx.x == 0) s_maxd = 0;
+  int sum = 0;
+  if (b < B) {
+    for (int t = t0; t < t1; ++t) {
+      int op = ops[(size_t)t * B + b];
+      sum += (op >= -1 && op <= 1) ? op : 0;
+    }
+  }
+  s_sum[c][seg] = sum;
+  __syncthreads();
+  int off = 0;
+  for (int s = 0; s < seg; ++s) off += s_sum[c][s];
+  int first_bad = 0x7fffffff, first_uf = 0x7fffffff, maxd = 0;
+  if (b < B) {
+    if (seg == 0) ptr[b] = 0;
+    int p = off;
+    for (int t = t0; t < t1; ++t) {
+      int op = ops[(size_t)t * B + b];
+      if (op < -1 || op > 1) { if (first_bad == 0x7fffffff) first_bad = t; op = 0; }
+      p += op;
+      if (p < 0 && first_uf == 0x7fffffff) first_uf = t;
+      ptr[(size_t)(t + 1) * B + b] = p;
+      maxd = max(maxd, p);
+    }
+    atomicMin(&s_first_bad[c], first_bad);
+    atomicMin(&s_first_uf[c], first_uf);
+    atomicMax(&s_maxd, maxd);
+  }
+  __syncthreads();
+  if (seg == 0 && b < B) {
+    int fb = s_first_bad[c], fu = s_first_uf[c];
+    int code = 0;
+    if (fb != 0x7fffffff || fu != 0x7fffffff) code = (fu < fb) ? ST_EUNDERFLOW : ST_EOPS;
+    if (code) atomicMin((int*)&ctl[CTL_STATUS], b * 8 + code);
+  }
+  if (threadIdx.x == 0) atomicMax(&ctl[CTL_MAXDEPTH], (uint32_t)s_maxd);
+}
+
+// h_top / c_top materialisation: the state returned at step t (Algorithm 1's return value)
+// is the one produced at step top[t][b], or the initial state when top is -1.
+__global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ top, const float* __restrict__ cellv,
+                                                    const float* __restrict__ init, float* __restrict__ out, int T,
+                                                    int B, int H) {
+  const size_t n = (size_t)T * B * H;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    size_t tb = i / H;
+    int u = (int)(i - tb * H);
+    int b = (int)(tb % B);
+    int s = top[tb];
+    int t = (int)(tb / B);
+    if (s < -1 || s > t) { out[i] = __builtin_nanf(""); continue; }   // not a valid producer
+    out[i] = (s < 0) ? init[(size_t)b * H + u] : cellv[((size_t)s * B + b) * H + u];
+  }
+}
+
+// W [I][4H] (gate-major columns) -> Wp [I][4H] gate-interleaved, as fp32 or bf16.
+__global__ void __launch_bounds__(256) k_permute_w(const float* __restrict__ W, float* __restrict__ Wp32,
+                                                   bf16_t* __restrict__ Wp16, int I, int H) {
+  const size_t n = (size_t)I * 4 * H;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    size_t row = i / (4 * (size_t)H);
+    int np = (int)(i - row * 4 * H);
+    float v = W[row * 4 * H + perm_to_orig(np, H)];
+    if (Wp32) Wp32[i] = v;
+    if (Wp16) Wp16[i] = f32_to_bf16_bits(v);
+  }
+}
+
+__global__ void __launch_bounds__(256) k_fill_f32(float* __restrict__ p, size_t n, float v) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+__global__ void __launch_bounds__(256) k_zero_u32(uint32_t* __restrict__ p, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
+}

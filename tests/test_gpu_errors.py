@@ -1,0 +1,84 @@
+"""Error paths of the C-ABI: every bad input returns its status code, nothing faults."""
+import numpy as np
+import pytest
+import torch
+
+from paper_1904_03409_amd import workloads as wk
+from tests.gpu_helpers import need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(wl, **kw):
+    from paper_1904_03409_amd.stacklstm import DeviceRun
+    r = DeviceRun.from_workload(wl, **kw)
+    return r, r.forward(check=False)
+
+
+def test_bad_op_and_underflow():
+    need_gpu()
+    ops = np.ones((10, 4), np.int8)
+    ops[3, 2] = 5
+    r, rc = _run(wk.custom(T=10, B=4, I=3, H=8, seed=0, ops=ops))
+    assert rc == 2
+    ops = np.ones((10, 4), np.int8)
+    ops[0, 1] = -1
+    r, rc = _run(wk.custom(T=10, B=4, I=3, H=8, seed=0, ops=ops))
+    assert rc == 3
+    ops = np.zeros((10, 4), np.int8)
+    ops[2, 3] = 1
+    ops[3, 3] = -1
+    ops[4, 3] = -1                # second pop of element 3 underflows at step 4
+    ops[6, 3] = 7                 # a later bad op does not change the code of element 3
+    r, rc = _run(wk.custom(T=10, B=4, I=3, H=8, seed=0, ops=ops))
+    assert rc == 3
+
+
+def test_workspace_dims_and_null():
+    need_gpu()
+    from paper_1904_03409_amd import stacklstm as s
+    wl = wk.custom(T=8, B=4, I=3, H=8, seed=0)
+    r, rc = _run(wl)
+    assert rc == 0
+    small = torch.empty(r.workspace.numel() - 256, dtype=torch.uint8, device="cuda")
+    rc = s.stacklstm_fwd(r.dims, r.x, r.ops, r.W, r.U, r.b, r.h0, r.c0, r.h_cell, r.c_cell, None, None, r.ptr,
+                         r.top, small, check=False)
+    assert rc == 4
+    bad = s.make_dims(8, 4, 3, 2000)
+    assert s.stacklstm_workspace_bytes(bad) == 0
+    rc = s.stacklstm_fwd(bad, r.x, r.ops, r.W, r.U, r.b, r.h0, r.c0, r.h_cell, r.c_cell, None, None, r.ptr, r.top,
+                         r.workspace, check=False)
+    assert rc == 1
+    rc = s.stacklstm_fwd(r.dims, None, r.ops, r.W, r.U, r.b, r.h0, r.c0, r.h_cell, r.c_cell, None, None, r.ptr,
+                         r.top, r.workspace, check=False)
+    assert rc == 1
+
+
+def test_spin_limit_timeout_reported():
+    """A one-poll barrier limit forced from the host: the kernels give up, every
+    workgroup leaves its loop, and the call reports SLSTM_ETIMEOUT."""
+    need_gpu()
+    wl = wk.make("parser")
+    r, rc = _run(wl, spin_limit=1)
+    assert rc in (0, 7)
+    assert rc == 7
+    torch.cuda.synchronize()
+    # the same buffers run normally afterwards
+    from paper_1904_03409_amd import stacklstm as s
+    r2, rc2 = _run(wl)
+    assert rc2 == 0
+    assert s.stacklstm_sync_status(r2.workspace) == 0
+
+
+def test_empty_T():
+    need_gpu()
+    wl = wk.custom(T=0, B=3, I=2, H=4, seed=0, ops=np.zeros((0, 3), np.int8))
+    from paper_1904_03409_amd.stacklstm import DeviceRun
+    r = DeviceRun.from_workload(wl)
+    r.forward()
+    r.backward()
+    torch.cuda.synchronize()
+    out = r.results()
+    assert np.all(out["ptr"] == 0)
+    for k in ("dW", "dU", "db", "dh0", "dc0"):
+        assert np.all(out[k] == 0)

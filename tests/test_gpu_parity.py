@@ -1,0 +1,86 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle on the same
+seeded inputs. Traces must match bit for bit; floats within the normwise tolerance
+(1e-5 fp32, 2e-2 bf16-GEMM against the oracle with bf16-rounded operands)."""
+import numpy as np
+import pytest
+
+from paper_1904_03409_amd import workloads as wk
+from tests.gpu_helpers import compare, need_gpu, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(oracle_mod, wl, precision, sel=None, alg1=True):
+    need_gpu()
+    print(f"[gpu] {wl.name} T={wl.T} B={wl.B} I={wl.I} H={wl.H} prec={precision}", flush=True)
+    gpu, _ = run_gpu(wl, precision=precision)
+    bf = precision == 1
+    ref = oracle_mod.run(wl, sel=sel, bf16=bf)
+    a1 = oracle_mod.alg1(wl, sel=sel, bf16=bf) if alg1 else None
+    errs = compare(wl, gpu, ref, precision, sel=sel, alg1=a1, check_weights=sel is None)
+    print(f"[gpu] errors {errs}", flush=True)
+    return gpu
+
+
+@pytest.mark.parametrize("precision", [0, 1])
+@pytest.mark.parametrize("name", ["tiny", "parser"])
+def test_named_configs(oracle_mod, name, precision):
+    _check(oracle_mod, wk.make(name), precision)
+
+
+SHAPES = [
+    # (T, B, I, H): odd sizes, ragged batch, the paper's H=200 / I=48 cell, the H=I=1 cell
+    (37, 5, 7, 13),
+    (50, 17, 48, 200),
+    (23, 3, 1, 1),
+    (64, 33, 64, 64),
+    (41, 130, 32, 96),
+]
+
+
+@pytest.mark.parametrize("precision", [0, 1])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_odd_shapes(oracle_mod, shape, precision):
+    T, B, I, H = shape
+    wl = wk.custom(T=T, B=B, I=I, H=H, seed=T * 7 + H, wscale=0.3, random_state=True, dc_top=True)
+    _check(oracle_mod, wl, precision)
+
+
+def _streams(kind, T, B, rng):
+    if kind == "all_push":
+        return np.ones((T, B), np.int8)
+    if kind == "all_hold":
+        return np.zeros((T, B), np.int8)
+    if kind == "hold_then_push":
+        o = np.zeros((T, B), np.int8)
+        o[T // 2:] = 1
+        return o
+    if kind == "alternate":
+        o = np.zeros((T, B), np.int8)
+        o[0::2] = 1
+        o[1::2] = -1
+        return o
+    if kind == "deep":
+        return np.stack([wk.ops_deep_stream(rng, T, (20, 40), (10, 30)) for _ in range(B)], axis=1)
+    raise ValueError(kind)
+
+
+@pytest.mark.parametrize("precision", [0, 1])
+@pytest.mark.parametrize("kind", ["all_push", "all_hold", "hold_then_push", "alternate", "deep"])
+def test_edge_streams(oracle_mod, kind, precision):
+    rng = np.random.default_rng(5)
+    T, B = 96, 20
+    wl = wk.custom(T=T, B=B, I=24, H=40, seed=3, ops=_streams(kind, T, B, rng), wscale=0.3, random_state=True)
+    gpu = _check(oracle_mod, wl, precision)
+    if kind == "all_hold":
+        assert np.all(gpu["dW"] == 0) and np.all(gpu["dU"] == 0) and np.all(gpu["db"] == 0)
+
+
+@pytest.mark.parametrize("precision", [0, 1])
+def test_deterministic(precision):
+    need_gpu()
+    wl = wk.make("parser")
+    a, _ = run_gpu(wl, precision=precision)
+    b, _ = run_gpu(wl, precision=precision)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
