@@ -67,7 +67,22 @@ typedef struct {
   int32_t H;               /* hidden size */
   int32_t precision;       /* slstm_precision */
   int32_t spin_limit;      /* 0 = default barrier spin limit; > 0 = debug limit + final sync */
+  void* phase_events;      /* NULL, or an array of SLSTM_PHASE_EVENTS hipEvent_t created by the
+                              caller; the calls record them on `stream` between their phases:
+                              fwd [0] start, [1] after the op scan and its status read-back,
+                              [2] after the input projection, [3] after the persistent forward
+                              kernel, [4] after the h_top/c_top gathers; bwd [5] start, [6] after
+                              the persistent backward kernel, [7] after dW and db, [8] after dU,
+                              [9] after dx. For profiling only. */
+  void* step_clock;        /* NULL, or a device int64 buffer of 2 * 512 * T * 4 entries: the
+                              persistent kernels store 100 MHz wall-clock stamps per workgroup
+                              and step, [pass (0 fwd, 1 bwd)][workgroup][t][4], at four points of
+                              each step (forward: loop top, h_prev staged, MFMA done, epilogue
+                              done; backward: loop top, epilogue done, barrier passed, dh
+                              scattered). For profiling only. */
 } slstm_dims;
+
+#define SLSTM_PHASE_EVENTS 10
 
 /* Bytes of device work space that stacklstm_fwd / stacklstm_bwd need for `d`
  * (0 for invalid dims). The work space carries the forward's gate activations and

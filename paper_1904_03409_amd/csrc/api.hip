@@ -144,6 +144,10 @@ int hip_status(hipError_t e) {
   return SLSTM_EDEVICE;
 }
 
+void mark(const slstm_dims* d, int i, hipStream_t st) {
+  if (d->phase_events) (void)hipEventRecord(((hipEvent_t*)d->phase_events)[i], st);
+}
+
 int grid1d(size_t n) { return (int)std::min<size_t>((n + 255) / 256, 8192); }
 
 int launch_gemm(int prec, int AL, int BL, const GemmArgs& g, int splits, hipStream_t st) {
@@ -176,6 +180,10 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L) 
   a.stack = (int32_t*)(ws + L.stack);
   a.stash = (float*)(ws + L.stash);
   a.hx = d->precision == SLSTM_BF16_GEMM ? (uint16_t*)(ws + L.hx) : nullptr;
+  a.clk = (long long*)d->step_clock;
+  const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
+  a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
+  a.coh_top = ((size_t)d->B * 4) % 128 != 0;
   return a;
 }
 
@@ -232,12 +240,14 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   const int T = d->T, B = d->B, I = d->I, H = d->H;
 
   // a1: validate ops and scan the pointer (the call's one host synchronisation)
+  mark(d, 0, st);
   hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl);
   hipLaunchKernelGGL(k_scan, dim3((B + 15) / 16), dim3(256), 0, st, ops, T, B, ptr, ctl);
   uint32_t hs[2] = {0, 0};
   if (hipMemcpyAsync(hs, ctl + CTL_STATUS, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
   if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
   if (hs[0] != 0x7fffffffu) return (int)(hs[0] & 7u);
+  mark(d, 1, st);
   if (T == 0) return SLSTM_OK;
 
   // a2: XW = x Wp + b for all steps (Wp = W with gate-interleaved columns)
@@ -254,17 +264,20 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   g.C = xw; g.ldc = 4 * H; g.bias = b; g.bias_H = H;
   g.k_chunk = ((I + kGemmBK - 1) / kGemmBK) * kGemmBK; g.split_stride = 0;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_KN, g, 1, st))) return rc;
+  mark(d, 2, st);
 
   // a3-a6: persistent recurrent kernel
   RecArgs a = rec_args(d, p, ws, L);
   a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
   if ((rc = hip_status(launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
+  mark(d, 3, st);
 
   // a7: Algorithm 1's return values
   size_t n = (size_t)T * B * H;
   if (h_top) hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H);
   if (c_top) hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, c_top, T, B, H);
   if ((rc = hip_status(hipGetLastError()))) return rc;
+  mark(d, 4, st);
   if (d->spin_limit > 0) return check_timeout(ctl, st);
   return SLSTM_OK;
 }
@@ -298,6 +311,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   }
 
   // a8: persistent reverse loop
+  mark(d, 5, st);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_XCC_SLOT_B, 16);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_BAR_B, 16 * MAX_GROUPS);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_ABORT, 2);
@@ -309,7 +323,9 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   a.dh_acc = (float*)(ws + L.dh); a.dc_acc = (float*)(ws + L.dc);
   a.db_part = (float*)(ws + L.dbp);
   a.dh0 = dh0; a.dc0 = dc0;
+  if (a.clk) a.clk += (size_t)512 * T * 4;
   if ((rc = hip_status(launch_bwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
+  mark(d, 6, st);
 
   // a9: post-loop gradients
   const int H4 = 4 * H;
@@ -330,6 +346,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if ((rc = launch_gemm(p.prec, GEMM_KM, GEMM_KN, g, sw, st))) return rc;
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, sw, g.split_stride, I,
                      H4, H, dW);
+  mark(d, 7, st);
   // dU = Hprev^T dA, Hprev rows gathered through the producer table
   memset(&g, 0, sizeof(g));
   g.M = H; g.N = H4; g.K = K;
@@ -344,6 +361,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if ((rc = launch_gemm(p.prec, GEMM_KM_GATHER, GEMM_KN, g, su, st))) return rc;
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, su, g.split_stride, H,
                      H4, H, dU);
+  mark(d, 8, st);
   // dx = dA Wp^T
   memset(&g, 0, sizeof(g));
   g.M = K; g.N = I; g.K = H4;
@@ -353,6 +371,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   g.k_chunk = ((H4 + kGemmBK - 1) / kGemmBK) * kGemmBK;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, 1, st))) return rc;
   if ((rc = hip_status(hipGetLastError()))) return rc;
+  mark(d, 9, st);
   if (d->spin_limit > 0) return check_timeout(ctl, st);
   return SLSTM_OK;
 }

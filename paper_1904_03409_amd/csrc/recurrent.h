@@ -6,6 +6,10 @@
 struct RecArgs {
   int T, B, I, H;
   int G, NW, ks_eff, spin_limit;   // batch groups, workgroups per group, K chunks in use, barrier spin limit
+  // 1 when a cache line of the exchanged arrays can hold entries of two different steps
+  // (rows not 128-byte multiples): then every exchanged value is read with L1-bypassing
+  // loads; with aligned rows a line is never read before its only write, plain loads suffice
+  int coh_rows, coh_top;
   const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)
@@ -27,4 +31,5 @@ struct RecArgs {
   float* db_part;        // [G][4H] per-group bias gradient (gate-interleaved)
   float* dh0;            // [B][H]
   float* dc0;            // [B][H]
+  long long* clk;        // optional per-step wall-clock stamps [grid][T][4] (profiling)
 };

@@ -91,7 +91,9 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
   __syncthreads();
 
+  long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
   for (int t = T - 1; t >= 0; --t) {
+    if (clk && threadIdx.x == 0) clk[t * 4 + 0] = wall_clock64();
     if ((int)threadIdx.x < BG) {
       int b = row0 + (int)threadIdx.x;
       int op = 0, tp = -1, sp = -1;
@@ -149,49 +151,82 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       }
     }
 
+    if (clk && threadIdx.x == 0) clk[t * 4 + 1] = wall_clock64();
     if (group_barrier(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_flag)) break;
+    if (clk && threadIdx.x == 0) clk[t * 4 + 2] = wall_clock64();
 
     // ---- dh_prev^T (16 units x 16 rows per tile) = U^T-slice x dA^T over this wave's gate columns
+    // B fragments are fetched one group of CG chunks ahead of the MFMAs that use them
+    constexpr int CG = (NT >= 8) ? 1 : (8 / NT);
+    constexpr int NG = (KS + CG - 1) / CG;
     f32x4 acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bool live[NT];
+    size_t rowo[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int r = nt * 16 + l16, b = row0 + r;
-      const bool live = (b < B) && (s_op[r] == 1);          // dA rows of non-push steps are zero
-      const size_t rowo = ((size_t)t * B + b) * H4 + (size_t)wave * H;
-#pragma unroll
-      for (int c = 0; c < KS; ++c) {
-        if (c >= ks_eff) continue;
-        const int kk = c * KC + (PREC ? 8 : 4) * lq;
-        if constexpr (PREC == 0) {
-          float4 bv = float4{0.f, 0.f, 0.f, 0.f};
-          if (live) {
-            const uint32_t off = (uint32_t)((rowo + kk) * 4);
-            if (vec_ok && kk + 3 < H) bv = __builtin_bit_cast(float4, ld_coh_b128(r_dA, off));
-            else {
-              bv.x = (kk < H) ? __uint_as_float(ld_coh_b32(r_dA, off)) : 0.f;
-              bv.y = (kk + 1 < H) ? __uint_as_float(ld_coh_b32(r_dA, off + 4)) : 0.f;
-              bv.z = (kk + 2 < H) ? __uint_as_float(ld_coh_b32(r_dA, off + 8)) : 0.f;
-              bv.w = (kk + 3 < H) ? __uint_as_float(ld_coh_b32(r_dA, off + 12)) : 0.f;
-            }
-          }
-          acc[nt] = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc[nt]);
-          acc[nt] = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc[nt]);
-          acc[nt] = mfma_f32_16x16x4(ureg32[c][2], bv.z, acc[nt]);
-          acc[nt] = mfma_f32_16x16x4(ureg32[c][3], bv.w, acc[nt]);
+      live[nt] = (b < B) && (s_op[r] == 1);              // dA rows of non-push steps are zero
+      rowo[nt] = ((size_t)t * B + (live[nt] ? b : 0)) * H4 + (size_t)wave * H;
+    }
+    auto fetch = [&](int c, int nt) -> uint4 {
+      uint4 raw = uint4{0u, 0u, 0u, 0u};
+      if (c >= ks_eff || !live[nt]) return raw;
+      const int kk = c * KC + (PREC ? 8 : 4) * lq;
+      const size_t el = rowo[nt] + kk;
+      if constexpr (PREC == 0) {
+        const uint32_t off = (uint32_t)(el * 4);
+        if (vec_ok && kk + 3 < H) {
+          raw = a.coh_rows ? ld_coh_b128(r_dA, off) : *(const uint4*)((const float*)a.dA + el);
         } else {
-          uint4 raw = uint4{0u, 0u, 0u, 0u};
-          if (live) {
-            const uint32_t off = (uint32_t)((rowo + kk) * 2);
-            if (vec_ok && kk + 7 < H) raw = ld_coh_b128(r_dA, off);
-            else {
-              bf16_t tmp[8];
-              for (int j = 0; j < 8; ++j) tmp[j] = (kk + j < H) ? ld_coh_b16(r_dA, off + 2 * j) : (bf16_t)0;
-              raw = *(const uint4*)tmp;
-            }
+          raw.x = (kk < H) ? ld_coh_b32(r_dA, off) : 0u;
+          raw.y = (kk + 1 < H) ? ld_coh_b32(r_dA, off + 4) : 0u;
+          raw.z = (kk + 2 < H) ? ld_coh_b32(r_dA, off + 8) : 0u;
+          raw.w = (kk + 3 < H) ? ld_coh_b32(r_dA, off + 12) : 0u;
+        }
+      } else {
+        const uint32_t off = (uint32_t)(el * 2);
+        if (vec_ok && kk + 7 < H) {
+          raw = a.coh_rows ? ld_coh_b128(r_dA, off) : *(const uint4*)((const bf16_t*)a.dA + el);
+        } else {
+          bf16_t tmp[8];
+          for (int j = 0; j < 8; ++j) tmp[j] = (kk + j < H) ? ld_coh_b16(r_dA, off + 2 * j) : (bf16_t)0;
+          raw = *(const uint4*)tmp;
+        }
+      }
+      return raw;
+    };
+    uint4 bufA[CG][NT], bufB[CG][NT];
+#pragma unroll
+    for (int j = 0; j < CG; ++j)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) bufA[j][nt] = fetch(j, nt);
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+      uint4 (&cur)[CG][NT] = (gi & 1) ? bufB : bufA;
+      uint4 (&nxt)[CG][NT] = (gi & 1) ? bufA : bufB;
+      if (gi + 1 < NG) {
+#pragma unroll
+        for (int j = 0; j < CG; ++j)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) nxt[j][nt] = fetch((gi + 1) * CG + j, nt);
+      }
+#pragma unroll
+      for (int j = 0; j < CG; ++j) {
+        const int c = gi * CG + j;
+        if (c >= KS || c >= ks_eff) continue;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          if constexpr (PREC == 0) {
+            const float4 bv = __builtin_bit_cast(float4, cur[j][nt]);
+            acc[nt] = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc[nt]);
+            acc[nt] = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc[nt]);
+            acc[nt] = mfma_f32_16x16x4(ureg32[c][2], bv.z, acc[nt]);
+            acc[nt] = mfma_f32_16x16x4(ureg32[c][3], bv.w, acc[nt]);
+          } else {
+            acc[nt] = mfma_bf16_16x16x32(ureg16[c], __builtin_bit_cast(bf16x8, cur[j][nt]), acc[nt]);
           }
-          acc[nt] = mfma_bf16_16x16x32(ureg16[c], __builtin_bit_cast(bf16x8, raw), acc[nt]);
         }
       }
     }
@@ -210,6 +245,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       a.dh_acc[((size_t)(s_src[r] + 1) * B + b) * H + u] += s;
     }
     __syncthreads();
+    if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
   }
 
   // ---- outputs of this workgroup: dh0, dc0 for its pairs; per-group bias gradient

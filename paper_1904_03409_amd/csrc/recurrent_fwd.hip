@@ -89,41 +89,37 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   if ((int)threadIdx.x < BG) s_src[threadIdx.x] = -1;
   if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)a.NW, a.ctl, a.spin_limit, &s_flag)) return;
 
+  long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
   for (int t = 0; t < T; ++t) {
+    if (clk && threadIdx.x == 0) clk[t * 4 + 0] = wall_clock64();
     // producer of the state each row reads at step t+1 (= top[t], written one step ago)
-    int src_next = -1;
-    if (row_thread && t + 1 < T) {
-      src_next = (int)ld_coh_b32(r_top, (uint32_t)(((size_t)t * B + my_row) * 4));
-      if (src_next < -1 || src_next > t) src_next = -1;   // only a valid producer is ever indexed
-    }
-    // trace for step t+1: stack[p+1] <- t+1, p <- p + op, top <- stack[p]
-    int tp_next = 0;
-    if (tracer && t + 1 < T) {
-      int op = op_next;
-      op_next = (t + 2 < T) ? a.ops[(size_t)(t + 2) * B + my_row] : 0;
-      a.stack[stk_base + my_p + 1] = t + 1;
-      my_p = max(0, my_p + op);
-      tp_next = (op == 1) ? t + 1 : (op == 0 ? my_top : a.stack[stk_base + my_p]);
-    }
+
+    int src_next = -1, tp_next = 0;
 
     for (int nb = 0; nb < NT / NTB; ++nb) {
       // ---- gather h_prev rows of this pass into LDS (zero beyond H and for rows past B)
       if (vec_ok) {
+        // every thread issues all of its loads before the first LDS write, so the
+        // latency of the L2 round trip is paid once per step, not once per vector
         constexpr int VW = PREC ? 8 : 4;
+        constexpr int NLD = (ROWS_B * (KP / VW) + 255) / 256;
         const int per_row = kmax / VW;
-        for (int e = threadIdx.x; e < ROWS_B * per_row; e += 256) {
-          int r = e / per_row, k = (e - r * per_row) * VW;
-          int rr = nb * ROWS_B + r, b = row0 + rr;
-          elem_t* dst = hs + r * LDS_LD + k;
-          if (b >= B || k >= H) {
-            if constexpr (PREC == 0) *(float4*)dst = float4{0.f, 0.f, 0.f, 0.f};
-            else *(uint4*)dst = uint4{0u, 0u, 0u, 0u};
-            continue;
-          }
-          int src = s_src[rr];
+        const int n_el = ROWS_B * per_row;
+        uint4 buf[NLD];
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+          const int e = threadIdx.x + 256 * i;
+          buf[i] = uint4{0u, 0u, 0u, 0u};
+          if (e >= n_el) continue;
+          const int r = e / per_row, k = (e - r * per_row) * VW;
+          const int rr = nb * ROWS_B + r, b = row0 + rr;
+          if (b >= B || k >= H) continue;
+          const int src = s_src[rr];
+          const size_t e2 = ((size_t)src * B + b) * H + k;
           if constexpr (PREC == 0) {
-            if (src < 0) *(float4*)dst = *(const float4*)(a.h0 + (size_t)b * H + k);
-            else *(uint4*)dst = ld_coh_b128(r_h, (uint32_t)((((size_t)src * B + b) * H + k) * 4));
+            if (src < 0) buf[i] = *(const uint4*)(a.h0 + (size_t)b * H + k);
+            else if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 4));
+            else buf[i] = *(const uint4*)(a.hcell + e2);
           } else {
             if (src < 0) {
               const float* p = a.h0 + (size_t)b * H + k;
@@ -131,11 +127,20 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
               bf16_t o[8] = {f32_to_bf16_bits(v0.x), f32_to_bf16_bits(v0.y), f32_to_bf16_bits(v0.z),
                              f32_to_bf16_bits(v0.w), f32_to_bf16_bits(v1.x), f32_to_bf16_bits(v1.y),
                              f32_to_bf16_bits(v1.z), f32_to_bf16_bits(v1.w)};
-              *(uint4*)dst = *(const uint4*)o;
+              buf[i] = *(const uint4*)o;
+            } else if (a.coh_rows) {
+              buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 2));
             } else {
-              *(uint4*)dst = ld_coh_b128(r_h, (uint32_t)((((size_t)src * B + b) * H + k) * 2));
+              buf[i] = *(const uint4*)(a.hx + e2);
             }
           }
+        }
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+          const int e = threadIdx.x + 256 * i;
+          if (e >= n_el) continue;
+          const int r = e / per_row, k = (e - r * per_row) * VW;
+          *(uint4*)(hs + r * LDS_LD + k) = buf[i];
         }
       } else {
         for (int e = threadIdx.x; e < ROWS_B * kmax; e += 256) {
@@ -154,6 +159,20 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         }
       }
       __syncthreads();
+      if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 1] = wall_clock64();
+      if (nb == 0 && row_thread && t + 1 < T) {
+        const size_t o = (size_t)t * B + my_row;
+        src_next = a.coh_top ? (int)ld_coh_b32(r_top, (uint32_t)(o * 4)) : a.top[o];
+      }
+      // trace for step t+1: stack[p+1] <- t+1, p <- p + op, top <- stack[p]; issued after the
+      // h_prev loads so that their wait does not include it, consumed before the barrier
+      if (nb == 0 && tracer && t + 1 < T) {
+        int op = op_next;
+        op_next = (t + 2 < T) ? a.ops[(size_t)(t + 2) * B + my_row] : 0;
+        a.stack[stk_base + my_p + 1] = t + 1;
+        my_p = max(0, my_p + op);
+        tp_next = (op == 1) ? t + 1 : (op == 0 ? my_top : a.stack[stk_base + my_p]);
+      }
 
       // ---- epilogue operands, fetched before the MFMA loop so their latency overlaps it
       const int u = unit_base + lq;
@@ -194,6 +213,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         }
       }
 
+      if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 2] = wall_clock64();
       // ---- fused LSTM cell: lane holds gates i, f, g, o of unit u for row l16 of each tile
 #pragma unroll
       for (int nt = 0; nt < NTB; ++nt) {
@@ -214,11 +234,13 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       if (NT / NTB > 1) __syncthreads();
     }
 
+    if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
     if (tracer && t + 1 < T) {
       a.top[(size_t)(t + 1) * B + my_row] = tp_next;
       my_top = tp_next;
     }
     if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_flag)) break;
+    if (src_next < -1 || src_next > t) src_next = -1;   // only a valid producer is ever indexed
     if ((int)threadIdx.x < BG) s_src[threadIdx.x] = src_next;
     __syncthreads();
   }
