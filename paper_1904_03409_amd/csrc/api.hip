@@ -19,6 +19,10 @@ __global__ void k_gather_top(const int32_t* top, const float* cellv, const float
 __global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
+__global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
+__global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
+__global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const bf16_t* hx, void* out,
+                               int T, int B, int H);
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
@@ -26,7 +30,7 @@ __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride,
 namespace {
 
 constexpr int kDefaultSpin = 1 << 22;
-constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 32;
+constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 64;
 
 struct DevInfo { int cus; bool ok; };
 
@@ -53,7 +57,7 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, dh, dc, dbp, part, total;
+  size_t ctl, stack, wp, r1, stash, hx, xb, hp, dh, dc, dbp, part, total;
 };
 
 bool dims_ok(const slstm_dims* d) {
@@ -129,7 +133,9 @@ Layout layout(const slstm_dims* d) {
   L.wp = o; o += align256(I * 4 * H * 4);
   L.r1 = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));   // XW (forward), dA (backward)
   L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
-  L.hx = o; o += bf ? align256(T * B * H * 2) : 0;
+  L.hx = o; o += bf ? align256((T + 1) * B * H * 2) : 0;
+  L.xb = o; o += bf ? align256(T * B * I * 2) : 0;                    // x in bf16 (bf16 mode)
+  L.hp = o; o += align256(std::max<size_t>(T * B * H * (bf ? 2 : 4), 16));   // Hprev rows
   L.dh = o; o += align256((T + 1) * B * H * 4);
   L.dc = o; o += align256((T + 1) * B * H * 4);
   L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
@@ -157,11 +163,14 @@ int launch_gemm(int prec, int AL, int BL, const GemmArgs& g, int splits, hipStre
     hipLaunchKernelGGL((k_gemm<P, A, B_>), grid, dim3(256), 0, st, g);        \
     return hip_status(hipGetLastError());                                     \
   }
-  GCASE(0, GEMM_MK, GEMM_KN) GCASE(0, GEMM_MK, GEMM_NK) GCASE(0, GEMM_KM, GEMM_KN) GCASE(0, GEMM_KM_GATHER, GEMM_KN)
-  GCASE(1, GEMM_MK, GEMM_KN) GCASE(1, GEMM_MK, GEMM_NK) GCASE(1, GEMM_KM, GEMM_KN) GCASE(1, GEMM_KM_GATHER, GEMM_KN)
+  GCASE(0, GEMM_MK, GEMM_KN) GCASE(0, GEMM_MK, GEMM_NK) GCASE(0, GEMM_KM, GEMM_KN)
+  GCASE(1, GEMM_MK, GEMM_KN) GCASE(1, GEMM_MK, GEMM_NK) GCASE(1, GEMM_KM, GEMM_KN)
 #undef GCASE
   return SLSTM_EINVAL;
 }
+
+// K slice per split, a multiple of the GEMM's K tile (64 covers both precisions)
+int k_chunk_for(int K, int splits) { return ((K + splits - 1) / splits + 63) / 64 * 64; }
 
 int check_timeout(const uint32_t* ctl, hipStream_t st) {
   uint32_t v = 0;
@@ -256,18 +265,25 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W,
                      bf ? nullptr : (float*)wp, bf ? (bf16_t*)wp : nullptr, I, H);
   float* xw = (float*)(ws + L.r1);
+  const void* xa = x;
+  if (bf) {
+    hipLaunchKernelGGL(k_to_bf16, dim3(grid1d((size_t)T * B * I)), dim3(256), 0, st, x, (bf16_t*)(ws + L.xb),
+                       (size_t)T * B * I);
+    xa = ws + L.xb;
+  }
   GemmArgs g;
   memset(&g, 0, sizeof(g));
   g.M = T * B; g.N = 4 * H; g.K = I;
-  g.A = x; g.lda = I; g.a_bf16 = 0; g.a_vec = (I % 4 == 0);
-  g.Bm = wp; g.ldb = 4 * H; g.b_bf16 = bf; g.b_vec = 1;
+  g.A = xa; g.lda = I; g.a_vec = (I % (bf ? 8 : 4) == 0);
+  g.Bm = wp; g.ldb = 4 * H; g.b_vec = (H % 2 == 0) || !bf;
   g.C = xw; g.ldc = 4 * H; g.bias = b; g.bias_H = H;
-  g.k_chunk = ((I + kGemmBK - 1) / kGemmBK) * kGemmBK; g.split_stride = 0;
+  g.k_chunk = k_chunk_for(I, 1); g.split_stride = 0;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_KN, g, 1, st))) return rc;
   mark(d, 2, st);
 
   // a3-a6: persistent recurrent kernel
   RecArgs a = rec_args(d, p, ws, L);
+  if (bf) hipLaunchKernelGGL(k_h0_bf16, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, h0, (bf16_t*)a.hx, (size_t)B * H);
   a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
   if ((rc = hip_status(launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
   mark(d, 3, st);
@@ -333,42 +349,46 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H4)), dim3(256), 0, st, a.db_part, p.G, (size_t)H4, 1, H4,
                      H, db);
   const int K = T * B;
+  const size_t esz = bf ? 2 : 4;
+  const void* xa = bf ? (const void*)(ws + L.xb) : (const void*)x;
   GemmArgs g;
   // dW = x^T dA
   memset(&g, 0, sizeof(g));
   g.M = I; g.N = H4; g.K = K;
-  g.A = x; g.lda = I; g.a_bf16 = 0; g.a_vec = (I % 4 == 0);
-  g.Bm = a.dA; g.ldb = H4; g.b_bf16 = bf; g.b_vec = 1;
+  g.A = xa; g.lda = I; g.a_vec = (I % (bf ? 8 : 4) == 0);
+  g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % (bf ? 8 : 4) == 0);
   g.C = part; g.ldc = H4;
-  g.k_chunk = ((K + p.splits_w - 1) / p.splits_w + kGemmBK - 1) / kGemmBK * kGemmBK;
+  g.k_chunk = k_chunk_for(K, p.splits_w);
   int sw = (K + g.k_chunk - 1) / g.k_chunk;
   g.split_stride = (size_t)I * H4;
   if ((rc = launch_gemm(p.prec, GEMM_KM, GEMM_KN, g, sw, st))) return rc;
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, sw, g.split_stride, I,
                      H4, H, dW);
   mark(d, 7, st);
-  // dU = Hprev^T dA, Hprev rows gathered through the producer table
+  // dU = Hprev^T dA, Hprev = the state each step read (gathered through the producer table)
+  void* hp = ws + L.hp;
+  hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0,
+                     bf ? (const bf16_t*)(ws + L.hx) : (const bf16_t*)nullptr, hp, T, B, H);
   memset(&g, 0, sizeof(g));
   g.M = H; g.N = H4; g.K = K;
-  g.A = nullptr; g.a_bf16 = 0; g.a_vec = (H % 4 == 0);
-  g.gtop = top; g.gh0 = h0; g.gcell = bf ? (const void*)(ws + L.hx) : (const void*)h_cell; g.gcell_bf16 = bf;
-  g.gB = B; g.gH = H;
-  g.Bm = a.dA; g.ldb = H4; g.b_bf16 = bf; g.b_vec = 1;
+  g.A = hp; g.lda = H; g.a_vec = (H % (bf ? 8 : 4) == 0);
+  g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % (bf ? 8 : 4) == 0);
   g.C = part; g.ldc = H4;
-  g.k_chunk = ((K + p.splits_u - 1) / p.splits_u + kGemmBK - 1) / kGemmBK * kGemmBK;
+  g.k_chunk = k_chunk_for(K, p.splits_u);
   int su = (K + g.k_chunk - 1) / g.k_chunk;
   g.split_stride = (size_t)H * H4;
-  if ((rc = launch_gemm(p.prec, GEMM_KM_GATHER, GEMM_KN, g, su, st))) return rc;
+  if ((rc = launch_gemm(p.prec, GEMM_KM, GEMM_KN, g, su, st))) return rc;
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, su, g.split_stride, H,
                      H4, H, dU);
   mark(d, 8, st);
   // dx = dA Wp^T
   memset(&g, 0, sizeof(g));
   g.M = K; g.N = I; g.K = H4;
-  g.A = a.dA; g.lda = H4; g.a_bf16 = bf; g.a_vec = 1;
-  g.Bm = ws + L.wp; g.ldb = H4; g.b_bf16 = bf; g.b_vec = 1;
+  g.A = a.dA; g.lda = H4; g.a_vec = (H4 % (bf ? 8 : 4) == 0);
+  g.Bm = ws + L.wp; g.ldb = H4; g.b_vec = (H4 % (bf ? 8 : 4) == 0);
   g.C = dx; g.ldc = I;
-  g.k_chunk = ((H4 + kGemmBK - 1) / kGemmBK) * kGemmBK;
+  g.k_chunk = k_chunk_for(H4, 1);
+  (void)esz;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, 1, st))) return rc;
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 9, st);

@@ -3,16 +3,14 @@
 #include <stddef.h>
 #include <stdint.h>
 
-enum { GEMM_MK = 0, GEMM_KM = 1, GEMM_KM_GATHER = 2 };  // A layouts
-enum { GEMM_KN = 0, GEMM_NK = 1 };                       // B layouts
+enum { GEMM_MK = 0, GEMM_KM = 1 };   // A layouts: A(m,k) = A[m*lda+k] or A[k*lda+m]
+enum { GEMM_KN = 0, GEMM_NK = 1 };   // B layouts: B(k,n) = B[k*ldb+n] or B[n*ldb+k]
 
 struct GemmArgs {
   int M, N, K;
-  const void* A; int lda; int a_bf16; int a_vec;   // A(m,k): MK -> A[m*lda+k]; KM -> A[k*lda+m]
-  const void* Bm; int ldb; int b_bf16; int b_vec;  // B(k,n): KN -> B[k*ldb+n]; NK -> B[n*ldb+k]
-  float* C; int ldc;                               // C[m*ldc+n] (+ split index * split_stride)
-  const float* bias; int bias_H;                   // + bias[caller column of n] when non-null
+  const void* A; int lda; int a_vec;   // a_vec: rows are 16-byte aligned vectors (ld % 4 (fp32) / % 8 (bf16) == 0)
+  const void* Bm; int ldb; int b_vec;
+  float* C; int ldc;                   // C[m*ldc+n] (+ split index * split_stride)
+  const float* bias; int bias_H;       // + bias[caller column of n] when non-null
   int k_chunk; size_t split_stride;
-  // KM_GATHER: row k = t*B + b of A is the state read at step t by element b
-  const int32_t* gtop; const float* gh0; const void* gcell; int gcell_bf16; int gB; int gH;
 };

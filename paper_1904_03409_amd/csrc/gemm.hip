@@ -1,164 +1,196 @@
 // Tiled MFMA GEMM for the non-recurrent contractions of the StackLSTM step:
-//   XW  = x Wp + b          (input projection for all T steps at once; paper, Algorithm 1's
-//                            LSTM(x_t, .) has an x_t part independent of the recurrence)
-//   dx  = dA Wp^T           (input gradient)
-//   dW  = x^T dA            (weight gradients, split over K = T*B with fixed-order reduction)
-//   dU  = Hprev^T dA        (Hprev rows gathered through the producer table)
-// C[M][N] = sum_k A(m, k) B(k, n). 128x128 block tile, 32-deep K slices staged in LDS,
-// four waves of 64x64, v_mfma_f32_16x16x4f32 (fp32) or v_mfma_f32_16x16x32_bf16.
+//   XW = x Wp + b     (input projection for all T steps at once: the x_t part of the cell's
+//                      pre-activation does not depend on the recurrence)
+//   dx = dA Wp^T      dW = x^T dA      dU = Hprev^T dA   (Hprev = the state each step read)
+// C[M][N] = sum_k A(m, k) B(k, n); A stored MK (A[m*lda+k]) or KM (A[k*lda+m]); B stored KN
+// (B[k*ldb+n]) or NK (B[n*ldb+k]). Both operands share one element type: fp32
+// (v_mfma_f32_16x16x4f32) or bf16 (v_mfma_f32_16x16x32_bf16), fp32 accumulation.
+// 128x128 block tile, four 64x64 wave tiles, K slices of BK; the next slice is fetched
+// into registers while the current one is multiplied (two LDS buffers, one barrier per
+// slice). Split K writes partials that k_reduce_splits adds in a fixed order.
 #include "common.h"
 #include "gemm.h"
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int BM = 128, BN = 128;
+template <int P> struct Cfg;
+// fp32: LDS tiles keep the global layout (k-contiguous rows read as 4-wide vectors,
+// m/n-contiguous rows read one value per MFMA step); 32-deep K slices.
+template <> struct Cfg<0> { using T = float; static constexpr int BK = 32; static constexpr int VE = 4; };
+// bf16: LDS tiles are always [m][k] / [n][k] so a lane reads its 8 consecutive k at once;
+// m/n-contiguous operands are transposed while being written to LDS. 64-deep K slices.
+template <> struct Cfg<1> { using T = bf16_t; static constexpr int BK = 64; static constexpr int VE = 8; };
 
-template <int PREC> struct Lds;
-template <> struct Lds<0> { using T = float; static constexpr int PAD = 4; };
-template <> struct Lds<1> { using T = bf16_t; static constexpr int PAD = 8; };
+// LDS geometry of one operand tile (elements): rows x (cols + pad)
+template <int P, bool KMAJOR> struct Geo {
+  static constexpr int BK = Cfg<P>::BK;
+  // fp32 k-major tile stored [k][m]: BK rows of 128 (+4); otherwise [m][k]: 128 rows of BK (+pad)
+  static constexpr bool KROWS = (P == 0) && KMAJOR;
+  static constexpr int ROWS = KROWS ? BK : 128;
+  static constexpr int LD = KROWS ? (128 + 16) : (BK + (P ? 8 : 4));   // pads keep fragment reads conflict-free
+  static constexpr int ELEMS = ROWS * LD;
+};
 
-__device__ __forceinline__ float ld_any(const void* p, size_t i, int src_bf16) {
-  return src_bf16 ? bf16_bits_to_f32(((const bf16_t*)p)[i]) : ((const float*)p)[i];
-}
+// Register staging of one operand tile: NV vectors of VE elements per thread.
+template <int P, bool KMAJOR> struct Stage {
+  using T = typename Cfg<P>::T;
+  static constexpr int BK = Cfg<P>::BK, VE = Cfg<P>::VE;
+  static constexpr int NV = 128 * BK / VE / 256;
+  uint4 v[NV];
 
-template <int PREC>
-__device__ __forceinline__ void st_lds(typename Lds<PREC>::T* s, float v) {
-  if constexpr (PREC == 0) *s = v; else *s = f32_to_bf16_bits(v);
-}
-
-// Loads 4 consecutive elements p[i..i+3] (bounded by lim) as floats.
-__device__ __forceinline__ void ld4(const void* p, size_t i, size_t lim, int src_bf16, bool vec_ok, float v[4]) {
-  if (vec_ok && i + 3 < lim) {
-    if (src_bf16) {
-      uint2 r = *(const uint2*)((const bf16_t*)p + i);
-      v[0] = __uint_as_float(r.x << 16); v[1] = __uint_as_float(r.x & 0xffff0000u);
-      v[2] = __uint_as_float(r.y << 16); v[3] = __uint_as_float(r.y & 0xffff0000u);
-    } else {
-      float4 r = *(const float4*)((const float*)p + i);
-      v[0] = r.x; v[1] = r.y; v[2] = r.z; v[3] = r.w;
-    }
-  } else {
-    for (int j = 0; j < 4; ++j) v[j] = (i + j < lim) ? ld_any(p, i + j, src_bf16) : 0.f;
-  }
-}
-
-// Base of row tb of Hprev: the state read at step t = tb / B by element b = tb % B.
-__device__ __forceinline__ const void* gather_row(const GemmArgs& g, int tb, int* is_bf16) {
-  int t = tb / g.gB, b = tb - t * g.gB;
-  int src = (t == 0) ? -1 : g.gtop[(size_t)(t - 1) * g.gB + b];
-  if (src >= t) src = -1;                       // a producer precedes its reader; guard bad tables
-  if (src < 0) { *is_bf16 = 0; return g.gh0 + (size_t)b * g.gH; }
-  *is_bf16 = g.gcell_bf16;
-  return g.gcell_bf16 ? (const void*)((const bf16_t*)g.gcell + ((size_t)src * g.gB + b) * g.gH)
-                      : (const void*)((const float*)g.gcell + ((size_t)src * g.gB + b) * g.gH);
-}
-
-// Stage A(m0.., k0..) into As[m][k] and B(k0.., n0..) into Bs[n][k].
-template <int PREC, int AL, int BL>
-__device__ __forceinline__ void stage(const GemmArgs& g, int m0, int n0, int k0, int kend,
-                                      typename Lds<PREC>::T* As, typename Lds<PREC>::T* Bs) {
-  constexpr int LD = BK + Lds<PREC>::PAD;
-  const int tid = threadIdx.x;
-  // A
-  for (int e = tid; e < BM * BK / 4; e += 256) {
-    float v[4];
-    if (AL == GEMM_MK) {
-      int m = e / (BK / 4), k4 = (e % (BK / 4)) * 4;
-      int gm = m0 + m, gk = k0 + k4;
-      if (gm < g.M && gk < kend) {
-        ld4(g.A, (size_t)gm * g.lda + gk, (size_t)gm * g.lda + kend, g.a_bf16, g.a_vec, v);
-      } else { v[0] = v[1] = v[2] = v[3] = 0.f; }
-      for (int j = 0; j < 4; ++j) st_lds<PREC>(&As[m * LD + k4 + j], v[j]);
-    } else {
-      int k = e / (BM / 4), m4 = (e % (BM / 4)) * 4;
-      int gk = k0 + k, gm = m0 + m4;
-      if (gk < kend && gm < g.M) {
-        if (AL == GEMM_KM) {
-          ld4(g.A, (size_t)gk * g.lda + gm, (size_t)gk * g.lda + g.M, g.a_bf16, g.a_vec, v);
+  // global tile element (r, c): KMAJOR -> row r in [0,BK) of k, col c in [0,128) of m/n;
+  // otherwise row r in [0,128) of m/n, col c in [0,BK) of k
+  __device__ __forceinline__ void load(const T* __restrict__ base, int ld, int r0, int rlim, int c0, int clim,
+                                       bool vec) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      int r, c;
+      if (KMAJOR) { r = e / (128 / VE); c = (e % (128 / VE)) * VE; }
+      else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
+      const int gr = r0 + r, gc = c0 + c;
+      uint4 x = uint4{0u, 0u, 0u, 0u};
+      if (gr < rlim) {
+        const T* p = base + (size_t)gr * ld + gc;
+        if (vec && gc + VE <= clim) {
+          x = *(const uint4*)p;
         } else {
-          int rb;
-          const void* row = gather_row(g, gk, &rb);
-          ld4(row, (size_t)gm, (size_t)g.M, rb, g.a_vec, v);
+          T tmp[VE];
+#pragma unroll
+          for (int j = 0; j < VE; ++j) tmp[j] = (gc + j < clim) ? p[j] : (T)0;
+          x = *(const uint4*)tmp;
         }
-      } else { v[0] = v[1] = v[2] = v[3] = 0.f; }
-      for (int j = 0; j < 4; ++j) st_lds<PREC>(&As[(m4 + j) * LD + k], v[j]);
+      }
+      v[i] = x;
     }
   }
-  // B
-  for (int e = tid; e < BN * BK / 4; e += 256) {
-    float v[4];
-    if (BL == GEMM_NK) {
-      int n = e / (BK / 4), k4 = (e % (BK / 4)) * 4;
-      int gn = n0 + n, gk = k0 + k4;
-      if (gn < g.N && gk < kend) {
-        ld4(g.Bm, (size_t)gn * g.ldb + gk, (size_t)gn * g.ldb + kend, g.b_bf16, g.b_vec, v);
-      } else { v[0] = v[1] = v[2] = v[3] = 0.f; }
-      for (int j = 0; j < 4; ++j) st_lds<PREC>(&Bs[n * LD + k4 + j], v[j]);
-    } else {
-      int k = e / (BN / 4), n4 = (e % (BN / 4)) * 4;
-      int gk = k0 + k, gn = n0 + n4;
-      if (gk < kend && gn < g.N) {
-        ld4(g.Bm, (size_t)gk * g.ldb + gn, (size_t)gk * g.ldb + g.N, g.b_bf16, g.b_vec, v);
-      } else { v[0] = v[1] = v[2] = v[3] = 0.f; }
-      for (int j = 0; j < 4; ++j) st_lds<PREC>(&Bs[(n4 + j) * LD + k], v[j]);
+
+  __device__ __forceinline__ void store(T* __restrict__ s) const {
+    using G = Geo<P, KMAJOR>;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      if (KMAJOR) {
+        const int r = e / (128 / VE), c = (e % (128 / VE)) * VE;   // r = k, c = m
+        if (G::KROWS) {
+          *(uint4*)&s[r * G::LD + c] = v[i];
+        } else {                                                    // bf16: transpose to [m][k]
+          const bf16_t* h = (const bf16_t*)&v[i];
+#pragma unroll
+          for (int j = 0; j < VE; ++j) s[(c + j) * G::LD + r] = h[j];
+        }
+      } else {
+        const int r = e / (BK / VE), c = (e % (BK / VE)) * VE;     // r = m, c = k
+        *(uint4*)&s[r * G::LD + c] = v[i];
+      }
     }
   }
-}
+};
 
 }  // namespace
 
-template <int PREC, int AL, int BL>
-__global__ void __launch_bounds__(256) k_gemm(GemmArgs g) {
-  using T = typename Lds<PREC>::T;
-  constexpr int LD = BK + Lds<PREC>::PAD;
-  __shared__ __align__(16) T As[BM * LD];
-  __shared__ __align__(16) T Bs[BN * LD];
+template <int P, int AL, int BL>
+__global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
+  using T = typename Cfg<P>::T;
+  constexpr int BK = Cfg<P>::BK;
+  constexpr bool AKM = (AL == GEMM_KM), BKN = (BL == GEMM_KN);
+  using GA = Geo<P, AKM>;
+  using GB = Geo<P, BKN>;
+  __shared__ __align__(16) T As[2][GA::ELEMS];
+  __shared__ __align__(16) T Bs[2][GB::ELEMS];
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kz = blockIdx.z;
-  const int kbeg = kz * g.k_chunk;
+  const int kbeg = blockIdx.z * g.k_chunk;
   const int kend = min(g.K, kbeg + g.k_chunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int l16 = lane & 15, lq = lane >> 4;
+  const T* A = (const T*)g.A;
+  const T* Bp = (const T*)g.Bm;
+
+  Stage<P, AKM> sa;
+  Stage<P, BKN> sb;
+  auto fetch = [&](int k0) {
+    if (AKM) sa.load(A, g.lda, k0, kend, m0, g.M, g.a_vec);
+    else     sa.load(A, g.lda, m0, g.M, k0, kend, g.a_vec);
+    if (BKN) sb.load(Bp, g.ldb, k0, kend, n0, g.N, g.b_vec);
+    else     sb.load(Bp, g.ldb, n0, g.N, k0, kend, g.b_vec);
+  };
+
   f32x4 acc[4][4];
+#pragma unroll
   for (int i = 0; i < 4; ++i)
+#pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  int buf = 0;
+  if (kbeg < kend) {
+    fetch(kbeg);
+    sa.store(As[0]);
+    sb.store(Bs[0]);
+  }
+  __syncthreads();
   for (int k0 = kbeg; k0 < kend; k0 += BK) {
-    __syncthreads();
-    stage<PREC, AL, BL>(g, m0, n0, k0, kend, As, Bs);
-    __syncthreads();
-    if constexpr (PREC == 0) {
-      for (int kc = 0; kc < BK / 16; ++kc) {
-        float4 a4[4], b4[4];
-        for (int i = 0; i < 4; ++i) a4[i] = *(const float4*)&As[(wm * 64 + i * 16 + l16) * LD + kc * 16 + 4 * lq];
-        for (int j = 0; j < 4; ++j) b4[j] = *(const float4*)&Bs[(wn * 64 + j * 16 + l16) * LD + kc * 16 + 4 * lq];
+    const bool more = k0 + BK < kend;
+    if (more) fetch(k0 + BK);                       // next slice in flight during this one
+    const T* as = As[buf];
+    const T* bs = Bs[buf];
+    if constexpr (P == 0) {
+#pragma unroll
+      for (int kc = 0; kc < BK / 4; ++kc) {
+        // one MFMA k-step covers k = 4*kc + lq (A and B use the same k for a lane)
+        float av[4], bv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = wm * 64 + i * 16 + l16;
+          if (AKM) av[i] = as[(4 * kc + lq) * GA::LD + m];
+          else     av[i] = as[m * GA::LD + 4 * kc + lq];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = wn * 64 + j * 16 + l16;
+          if (BKN) bv[j] = bs[(4 * kc + lq) * GB::LD + n];
+          else     bv[j] = bs[n * GB::LD + 4 * kc + lq];
+        }
+#pragma unroll
         for (int i = 0; i < 4; ++i)
-          for (int j = 0; j < 4; ++j) {
-            acc[i][j] = mfma_f32_16x16x4(a4[i].x, b4[j].x, acc[i][j]);
-            acc[i][j] = mfma_f32_16x16x4(a4[i].y, b4[j].y, acc[i][j]);
-            acc[i][j] = mfma_f32_16x16x4(a4[i].z, b4[j].z, acc[i][j]);
-            acc[i][j] = mfma_f32_16x16x4(a4[i].w, b4[j].w, acc[i][j]);
-          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32_16x16x4(av[i], bv[j], acc[i][j]);
       }
     } else {
-      bf16x8 a8[4], b8[4];
-      for (int i = 0; i < 4; ++i) a8[i] = *(const bf16x8*)&As[(wm * 64 + i * 16 + l16) * LD + 8 * lq];
-      for (int j = 0; j < 4; ++j) b8[j] = *(const bf16x8*)&Bs[(wn * 64 + j * 16 + l16) * LD + 8 * lq];
-      for (int i = 0; i < 4; ++i)
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16_16x16x32(a8[i], b8[j], acc[i][j]);
+#pragma unroll
+      for (int kc = 0; kc < BK / 32; ++kc) {
+        bf16x8 a8[4], b8[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a8[i] = *(const bf16x8*)&as[(wm * 64 + i * 16 + l16) * GA::LD + kc * 32 + 8 * lq];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b8[j] = *(const bf16x8*)&bs[(wn * 64 + j * 16 + l16) * GB::LD + kc * 32 + 8 * lq];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16_16x16x32(a8[i], b8[j], acc[i][j]);
+      }
     }
+    if (more) {
+      sa.store(As[buf ^ 1]);
+      sb.store(Bs[buf ^ 1]);
+    }
+    __syncthreads();
+    buf ^= 1;
   }
 
   // epilogue: lane holds rows 4*lq + r, column l16 of each 16x16 tile
-  float* C = g.C + (size_t)kz * g.split_stride;
+  float* C = g.C + (size_t)blockIdx.z * g.split_stride;
+#pragma unroll
   for (int i = 0; i < 4; ++i)
+#pragma unroll
     for (int j = 0; j < 4; ++j) {
-      int n = n0 + wn * 64 + j * 16 + l16;
+      const int n = n0 + wn * 64 + j * 16 + l16;
       if (n >= g.N) continue;
-      float bv = g.bias ? g.bias[perm_to_orig(n, g.bias_H)] : 0.f;
+      const float bv = g.bias ? g.bias[perm_to_orig(n, g.bias_H)] : 0.f;
+#pragma unroll
       for (int r = 0; r < 4; ++r) {
-        int m = m0 + wm * 64 + i * 16 + 4 * lq + r;
+        const int m = m0 + wm * 64 + i * 16 + 4 * lq + r;
         if (m < g.M) C[(size_t)m * g.ldc + n] = acc[i][j][r] + bv;
       }
     }
@@ -182,8 +214,6 @@ __global__ void __launch_bounds__(256) k_reduce_splits(const float* __restrict__
 INST(0, GEMM_MK, GEMM_KN)
 INST(0, GEMM_MK, GEMM_NK)
 INST(0, GEMM_KM, GEMM_KN)
-INST(0, GEMM_KM_GATHER, GEMM_KN)
 INST(1, GEMM_MK, GEMM_KN)
 INST(1, GEMM_MK, GEMM_NK)
 INST(1, GEMM_KM, GEMM_KN)
-INST(1, GEMM_KM_GATHER, GEMM_KN)

@@ -17,7 +17,7 @@ struct RecArgs {
   const float* c0;       // [B][H]
   float* hcell;          // [T][B][H]  state computed at step t (written to slot p+1)
   float* ccell;          // [T][B][H]
-  uint16_t* hx;          // [T][B][H]  bf16 copy of hcell (bf16-GEMM mode)
+  uint16_t* hx;          // [T+1][B][H] bf16 copies: slot 0 = h0, slot t+1 = hcell[t] (bf16-GEMM mode)
   float* stash;          // [T][B][4H] gate activations i, f, g, o, gate-interleaved
   int32_t* top;          // [T][B]     producer step of the state returned at step t (-1 = initial)
   int32_t* stack;        // [B][T+1]   step index written to each stack slot

@@ -37,7 +37,8 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   const int l16 = lane & 15, lq = lane >> 4;
   const int row0 = g * BG;
   const int ks_eff = a.ks_eff;
-  const rsrc_t r_dA = make_rsrc(a.dA, (size_t)T * B * H4 * (PREC ? 2 : 4));
+  constexpr int ESZ = PREC ? 2 : 4;
+  const rsrc_t r_dA = make_rsrc(a.dA, (size_t)T * B * H4 * ESZ);
 
   // ---- U^T slice: A(m = unit 16w + l16, k = gate column q*H + kk) = U[unit][caller column]
   const int a_unit = w * 16 + l16;
@@ -170,29 +171,28 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       live[nt] = (b < B) && (s_op[r] == 1);              // dA rows of non-push steps are zero
       rowo[nt] = ((size_t)t * B + (live[nt] ? b : 0)) * H4 + (size_t)wave * H;
     }
+    // Branch-free fragment loads through the bounds-checked descriptor: a lane whose row
+    // is not a push (its dA row is exactly 0) or whose k is past H gets an offset beyond
+    // the buffer, which returns 0 without a memory access.
+    const uint32_t kOOB = 0xffffffffu;
     auto fetch = [&](int c, int nt) -> uint4 {
-      uint4 raw = uint4{0u, 0u, 0u, 0u};
-      if (c >= ks_eff || !live[nt]) return raw;
       const int kk = c * KC + (PREC ? 8 : 4) * lq;
       const size_t el = rowo[nt] + kk;
+      if (vec_ok) {
+        const uint32_t off = (live[nt] && kk < H) ? (uint32_t)(el * ESZ) : kOOB;
+        if (a.coh_rows) return ld_coh_b128(r_dA, off);
+        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r_dA, off, 0, 0));
+      }
+      uint4 raw;
+      uint32_t* rw = (uint32_t*)&raw;
       if constexpr (PREC == 0) {
-        const uint32_t off = (uint32_t)(el * 4);
-        if (vec_ok && kk + 3 < H) {
-          raw = a.coh_rows ? ld_coh_b128(r_dA, off) : *(const uint4*)((const float*)a.dA + el);
-        } else {
-          raw.x = (kk < H) ? ld_coh_b32(r_dA, off) : 0u;
-          raw.y = (kk + 1 < H) ? ld_coh_b32(r_dA, off + 4) : 0u;
-          raw.z = (kk + 2 < H) ? ld_coh_b32(r_dA, off + 8) : 0u;
-          raw.w = (kk + 3 < H) ? ld_coh_b32(r_dA, off + 12) : 0u;
-        }
+        for (int j = 0; j < 4; ++j)
+          rw[j] = ld_coh_b32(r_dA, (live[nt] && kk + j < H) ? (uint32_t)((el + j) * 4) : kOOB);
       } else {
-        const uint32_t off = (uint32_t)(el * 2);
-        if (vec_ok && kk + 7 < H) {
-          raw = a.coh_rows ? ld_coh_b128(r_dA, off) : *(const uint4*)((const bf16_t*)a.dA + el);
-        } else {
-          bf16_t tmp[8];
-          for (int j = 0; j < 8; ++j) tmp[j] = (kk + j < H) ? ld_coh_b16(r_dA, off + 2 * j) : (bf16_t)0;
-          raw = *(const uint4*)tmp;
+        for (int j = 0; j < 4; ++j) {
+          uint32_t lo = ld_coh_b16(r_dA, (live[nt] && kk + 2 * j < H) ? (uint32_t)((el + 2 * j) * 2) : kOOB);
+          uint32_t hi = ld_coh_b16(r_dA, (live[nt] && kk + 2 * j + 1 < H) ? (uint32_t)((el + 2 * j + 1) * 2) : kOOB);
+          rw[j] = lo | (hi << 16);
         }
       }
       return raw;
@@ -215,7 +215,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
 #pragma unroll
       for (int j = 0; j < CG; ++j) {
         const int c = gi * CG + j;
-        if (c >= KS || c >= ks_eff) continue;
+        if (c >= KS) continue;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           if constexpr (PREC == 0) {

@@ -12,6 +12,12 @@
 // nonlinearities and the cell update in registers, writes h, c, the bf16 copy of h
 // and the gate activations, and meets the group at a barrier. Workgroup 0 of the
 // group also keeps the integer stack: stack[b][p+1] <- t, p <- p + op, top <- stack[b][p].
+//
+// Latency schedule of one step: the h_prev rows go straight from L2 into LDS
+// (global_load_lds, whole 1 KB row segments per wave instruction) when the row length
+// allows it; the input projection of the next step, the producer indices of the next
+// step and, once those are known, the c_prev values of the next step are fetched
+// while this step computes, so the epilogue works from registers only.
 #include "common.h"
 #include "recurrent.h"
 #include "rec_config.h"
@@ -20,9 +26,12 @@ template <int PREC, int NT, int NTB, int KS, int OCC>
 __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;               // K per chunk
   constexpr int KP = KS * KC;                      // K capacity of the U registers
-  constexpr int LDS_LD = KP + (PREC ? 8 : 4);      // LDS row stride (elements)
+  constexpr int ESZ = PREC ? 2 : 4;                // bytes per staged element
+  constexpr int LDS_LD = KP + (PREC ? 8 : 4);      // LDS row stride (elements): 16-byte pad
   constexpr int ROWS_B = NTB * 16;                 // rows staged per pass
+  constexpr int NPASS = NT / NTB;
   constexpr int BG = NT * 16;                      // rows per group
+  typedef __attribute__((address_space(3))) void* lds_ptr_t;
   using elem_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
   extern __shared__ __align__(16) unsigned char smem[];
   elem_t* hs = reinterpret_cast<elem_t*>(smem);
@@ -38,10 +47,13 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   const int l16 = lane & 15, lq = lane >> 4;
   const int row0 = g * BG;
   const int unit_base = w * 16 + wave * 4;
+  const int u = unit_base + lq;                    // epilogue unit of this lane
   const int ks_eff = a.ks_eff;
   const size_t TBH = (size_t)T * B * H;
   const rsrc_t r_top = make_rsrc(a.top, (size_t)T * B * 4);
-  const rsrc_t r_h = PREC ? make_rsrc(a.hx, TBH * 2) : make_rsrc(a.hcell, TBH * 4);
+  // staged rows: fp32 mode reads h_cell (src >= 0) or h0; bf16 mode reads the bf16 copy
+  // whose slot 0 holds h0 and slot s+1 the state of step s
+  const rsrc_t r_h = PREC ? make_rsrc(a.hx, TBH * 2 + (size_t)B * H * 2) : make_rsrc(a.hcell, TBH * 4);
 
   // ---- U slice into registers: A operand, row m = l16 -> (unit_base + m/4, gate m%4), K permuted per chunk
   const int a_unit = unit_base + (l16 >> 2), a_gate = l16 & 3;
@@ -68,14 +80,30 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
 
   const bool tracer = (w == 0) && ((int)threadIdx.x < BG) && (row0 + (int)threadIdx.x < B);
   const int my_row = row0 + (int)threadIdx.x;
-  const bool row_thread = ((int)threadIdx.x < BG) && (my_row < B);
   const size_t stk_base = (size_t)my_row * (T + 1);
-  const int kmax = ks_eff * KC;                    // staged K (>= H, zero beyond H)
+  const int kmax = ks_eff * KC;                    // staged K (>= H)
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
+  const bool direct = vec_ok && kmax == KP && (KP * ESZ) % 1024 == 0;
+  const int seg_per_row = (kmax * ESZ) / 1024;
 
-  // Integer stack of the group's rows, kept by workgroup 0 one step ahead of the floats:
-  // step t's trace is written during step t-1, so every workgroup can fetch the producer
-  // it reads at step t+1 while step t is still running.
+  // rows of this lane in the MFMA output layout: tile ti covers rows ti*16 .. ti*16+15
+  int lrow[NT];
+  bool lok[NT];
+#pragma unroll
+  for (int ti = 0; ti < NT; ++ti) {
+    lrow[ti] = row0 + ti * 16 + l16;
+    lok[ti] = (lrow[ti] < B) && (u < H);
+  }
+  auto xw_at = [&](int t, int ti) -> float4 {
+    const int b = lok[ti] ? lrow[ti] : 0, uu = lok[ti] ? u : 0;
+    return *(const float4*)(a.xw + ((size_t)t * B + b) * H4 + 4 * uu);
+  };
+  auto top_at = [&](int t, int ti) -> int {
+    const int b = lrow[ti] < B ? lrow[ti] : 0;
+    return (int)ld_coh_b32(r_top, (uint32_t)(((size_t)t * B + b) * 4));
+  };
+
+  // Integer stack of the group's rows, kept by workgroup 0 one step ahead of the floats.
   int my_p = 0, my_top = -1, op_next = 0;
   if (tracer) {
     int op0 = a.ops[my_row];
@@ -87,86 +115,130 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     a.top[my_row] = my_top;
   }
   if ((int)threadIdx.x < BG) s_src[threadIdx.x] = -1;
+  constexpr int NV = (BG + 63) / 64;
+  int vsrc[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) vsrc[j] = -1;
+  for (int i = threadIdx.x; i < ROWS_B * LDS_LD * ESZ / 16; i += 256) ((uint4*)smem)[i] = uint4{0u, 0u, 0u, 0u};
+  // operands of step 0's epilogue
+  float4 xw_cur[NT];
+  float cp_cur[NT];
+#pragma unroll
+  for (int ti = 0; ti < NT; ++ti) {
+    xw_cur[ti] = xw_at(0, ti);
+    cp_cur[ti] = lok[ti] ? a.c0[(size_t)lrow[ti] * H + u] : 0.f;
+  }
   if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)a.NW, a.ctl, a.spin_limit, &s_flag)) return;
 
   long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
   for (int t = 0; t < T; ++t) {
     if (clk && threadIdx.x == 0) clk[t * 4 + 0] = wall_clock64();
-    // producer of the state each row reads at step t+1 (= top[t], written one step ago)
+    const bool more = t + 1 < T;
+    float4 xw_nxt[NT];
+    int src_nxt[NT];
+    float cp_nxt[NT];
+    int tp_next = 0;
 
-    int src_next = -1, tp_next = 0;
-
-    for (int nb = 0; nb < NT / NTB; ++nb) {
-      // ---- gather h_prev rows of this pass into LDS (zero beyond H and for rows past B)
-      if (vec_ok) {
-        // every thread issues all of its loads before the first LDS write, so the
-        // latency of the L2 round trip is paid once per step, not once per vector
-        constexpr int VW = PREC ? 8 : 4;
-        constexpr int NLD = (ROWS_B * (KP / VW) + 255) / 256;
-        const int per_row = kmax / VW;
-        const int n_el = ROWS_B * per_row;
-        uint4 buf[NLD];
 #pragma unroll
-        for (int i = 0; i < NLD; ++i) {
-          const int e = threadIdx.x + 256 * i;
-          buf[i] = uint4{0u, 0u, 0u, 0u};
-          if (e >= n_el) continue;
-          const int r = e / per_row, k = (e - r * per_row) * VW;
-          const int rr = nb * ROWS_B + r, b = row0 + rr;
-          if (b >= B || k >= H) continue;
-          const int src = s_src[rr];
-          const size_t e2 = ((size_t)src * B + b) * H + k;
-          if constexpr (PREC == 0) {
-            if (src < 0) buf[i] = *(const uint4*)(a.h0 + (size_t)b * H + k);
-            else if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 4));
-            else buf[i] = *(const uint4*)(a.hcell + e2);
-          } else {
-            if (src < 0) {
-              const float* p = a.h0 + (size_t)b * H + k;
-              float4 v0 = *(const float4*)p, v1 = *(const float4*)(p + 4);
-              bf16_t o[8] = {f32_to_bf16_bits(v0.x), f32_to_bf16_bits(v0.y), f32_to_bf16_bits(v0.z),
-                             f32_to_bf16_bits(v0.w), f32_to_bf16_bits(v1.x), f32_to_bf16_bits(v1.y),
-                             f32_to_bf16_bits(v1.z), f32_to_bf16_bits(v1.w)};
-              buf[i] = *(const uint4*)o;
-            } else if (a.coh_rows) {
-              buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 2));
-            } else {
-              buf[i] = *(const uint4*)(a.hx + e2);
-            }
+    for (int nb = 0; nb < NPASS; ++nb) {
+      // ---- gather this pass's h_prev rows into LDS
+      if (direct) {
+        // one wave instruction moves one 1 KB segment of one row (16 bytes per lane);
+        // the row's producer comes from lane rr of vsrc (wave-uniform), no LDS round trip
+        constexpr int SEG = KP * ESZ / 1024;
+        constexpr int NSEG_W = (ROWS_B * SEG + 3) / 4;
+#pragma unroll
+        for (int i = 0; i < NSEG_W; ++i) {
+          const int sgi = wave + 4 * i;
+          if (sgi < ROWS_B * SEG) {
+            const int r = sgi / SEG, sj = sgi % SEG;
+            const int rr = nb * ROWS_B + r;
+            const int b = min(row0 + rr, B - 1);  // rows past B: any finite row (columns masked)
+            const int src = __builtin_amdgcn_readlane(vsrc[rr >> 6], rr & 63);
+            int k = sj * (1024 / ESZ) + lane * (16 / ESZ);
+            if (k >= H) k = 0;                    // finite filler; the U registers are 0 there
+            const elem_t* gp;
+            if constexpr (PREC == 0) gp = (src < 0) ? (const elem_t*)(a.h0 + (size_t)b * H + k)
+                                                    : (const elem_t*)(a.hcell + ((size_t)src * B + b) * H + k);
+            else gp = (const elem_t*)(a.hx + ((size_t)(src + 1) * B + b) * H + k);
+            lds_ptr_t dst = (lds_ptr_t)(hs + r * LDS_LD + sj * (1024 / ESZ));
+            if (a.coh_rows) __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, kSc1);
+            else __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, 0);
           }
-        }
-#pragma unroll
-        for (int i = 0; i < NLD; ++i) {
-          const int e = threadIdx.x + 256 * i;
-          if (e >= n_el) continue;
-          const int r = e / per_row, k = (e - r * per_row) * VW;
-          *(uint4*)(hs + r * LDS_LD + k) = buf[i];
         }
       } else {
-        for (int e = threadIdx.x; e < ROWS_B * kmax; e += 256) {
-          int r = e / kmax, k = e - r * kmax;
-          int rr = nb * ROWS_B + r, b = row0 + rr;
-          float v = 0.f;
-          if (b < B && k < H) {
-            int src = s_src[rr];
-            size_t e2 = ((size_t)src * B + b) * H + k;
-            if (src < 0) v = a.h0[(size_t)b * H + k];
-            else if constexpr (PREC == 0) v = __uint_as_float(ld_coh_b32(r_h, (uint32_t)(e2 * 4)));
-            else v = bf16_bits_to_f32(ld_coh_b16(r_h, (uint32_t)(e2 * 2)));
+        constexpr int VW = PREC ? 8 : 4;
+        if (vec_ok) {
+          // batches of four vector loads per thread: latency paid once per batch
+          const int per_row = kmax / VW;
+          const int n_el = ROWS_B * per_row;
+          for (int e0 = 0; e0 < n_el; e0 += 4 * 256) {
+            uint4 buf[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int e = e0 + threadIdx.x + 256 * i;
+              buf[i] = uint4{0u, 0u, 0u, 0u};
+              if (e >= n_el) continue;
+              const int r = e / per_row, k = (e - r * per_row) * VW;
+              const int rr = nb * ROWS_B + r, b = row0 + rr;
+              if (b >= B || k >= H) continue;
+              const int src = s_src[rr];
+              if constexpr (PREC == 0) {
+                const size_t e2 = ((size_t)src * B + b) * H + k;
+                if (src < 0) buf[i] = *(const uint4*)(a.h0 + (size_t)b * H + k);
+                else if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 4));
+                else buf[i] = *(const uint4*)(a.hcell + e2);
+              } else {
+                const size_t e2 = ((size_t)(src + 1) * B + b) * H + k;
+                if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 2));
+                else buf[i] = *(const uint4*)(a.hx + e2);
+              }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int e = e0 + threadIdx.x + 256 * i;
+              if (e >= n_el) continue;
+              const int r = e / per_row, k = (e - r * per_row) * VW;
+              *(uint4*)(hs + r * LDS_LD + k) = buf[i];
+            }
           }
-          if constexpr (PREC == 0) hs[r * LDS_LD + k] = v;
-          else hs[r * LDS_LD + k] = f32_to_bf16_bits(v);
+        } else {
+          for (int e = threadIdx.x; e < ROWS_B * kmax; e += 256) {
+            const int r = e / kmax, k = e - r * kmax;
+            const int rr = nb * ROWS_B + r, b = row0 + rr;
+            float v = 0.f;
+            if (b < B && k < H) {
+              const int src = s_src[rr];
+              if constexpr (PREC == 0) {
+                if (src < 0) v = a.h0[(size_t)b * H + k];
+                else v = __uint_as_float(ld_coh_b32(r_h, (uint32_t)((((size_t)src * B + b) * H + k) * 4)));
+              } else {
+                v = bf16_bits_to_f32(ld_coh_b16(r_h, (uint32_t)((((size_t)(src + 1) * B + b) * H + k) * 2)));
+              }
+            }
+            if constexpr (PREC == 0) hs[r * LDS_LD + k] = v;
+            else hs[r * LDS_LD + k] = f32_to_bf16_bits(v);
+          }
         }
+      }
+      asm volatile("" ::: "memory");
+      if (nb == 0) {
+        // producers read at step t+1 (top[t], written one step ago) and the next step's
+        // input projection: in flight during this step; the wait below leaves exactly
+        // these 2*NT loads outstanding
+#pragma unroll
+        for (int ti = 0; ti < NT; ++ti) src_nxt[ti] = top_at(t, ti);
+#pragma unroll
+        for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NT) : "memory");
+      } else {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       }
       __syncthreads();
       if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 1] = wall_clock64();
-      if (nb == 0 && row_thread && t + 1 < T) {
-        const size_t o = (size_t)t * B + my_row;
-        src_next = a.coh_top ? (int)ld_coh_b32(r_top, (uint32_t)(o * 4)) : a.top[o];
-      }
-      // trace for step t+1: stack[p+1] <- t+1, p <- p + op, top <- stack[p]; issued after the
-      // h_prev loads so that their wait does not include it, consumed before the barrier
-      if (nb == 0 && tracer && t + 1 < T) {
+
+      // trace for step t+1 (stack[p+1] <- t+1, p <- p + op, top <- stack[p]), stored before the barrier
+      if (nb == 0 && tracer && more) {
         int op = op_next;
         op_next = (t + 2 < T) ? a.ops[(size_t)(t + 2) * B + my_row] : 0;
         a.stack[stk_base + my_p + 1] = t + 1;
@@ -174,75 +246,97 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         tp_next = (op == 1) ? t + 1 : (op == 0 ? my_top : a.stack[stk_base + my_p]);
       }
 
-      // ---- epilogue operands, fetched before the MFMA loop so their latency overlaps it
-      const int u = unit_base + lq;
-      float4 xw4[NTB];
-      float cprev[NTB];
-#pragma unroll
-      for (int nt = 0; nt < NTB; ++nt) {
-        int rr = nb * ROWS_B + nt * 16 + l16, b = row0 + rr;
-        xw4[nt] = float4{0.f, 0.f, 0.f, 0.f};
-        cprev[nt] = 0.f;
-        if (b < B && u < H) {
-          xw4[nt] = *(const float4*)(a.xw + ((size_t)t * B + b) * H4 + 4 * u);
-          int src = s_src[rr];
-          cprev[nt] = (src < 0) ? a.c0[(size_t)b * H + u] : a.ccell[((size_t)src * B + b) * H + u];
-        }
-      }
-
-      // ---- gates^T (16 cols x 16 rows per tile) = U^T h_prev^T
+      // ---- gates^T (16 cols x 16 rows per tile) = U^T h_prev^T; B fragments read one chunk ahead
       f32x4 acc[NTB];
 #pragma unroll
       for (int nt = 0; nt < NTB; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // all KS chunks run: U registers and staged LDS columns are zero beyond H
+      if constexpr (PREC == 0) {
+        float4 bcur[NTB], bnxt[NTB];
 #pragma unroll
-      for (int c = 0; c < KS; ++c) {
-        if (c < ks_eff) {
+        for (int nt = 0; nt < NTB; ++nt) bcur[nt] = *(const float4*)&hs[(nt * 16 + l16) * LDS_LD + 4 * lq];
 #pragma unroll
-          for (int nt = 0; nt < NTB; ++nt) {
-            if constexpr (PREC == 0) {
-              float4 bv = *(const float4*)&hs[(nt * 16 + l16) * LDS_LD + c * 16 + 4 * lq];
-              acc[nt] = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc[nt]);
-              acc[nt] = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc[nt]);
-              acc[nt] = mfma_f32_16x16x4(ureg32[c][2], bv.z, acc[nt]);
-              acc[nt] = mfma_f32_16x16x4(ureg32[c][3], bv.w, acc[nt]);
-            } else {
-              bf16x8 bv = *(const bf16x8*)&hs[(nt * 16 + l16) * LDS_LD + c * 32 + 8 * lq];
-              acc[nt] = mfma_bf16_16x16x32(ureg16[c], bv, acc[nt]);
-            }
+        for (int c = 0; c < KS; ++c) {
+          if (c + 1 < KS) {
+#pragma unroll
+            for (int nt = 0; nt < NTB; ++nt)
+              bnxt[nt] = *(const float4*)&hs[(nt * 16 + l16) * LDS_LD + (c + 1) * 16 + 4 * lq];
           }
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int nt = 0; nt < NTB; ++nt) acc[nt] = mfma_f32_16x16x4(ureg32[c][j], bcur[nt][j], acc[nt]);
+#pragma unroll
+          for (int nt = 0; nt < NTB; ++nt) bcur[nt] = bnxt[nt];
+        }
+      } else {
+        bf16x8 bcur[NTB], bnxt[NTB];
+#pragma unroll
+        for (int nt = 0; nt < NTB; ++nt) bcur[nt] = *(const bf16x8*)&hs[(nt * 16 + l16) * LDS_LD + 8 * lq];
+#pragma unroll
+        for (int c = 0; c < KS; ++c) {
+          if (c + 1 < KS) {
+#pragma unroll
+            for (int nt = 0; nt < NTB; ++nt)
+              bnxt[nt] = *(const bf16x8*)&hs[(nt * 16 + l16) * LDS_LD + (c + 1) * 32 + 8 * lq];
+          }
+#pragma unroll
+          for (int nt = 0; nt < NTB; ++nt) acc[nt] = mfma_bf16_16x16x32(ureg16[c], bcur[nt], acc[nt]);
+#pragma unroll
+          for (int nt = 0; nt < NTB; ++nt) bcur[nt] = bnxt[nt];
         }
       }
-
       if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 2] = wall_clock64();
+
       // ---- fused LSTM cell: lane holds gates i, f, g, o of unit u for row l16 of each tile
 #pragma unroll
       for (int nt = 0; nt < NTB; ++nt) {
-        int rr = nb * ROWS_B + nt * 16 + l16, b = row0 + rr;
-        if (b >= B || u >= H) continue;
-        float gi = sigmoidf_(acc[nt][0] + xw4[nt].x);
-        float gf = sigmoidf_(acc[nt][1] + xw4[nt].y);
-        float gg = tanhf(acc[nt][2] + xw4[nt].z);
-        float go = sigmoidf_(acc[nt][3] + xw4[nt].w);
-        float c = gf * cprev[nt] + gi * gg;
-        float h = go * tanhf(c);
-        size_t o = ((size_t)t * B + b) * H + u;
+        const int ti = nb * NTB + nt;
+        if (!lok[ti]) continue;
+        const int b = lrow[ti];
+        const float gi = sigmoidf_(acc[nt][0] + xw_cur[ti].x);
+        const float gf = sigmoidf_(acc[nt][1] + xw_cur[ti].y);
+        const float gg = tanhf(acc[nt][2] + xw_cur[ti].z);
+        const float go = sigmoidf_(acc[nt][3] + xw_cur[ti].w);
+        const float c = gf * cp_cur[ti] + gi * gg;
+        const float h = go * tanhf(c);
+        const size_t o = ((size_t)t * B + b) * H + u;
         a.hcell[o] = h;
         a.ccell[o] = c;
-        if constexpr (PREC == 1) a.hx[o] = f32_to_bf16_bits(h);
+        if constexpr (PREC == 1) a.hx[o + (size_t)B * H] = f32_to_bf16_bits(h);
         *(float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * u) = float4{gi, gf, gg, go};
+        cp_cur[ti] = c;                            // the state this step produced
       }
-      if (NT / NTB > 1) __syncthreads();
+      if (NPASS > 1) __syncthreads();
     }
 
+    // c_prev of step t+1: the state produced now (push at t) or an older one of this workgroup
+#pragma unroll
+    for (int ti = 0; ti < NT; ++ti) {
+      int s = src_nxt[ti];
+      if (!more || s < -1 || s > t) s = -1;
+      src_nxt[ti] = s;
+      cp_nxt[ti] = cp_cur[ti];
+      if (lok[ti] && s != t) {
+        const int b = lrow[ti];
+        cp_nxt[ti] = (s < 0) ? a.c0[(size_t)b * H + u] : a.ccell[((size_t)s * B + b) * H + u];
+      }
+    }
     if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
-    if (tracer && t + 1 < T) {
+    if (tracer && more) {
       a.top[(size_t)(t + 1) * B + my_row] = tp_next;
       my_top = tp_next;
     }
     if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_flag)) break;
-    if (src_next < -1 || src_next > t) src_next = -1;   // only a valid producer is ever indexed
-    if ((int)threadIdx.x < BG) s_src[threadIdx.x] = src_next;
+    if (wave == 0 && lq == 0) {
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti) s_src[ti * 16 + l16] = src_nxt[ti];
+    }
+#pragma unroll
+    for (int ti = 0; ti < NT; ++ti) { xw_cur[ti] = xw_nxt[ti]; cp_cur[ti] = cp_nxt[ti]; }
     __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NV; ++j) vsrc[j] = (64 * j + lane < BG) ? s_src[64 * j + lane] : -1;
   }
 }
 

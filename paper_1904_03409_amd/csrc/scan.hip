@@ -96,3 +96,33 @@ __global__ void __launch_bounds__(256) k_fill_f32(float* __restrict__ p, size_t 
 __global__ void __launch_bounds__(256) k_zero_u32(uint32_t* __restrict__ p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
 }
+
+// bf16 copy of h0 into slot 0 of the bf16 state array (slot s+1 holds the state of step s)
+__global__ void __launch_bounds__(256) k_h0_bf16(const float* __restrict__ h0, bf16_t* __restrict__ hx, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    hx[i] = f32_to_bf16_bits(h0[i]);
+}
+
+// fp32 -> bf16 (nearest even), elementwise
+__global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ in, bf16_t* __restrict__ out, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    out[i] = f32_to_bf16_bits(in[i]);
+}
+
+// Hprev[t][b][:] = the state read at step t: h0[b] for t = 0, else the state produced at step
+// top[t-1][b] (-1 = h0). fp32 rows from h_cell, or bf16 rows from the bf16 state copy (slot
+// s+1 = step s, slot 0 = h0) in bf16-GEMM mode.
+__global__ void __launch_bounds__(256) k_gather_hprev(const int32_t* __restrict__ top, const float* __restrict__ hcell,
+                                                      const float* __restrict__ h0, const bf16_t* __restrict__ hx,
+                                                      void* __restrict__ out, int T, int B, int H) {
+  const size_t n = (size_t)T * B * H;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    size_t tb = i / H;
+    int u = (int)(i - tb * H);
+    int t = (int)(tb / B), b = (int)(tb - (size_t)t * B);
+    int s = (t == 0) ? -1 : top[tb - B];
+    if (s < -1 || s >= t) s = -1;                 // only a valid producer is ever indexed
+    if (hx) ((bf16_t*)out)[i] = hx[((size_t)(s + 1) * B + b) * H + u];
+    else ((float*)out)[i] = (s < 0) ? h0[(size_t)b * H + u] : hcell[((size_t)s * B + b) * H + u];
+  }
+}
