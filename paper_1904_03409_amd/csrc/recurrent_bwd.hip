@@ -24,7 +24,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   constexpr int BG = NT * 16;
   constexpr int PAIRS = BG * 16 / 256;            // (row, unit) pairs per thread
   __shared__ float red[4][BG][17];
-  __shared__ int s_op[BG], s_top[BG], s_src[BG];
+  __shared__ int s_op[BG], s_top[BG], s_src[BG], s_crow[BG], s_cidx[BG], s_nlive;
   __shared__ float s_db[16][16][4];
   __shared__ int s_g, s_w, s_flag;
 
@@ -66,6 +66,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // ---- this thread's (row, unit) pairs: unit fixed per thread, rows r = tid/16 + 16 i
   const int uu = threadIdx.x & 15;
   const int u = w * 16 + uu;
+  const int ul = (u < H) ? u : 0;                   // unit used in load addresses (in bounds)
   int prow[PAIRS];
   bool pok[PAIRS];
 #pragma unroll
@@ -73,182 +74,295 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     prow[i] = (threadIdx.x >> 4) + 16 * i;
     pok[i] = (row0 + prow[i] < B) && (u < H);
   }
-  // zero the accumulator slots that can receive gradient: slot 0 and the slots of push steps
-#pragma unroll
-  for (int i = 0; i < PAIRS; ++i) {
-    if (!pok[i]) continue;
-    int b = row0 + prow[i];
-    a.dh_acc[(size_t)b * H + u] = 0.f;
-    a.dc_acc[(size_t)b * H + u] = 0.f;
-    for (int s = 0; s < T; ++s) {
-      if (a.ops[(size_t)s * B + b] == 1) {
-        size_t o = ((size_t)(s + 1) * B + b) * H + u;
-        a.dh_acc[o] = 0.f;
-        a.dc_acc[o] = 0.f;
+  // zero this workgroup's accumulator slots ([T+1] slots x group rows x its 16 units) with
+  // 16-byte stores; slot 0 is the initial state
+  {
+    const int n4 = (T + 1) * BG * 4;
+    for (int i = threadIdx.x; i < n4; i += 256) {
+      const int slot = i / (BG * 4), rem = i - slot * (BG * 4);
+      const int r = rem >> 2, q = rem & 3;
+      const int b = row0 + r, u0 = w * 16 + 4 * q;
+      if (b >= B) continue;
+      const size_t o = ((size_t)slot * B + b) * H + u0;
+      if (u0 + 3 < H && (H & 3) == 0) {
+        *(float4*)(a.dh_acc + o) = float4{0.f, 0.f, 0.f, 0.f};
+        *(float4*)(a.dc_acc + o) = float4{0.f, 0.f, 0.f, 0.f};
+      } else {
+        for (int j = 0; j < 4; ++j)
+          if (u0 + j < H) { a.dh_acc[o + j] = 0.f; a.dc_acc[o + j] = 0.f; }
       }
     }
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+
+  // Loads are issued a step (or at least a phase) before their values are used. Per pair:
+  //   cur_*  operands of the current step t, fetched during step t+1;
+  //   slot_* gradient of the state produced at step t (dh_acc/dc_acc slot t+1), fetched at the
+  //          start of step t+1 and updated in registers by step t+1's contributions to it;
+  //   tg_*   the slot this step adds into (src+1 for a push, top+1 otherwise), fetched at the
+  //          start of step t and written back with the contribution.
+  auto valid = [&](int t, int op, int& tp, int& sp) {
+    // guard against a producer table that is not the forward's: no access outside [-1, t]
+    if (tp < -1 || tp > t || (op == 1 && tp != t)) tp = -1;
+    if (sp < -1 || sp >= t) sp = -1;
+  };
+  int c_op[PAIRS], c_tp[PAIRS], c_sp[PAIRS];            // step t row info
+  int n_op[PAIRS], n_sp[PAIRS];                          // step t-1 (top[t-1] = c_sp)
+  float c_gh[PAIRS], c_gc[PAIRS], c_c[PAIRS], c_cp[PAIRS];
+  float4 c_act[PAIRS];
+  float n_gh[PAIRS], n_gc[PAIRS], n_c[PAIRS], n_cp[PAIRS];
+  float4 n_act[PAIRS];
+  float slot_dh[PAIRS], slot_dc[PAIRS], nx_dh[PAIRS], nx_dc[PAIRS], tg_dh[PAIRS], tg_dc[PAIRS];
+  auto ld_row = [&](int t, int b, int& op, int& sp) {
+    op = a.ops[(size_t)t * B + b];
+    sp = (t == 0) ? -1 : a.top[(size_t)(t - 1) * B + b];
+  };
+  auto ld_ops = [&](int t, int b, float& gh, float& gc, float4& act, float& c) {
+    const size_t o = ((size_t)t * B + b) * H + ul;
+    gh = a.dh_top[o];
+    gc = a.dc_top ? a.dc_top[o] : 0.f;
+    act = *(const float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * ul);
+    c = a.ccell[o];
+  };
+  auto ld_cp = [&](int sp, int b) -> float {
+    return (sp < 0) ? a.c0[(size_t)b * H + ul] : a.ccell[((size_t)sp * B + b) * H + ul];
+  };
+#pragma unroll
+  for (int i = 0; i < PAIRS; ++i) {
+    const int b = pok[i] ? row0 + prow[i] : 0;
+    int op, sp;
+    ld_row(T - 1, b, op, sp);
+    int tp = a.top[(size_t)(T - 1) * B + b];
+    valid(T - 1, op, tp, sp);
+    c_op[i] = op; c_tp[i] = tp; c_sp[i] = sp;
+    ld_ops(T - 1, b, c_gh[i], c_gc[i], c_act[i], c_c[i]);
+    c_cp[i] = ld_cp(sp, b);
+    slot_dh[i] = 0.f; slot_dc[i] = 0.f;                // slot T was zeroed and nothing adds to it later
+  }
 
   long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
   for (int t = T - 1; t >= 0; --t) {
     if (clk && threadIdx.x == 0) clk[t * 4 + 0] = wall_clock64();
-    if ((int)threadIdx.x < BG) {
-      int b = row0 + (int)threadIdx.x;
-      int op = 0, tp = -1, sp = -1;
-      if (b < B) {
-        op = a.ops[(size_t)t * B + b];
-        tp = a.top[(size_t)t * B + b];
-        sp = (t == 0) ? -1 : a.top[(size_t)(t - 1) * B + b];
-        // guard against a producer table that is not the forward's: no access outside [-1, t]
-        if (tp < -1 || tp > t || (op == 1 && tp != t)) { tp = -1; op = (op == 1) ? 0 : op; }
-        if (sp < -1 || sp >= t) sp = -1;
+    // row tables of step t for the compaction (from the registers of the unit-0 threads)
+    if (uu == 0) {
+#pragma unroll
+      for (int i = 0; i < PAIRS; ++i) {
+        s_op[prow[i]] = pok[i] ? c_op[i] : 0;
+        s_src[prow[i]] = c_sp[i];
+        s_top[prow[i]] = c_tp[i];
       }
-      s_op[threadIdx.x] = op; s_top[threadIdx.x] = tp; s_src[threadIdx.x] = sp;
+    }
+    // loads, in the order they are needed (vector loads complete in issue order, so the
+    // epilogue's wait for the target slot does not include the HBM prefetch behind it):
+    // this step's target slot, slot t, then row info and operands of step t-1
+#pragma unroll
+    for (int i = 0; i < PAIRS; ++i) {
+      const int b = pok[i] ? row0 + prow[i] : 0;
+      const int tgt = (c_op[i] == 1) ? c_sp[i] : c_tp[i];
+      const size_t to = ((size_t)(tgt + 1) * B + b) * H + ul;
+      tg_dh[i] = a.dh_acc[to];
+      tg_dc[i] = a.dc_acc[to];
+    }
+#pragma unroll
+    for (int i = 0; i < PAIRS; ++i) {
+      const int b = pok[i] ? row0 + prow[i] : 0;
+      if (t > 0) {
+        const size_t no = ((size_t)t * B + b) * H + ul;
+        nx_dh[i] = a.dh_acc[no];
+        nx_dc[i] = a.dc_acc[no];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < PAIRS; ++i) {
+      const int b = pok[i] ? row0 + prow[i] : 0;
+      if (t > 0) {
+        ld_row(t - 1, b, n_op[i], n_sp[i]);
+        ld_ops(t - 1, b, n_gh[i], n_gc[i], n_act[i], n_c[i]);
+      }
     }
     __syncthreads();
+    if (wave == 0) {
+      // list the push rows in row order (wave-wide ballot + prefix count)
+      int base = 0;
+#pragma unroll
+      for (int r0 = 0; r0 < BG; r0 += 64) {
+        const int r = r0 + lane;
+        const bool live = (r < BG) && (s_op[r] == 1);
+        const unsigned long long m = __ballot(live);
+        const int ci = base + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+        if (live) { s_cidx[r] = ci; s_crow[ci] = r; }
+        base += __popcll(m);
+      }
+      if (lane == 0) s_nlive = base;
+    }
 
     // ---- cell backward for this workgroup's (row, unit) pairs
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
-      if (!pok[i]) continue;
-      const int r = prow[i], b = row0 + r;
-      const size_t o = ((size_t)t * B + b) * H + u;
-      const int op = s_op[r];
-      float gh = a.dh_top[o];
-      float gc = a.dc_top ? a.dc_top[o] : 0.f;
       float4 dA4 = float4{0.f, 0.f, 0.f, 0.f};
-      if (op == 1) {
-        const int src = s_src[r];
-        const size_t so = ((size_t)(t + 1) * B + b) * H + u;
-        float dh = a.dh_acc[so] + gh;
-        float dcin = a.dc_acc[so] + gc;
-        float4 act = *(const float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * u);
-        float c = a.ccell[o];
-        float cp = (src < 0) ? a.c0[(size_t)b * H + u] : a.ccell[((size_t)src * B + b) * H + u];
-        float tc = tanhf(c);
-        float dc = dcin + dh * act.w * (1.f - tc * tc);
+      const int b = row0 + prow[i];
+      const int tgt = (c_op[i] == 1) ? c_sp[i] : c_tp[i];
+      const bool fwd_slot = (t > 0) && (tgt + 1 == t);   // contribution lands in next step's slot
+      float add_dh = 0.f, add_dc = 0.f;
+      if (c_op[i] == 1) {
+        const float4 act = c_act[i];
+        const float dh = slot_dh[i] + c_gh[i];
+        const float dcin = slot_dc[i] + c_gc[i];
+        const float tc = tanhf(c_c[i]);
+        const float dc = dcin + dh * act.w * (1.f - tc * tc);
         dA4.x = dc * act.z * act.x * (1.f - act.x);
-        dA4.y = dc * cp * act.y * (1.f - act.y);
+        dA4.y = dc * c_cp[i] * act.y * (1.f - act.y);
         dA4.z = dc * act.x * (1.f - act.z * act.z);
         dA4.w = dh * tc * act.w * (1.f - act.w);
-        const size_t po = ((size_t)(src + 1) * B + b) * H + u;
-        a.dc_acc[po] += dc * act.y;
-        dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w;
+        add_dc = dc * act.y;
+        if (pok[i]) { dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w; }
       } else {
-        const size_t io = ((size_t)(s_top[r] + 1) * B + b) * H + u;
-        a.dh_acc[io] += gh;
-        if (a.dc_top) a.dc_acc[io] += gc;
+        add_dh = c_gh[i];
+        add_dc = c_gc[i];
       }
-      const size_t ao = ((size_t)t * B + b) * H4 + 4 * u;
-      if constexpr (PREC == 0) {
-        *(float4*)((float*)a.dA + ao) = dA4;
-      } else {
-        bf16_t q[4] = {f32_to_bf16_bits(dA4.x), f32_to_bf16_bits(dA4.y), f32_to_bf16_bits(dA4.z),
-                       f32_to_bf16_bits(dA4.w)};
-        *(uint2*)((bf16_t*)a.dA + ao) = *(const uint2*)q;
+      if (fwd_slot) {
+        nx_dh[i] += add_dh;
+        nx_dc[i] += add_dc;
+      } else if (pok[i]) {
+        const size_t to = ((size_t)(tgt + 1) * B + b) * H + u;
+        tg_dh[i] += add_dh;
+        tg_dc[i] += add_dc;
+        if (c_op[i] != 1) a.dh_acc[to] = tg_dh[i];   // a push's dh contribution comes after the GEMM
+        a.dc_acc[to] = tg_dc[i];
+      }
+      if (pok[i]) {
+        const size_t ao = ((size_t)t * B + b) * H4 + 4 * u;
+        if constexpr (PREC == 0) {
+          *(float4*)((float*)a.dA + ao) = dA4;
+        } else {
+          bf16_t q[4] = {f32_to_bf16_bits(dA4.x), f32_to_bf16_bits(dA4.y), f32_to_bf16_bits(dA4.z),
+                         f32_to_bf16_bits(dA4.w)};
+          *(uint2*)((bf16_t*)a.dA + ao) = *(const uint2*)q;
+        }
       }
     }
 
     if (clk && threadIdx.x == 0) clk[t * 4 + 1] = wall_clock64();
     if (group_barrier(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_flag)) break;
     if (clk && threadIdx.x == 0) clk[t * 4 + 2] = wall_clock64();
-
-    // ---- dh_prev^T (16 units x 16 rows per tile) = U^T-slice x dA^T over this wave's gate columns
-    // B fragments are fetched one group of CG chunks ahead of the MFMAs that use them
-    constexpr int CG = (NT >= 8) ? 1 : (8 / NT);
-    constexpr int NG = (KS + CG - 1) / CG;
-    f32x4 acc[NT];
+    // c_prev of step t-1 (its producer index arrived with the prefetch above)
+    if (t > 0) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bool live[NT];
-    size_t rowo[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int r = nt * 16 + l16, b = row0 + r;
-      live[nt] = (b < B) && (s_op[r] == 1);              // dA rows of non-push steps are zero
-      rowo[nt] = ((size_t)t * B + (live[nt] ? b : 0)) * H4 + (size_t)wave * H;
+      for (int i = 0; i < PAIRS; ++i) {
+        int op = n_op[i], tp = c_sp[i], sp = n_sp[i];
+        valid(t - 1, op, tp, sp);
+        n_sp[i] = sp;
+        n_cp[i] = ld_cp(sp, pok[i] ? row0 + prow[i] : 0);
+      }
     }
-    // Branch-free fragment loads through the bounds-checked descriptor: a lane whose row
-    // is not a push (its dA row is exactly 0) or whose k is past H gets an offset beyond
-    // the buffer, which returns 0 without a memory access.
+
+    // Only push rows have non-zero dA. They are listed (in row order) in s_crow and run as
+    // compacted 16-row MFMA tiles; each tile's K loop fetches its fragments one group of CG
+    // chunks ahead, through the bounds-checked descriptor (a lane past the list or k past H
+    // gets an out-of-range offset: value 0, no memory access). Two accumulators per tile
+    // keep two independent MFMA chains.
+    constexpr int CG = 8;
+    constexpr int NG = (KS + CG - 1) / CG;
     const uint32_t kOOB = 0xffffffffu;
-    auto fetch = [&](int c, int nt) -> uint4 {
-      const int kk = c * KC + (PREC ? 8 : 4) * lq;
-      const size_t el = rowo[nt] + kk;
-      if (vec_ok) {
-        const uint32_t off = (live[nt] && kk < H) ? (uint32_t)(el * ESZ) : kOOB;
-        if (a.coh_rows) return ld_coh_b128(r_dA, off);
-        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r_dA, off, 0, 0));
-      }
-      uint4 raw;
-      uint32_t* rw = (uint32_t*)&raw;
-      if constexpr (PREC == 0) {
-        for (int j = 0; j < 4; ++j)
-          rw[j] = ld_coh_b32(r_dA, (live[nt] && kk + j < H) ? (uint32_t)((el + j) * 4) : kOOB);
-      } else {
-        for (int j = 0; j < 4; ++j) {
-          uint32_t lo = ld_coh_b16(r_dA, (live[nt] && kk + 2 * j < H) ? (uint32_t)((el + 2 * j) * 2) : kOOB);
-          uint32_t hi = ld_coh_b16(r_dA, (live[nt] && kk + 2 * j + 1 < H) ? (uint32_t)((el + 2 * j + 1) * 2) : kOOB);
-          rw[j] = lo | (hi << 16);
+    const int nlive = s_nlive;
+    for (int jt = 0; jt < NT; ++jt) {
+      if (jt * 16 >= nlive) break;
+      const int ci = jt * 16 + l16;
+      const bool lv = ci < nlive;
+      const int r = lv ? s_crow[ci] : 0;
+      const size_t rowo = ((size_t)t * B + row0 + r) * H4 + (size_t)wave * H;
+      auto fetch = [&](int c) -> uint4 {
+        const int kk = c * KC + (PREC ? 8 : 4) * lq;
+        const size_t el = rowo + kk;
+        if (vec_ok) {
+          const uint32_t off = (lv && kk < H) ? (uint32_t)(el * ESZ) : kOOB;
+          if (a.coh_rows) return ld_coh_b128(r_dA, off);
+          return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r_dA, off, 0, 0));
         }
-      }
-      return raw;
-    };
-    uint4 bufA[CG][NT], bufB[CG][NT];
+        uint4 raw;
+        uint32_t* rw = (uint32_t*)&raw;
+        if constexpr (PREC == 0) {
+          for (int j = 0; j < 4; ++j) rw[j] = ld_coh_b32(r_dA, (lv && kk + j < H) ? (uint32_t)((el + j) * 4) : kOOB);
+        } else {
+          for (int j = 0; j < 4; ++j) {
+            uint32_t lo = ld_coh_b16(r_dA, (lv && kk + 2 * j < H) ? (uint32_t)((el + 2 * j) * 2) : kOOB);
+            uint32_t hi = ld_coh_b16(r_dA, (lv && kk + 2 * j + 1 < H) ? (uint32_t)((el + 2 * j + 1) * 2) : kOOB);
+            rw[j] = lo | (hi << 16);
+          }
+        }
+        return raw;
+      };
+      f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint4 bufA[CG], bufB[CG];
 #pragma unroll
-    for (int j = 0; j < CG; ++j)
+      for (int j = 0; j < CG; ++j) bufA[j] = (j < KS) ? fetch(j) : uint4{0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) bufA[j][nt] = fetch(j, nt);
+      for (int gi = 0; gi < NG; ++gi) {
+        uint4 (&cur)[CG] = (gi & 1) ? bufB : bufA;
+        uint4 (&nxt)[CG] = (gi & 1) ? bufA : bufB;
+        if (gi + 1 < NG) {
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {
-      uint4 (&cur)[CG][NT] = (gi & 1) ? bufB : bufA;
-      uint4 (&nxt)[CG][NT] = (gi & 1) ? bufA : bufB;
-      if (gi + 1 < NG) {
+          for (int j = 0; j < CG; ++j) nxt[j] = ((gi + 1) * CG + j < KS) ? fetch((gi + 1) * CG + j) : uint4{0u, 0u, 0u, 0u};
+        }
 #pragma unroll
-        for (int j = 0; j < CG; ++j)
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) nxt[j][nt] = fetch((gi + 1) * CG + j, nt);
-      }
-#pragma unroll
-      for (int j = 0; j < CG; ++j) {
-        const int c = gi * CG + j;
-        if (c >= KS) continue;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
+        for (int j = 0; j < CG; ++j) {
+          const int c = gi * CG + j;
+          if (c >= KS) continue;
+          f32x4& acc = (j & 1) ? acc1 : acc0;
           if constexpr (PREC == 0) {
-            const float4 bv = __builtin_bit_cast(float4, cur[j][nt]);
-            acc[nt] = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc[nt]);
-            acc[nt] = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc[nt]);
-            acc[nt] = mfma_f32_16x16x4(ureg32[c][2], bv.z, acc[nt]);
-            acc[nt] = mfma_f32_16x16x4(ureg32[c][3], bv.w, acc[nt]);
+            const float4 bv = __builtin_bit_cast(float4, cur[j]);
+            acc = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc);
+            acc = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc);
+            acc = mfma_f32_16x16x4(ureg32[c][2], bv.z, acc);
+            acc = mfma_f32_16x16x4(ureg32[c][3], bv.w, acc);
           } else {
-            acc[nt] = mfma_bf16_16x16x32(ureg16[c], __builtin_bit_cast(bf16x8, cur[j][nt]), acc[nt]);
+            acc = mfma_bf16_16x16x32(ureg16[c], __builtin_bit_cast(bf16x8, cur[j]), acc);
           }
         }
       }
+      // lane holds units 4*lq + j of compacted row ci
+      if (lv) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) red[wave][ci][4 * lq + j] = acc0[j] + acc1[j];
+      }
     }
-    // lane holds units 4*lq + j of row l16 of each tile
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) red[wave][nt * 16 + l16][4 * lq + j] = acc[nt][j];
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
-      if (!pok[i]) continue;
-      const int r = prow[i], b = row0 + r;
-      if (s_op[r] != 1) continue;
-      float s = red[0][r][uu] + red[1][r][uu] + red[2][r][uu] + red[3][r][uu];
-      a.dh_acc[((size_t)(s_src[r] + 1) * B + b) * H + u] += s;
+      if (c_op[i] == 1) {
+        const int r = prow[i], b = row0 + r;
+        const int ci = s_cidx[r];
+        const float sdh = red[0][ci][uu] + red[1][ci][uu] + red[2][ci][uu] + red[3][ci][uu];
+        if (t > 0 && c_sp[i] + 1 == t) {
+          nx_dh[i] += sdh;
+        } else if (pok[i]) {
+          tg_dh[i] += sdh;
+          a.dh_acc[((size_t)(c_sp[i] + 1) * B + b) * H + u] = tg_dh[i];
+        }
+      }
+    }
+    if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
+    // rotate: step t-1 becomes current
+#pragma unroll
+    for (int i = 0; i < PAIRS; ++i) {
+      slot_dh[i] = nx_dh[i]; slot_dc[i] = nx_dc[i];
+      c_tp[i] = c_sp[i];
+      c_op[i] = n_op[i]; c_sp[i] = n_sp[i];
+      {
+        int op = c_op[i], tp = c_tp[i], sp = c_sp[i];
+        valid(t - 1, op, tp, sp);
+        c_tp[i] = tp;
+      }
+      c_gh[i] = n_gh[i]; c_gc[i] = n_gc[i]; c_act[i] = n_act[i]; c_c[i] = n_c[i]; c_cp[i] = n_cp[i];
     }
     __syncthreads();
-    if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
   }
 
   // ---- outputs of this workgroup: dh0, dc0 for its pairs; per-group bias gradient
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
   for (int i = 0; i < PAIRS; ++i) {
     if (!pok[i]) continue;
