@@ -23,6 +23,8 @@ __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
 __global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const bf16_t* hx, void* out,
                                int T, int B, int H);
+__global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int rows, int cols, const int32_t* gtop, int B,
+                                 bf16_t* out);
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
@@ -57,7 +59,7 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, xb, hp, dh, dc, dbp, part, total;
+  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, total;
 };
 
 bool dims_ok(const slstm_dims* d) {
@@ -135,7 +137,9 @@ Layout layout(const slstm_dims* d) {
   L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
   L.hx = o; o += bf ? align256((T + 1) * B * H * 2) : 0;
   L.xb = o; o += bf ? align256(T * B * I * 2) : 0;                    // x in bf16 (bf16 mode)
-  L.hp = o; o += align256(std::max<size_t>(T * B * H * (bf ? 2 : 4), 16));   // Hprev rows
+  L.xbt = o; o += bf ? align256(T * B * I * 2) : 0;                   // x^T in bf16 (bf16 mode)
+  L.hp = o; o += align256(std::max<size_t>(T * B * H * (bf ? 2 : 4), 16));   // Hprev (bf16 mode: Hprev^T)
+  L.dat = o; o += bf ? align256(T * B * 4 * H * 2) : 0;               // dA^T in bf16 (bf16 mode)
   L.dh = o; o += align256((T + 1) * B * H * 4);
   L.dc = o; o += align256((T + 1) * B * H * 4);
   L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
@@ -352,32 +356,43 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   const size_t esz = bf ? 2 : 4;
   const void* xa = bf ? (const void*)(ws + L.xb) : (const void*)x;
   GemmArgs g;
-  // dW = x^T dA
+  // dW = x^T dA and dU = Hprev^T dA. In bf16 mode both operands are first written
+  // transposed (k = step*B + element contiguous), so the GEMM reads k-contiguous rows.
+  void* hp = ws + L.hp;
+  const void* dAt = a.dA;
+  if (bf) {
+    const dim3 tg4((H4 + 63) / 64, (K + 63) / 64), tgI((I + 63) / 64, (K + 63) / 64), tgH((H + 63) / 64, (K + 63) / 64);
+    hipLaunchKernelGGL(k_transpose_bf16, tg4, dim3(256), 0, st, a.dA, 0, H4, K, H4, (const int32_t*)nullptr, B,
+                       (bf16_t*)(ws + L.dat));
+    hipLaunchKernelGGL(k_transpose_bf16, tgI, dim3(256), 0, st, x, 1, I, K, I, (const int32_t*)nullptr, B,
+                       (bf16_t*)(ws + L.xbt));
+    hipLaunchKernelGGL(k_transpose_bf16, tgH, dim3(256), 0, st, ws + L.hx, 0, H, K, H, top, B, (bf16_t*)hp);
+    dAt = ws + L.dat;
+  } else {
+    hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0,
+                       (const bf16_t*)nullptr, hp, T, B, H);
+  }
   memset(&g, 0, sizeof(g));
   g.M = I; g.N = H4; g.K = K;
-  g.A = xa; g.lda = I; g.a_vec = (I % (bf ? 8 : 4) == 0);
-  g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % (bf ? 8 : 4) == 0);
+  if (bf) { g.A = ws + L.xbt; g.lda = K; g.a_vec = (K % 8 == 0); g.Bm = dAt; g.ldb = K; g.b_vec = (K % 8 == 0); }
+  else    { g.A = x; g.lda = I; g.a_vec = (I % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % 4 == 0); }
   g.C = part; g.ldc = H4;
   g.k_chunk = k_chunk_for(K, p.splits_w);
   int sw = (K + g.k_chunk - 1) / g.k_chunk;
   g.split_stride = (size_t)I * H4;
-  if ((rc = launch_gemm(p.prec, GEMM_KM, GEMM_KN, g, sw, st))) return rc;
+  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, sw, st))) return rc;
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, sw, g.split_stride, I,
                      H4, H, dW);
   mark(d, 7, st);
-  // dU = Hprev^T dA, Hprev = the state each step read (gathered through the producer table)
-  void* hp = ws + L.hp;
-  hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0,
-                     bf ? (const bf16_t*)(ws + L.hx) : (const bf16_t*)nullptr, hp, T, B, H);
   memset(&g, 0, sizeof(g));
   g.M = H; g.N = H4; g.K = K;
-  g.A = hp; g.lda = H; g.a_vec = (H % (bf ? 8 : 4) == 0);
-  g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % (bf ? 8 : 4) == 0);
+  if (bf) { g.A = hp; g.lda = K; g.a_vec = (K % 8 == 0); g.Bm = dAt; g.ldb = K; g.b_vec = (K % 8 == 0); }
+  else    { g.A = hp; g.lda = H; g.a_vec = (H % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % 4 == 0); }
   g.C = part; g.ldc = H4;
   g.k_chunk = k_chunk_for(K, p.splits_u);
   int su = (K + g.k_chunk - 1) / g.k_chunk;
   g.split_stride = (size_t)H * H4;
-  if ((rc = launch_gemm(p.prec, GEMM_KM, GEMM_KN, g, su, st))) return rc;
+  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, su, st))) return rc;
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, su, g.split_stride, H,
                      H4, H, dU);
   mark(d, 8, st);

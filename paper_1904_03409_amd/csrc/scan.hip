@@ -126,3 +126,38 @@ __global__ void __launch_bounds__(256) k_gather_hprev(const int32_t* __restrict_
     else ((float*)out)[i] = (s < 0) ? h0[(size_t)b * H + u] : hcell[((size_t)s * B + b) * H + u];
   }
 }
+
+// Tiled transpose to bf16: out[c][r] = bf16(row r, column c) for r < rows, c < cols, where
+// row r is src + r*ld (fp32 or bf16). With a producer table (gtop != null) row r = t*B + b is
+// the state read at step t (Hprev): h0[b] for t = 0, else the state produced at top[t-1][b]
+// (-1 = h0), taken from the bf16 state copy (slot s+1 = step s, slot 0 = h0).
+// 64x64 tiles through LDS: reads and writes are both along contiguous rows.
+__global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__ src, int src_f32, int ld, int rows,
+                                                        int cols, const int32_t* __restrict__ gtop, int B,
+                                                        bf16_t* __restrict__ out) {
+  __shared__ bf16_t tile[64][66];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tc = threadIdx.x & 63, tr = threadIdx.x >> 6;   // 4 rows per pass
+  for (int i = tr; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tc;
+    bf16_t v = 0;
+    if (r < rows && c < cols) {
+      if (gtop) {
+        const int t = r / B, b = r - t * B;
+        int s = (t == 0) ? -1 : gtop[(size_t)r - B];
+        if (s < -1 || s >= t) s = -1;                        // only a valid producer is ever indexed
+        v = ((const bf16_t*)src)[((size_t)(s + 1) * B + b) * ld + c];
+      } else if (src_f32) {
+        v = f32_to_bf16_bits(((const float*)src)[(size_t)r * ld + c]);
+      } else {
+        v = ((const bf16_t*)src)[(size_t)r * ld + c];
+      }
+    }
+    tile[i][tc] = v;
+  }
+  __syncthreads();
+  for (int i = tr; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tc;
+    if (c < cols && r < rows) out[(size_t)c * rows + r] = tile[tc][i];
+  }
+}
