@@ -197,6 +197,12 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L) 
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
   a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
   a.coh_top = ((size_t)d->B * 4) % 128 != 0;
+  // backward direct staging: whole 1 KB row segments, K range equal to the register capacity,
+  // and the LDS slice plus static LDS within one CU (one workgroup per CU)
+  const int KC = rec_kc(d->precision);
+  a.bwd_direct = ((size_t)d->H * esz) % 1024 == 0 && p.KS * KC == d->H && rec_occ(d->precision, p.KS) == 1 &&
+                 rec_bwd_lds_bytes(d->precision, p.KS) + rec_bwd_static_lds(p.NT) <= 160 * 1024 &&
+                 p.per_xcc <= std::max(1, device_cus() / 8);
   return a;
 }
 
@@ -278,8 +284,9 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   GemmArgs g;
   memset(&g, 0, sizeof(g));
   g.M = T * B; g.N = 4 * H; g.K = I;
-  g.A = xa; g.lda = I; g.a_vec = (I % (bf ? 8 : 4) == 0);
-  g.Bm = wp; g.ldb = 4 * H; g.b_vec = (H % 2 == 0) || !bf;
+  const int VE = bf ? 8 : 4;
+  g.A = xa; g.lda = I; g.a_vec = (I % VE == 0);
+  g.Bm = wp; g.ldb = 4 * H; g.b_vec = ((4 * H) % VE == 0);
   g.C = xw; g.ldc = 4 * H; g.bias = b; g.bias_H = H;
   g.k_chunk = k_chunk_for(I, 1); g.split_stride = 0;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_KN, g, 1, st))) return rc;
@@ -374,8 +381,9 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   }
   memset(&g, 0, sizeof(g));
   g.M = I; g.N = H4; g.K = K;
+  const int VE = bf ? 8 : 4;
   if (bf) { g.A = ws + L.xbt; g.lda = K; g.a_vec = (K % 8 == 0); g.Bm = dAt; g.ldb = K; g.b_vec = (K % 8 == 0); }
-  else    { g.A = x; g.lda = I; g.a_vec = (I % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % 4 == 0); }
+  else    { g.A = x; g.lda = I; g.a_vec = (I % 4 == 0) && (K % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (K % 4 == 0); }
   g.C = part; g.ldc = H4;
   g.k_chunk = k_chunk_for(K, p.splits_w);
   int sw = (K + g.k_chunk - 1) / g.k_chunk;
@@ -387,7 +395,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   memset(&g, 0, sizeof(g));
   g.M = H; g.N = H4; g.K = K;
   if (bf) { g.A = hp; g.lda = K; g.a_vec = (K % 8 == 0); g.Bm = dAt; g.ldb = K; g.b_vec = (K % 8 == 0); }
-  else    { g.A = hp; g.lda = H; g.a_vec = (H % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (H4 % 4 == 0); }
+  else    { g.A = hp; g.lda = H; g.a_vec = (H % 4 == 0) && (K % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (K % 4 == 0); }
   g.C = part; g.ldc = H4;
   g.k_chunk = k_chunk_for(K, p.splits_u);
   int su = (K + g.k_chunk - 1) / g.k_chunk;
@@ -399,8 +407,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   // dx = dA Wp^T
   memset(&g, 0, sizeof(g));
   g.M = K; g.N = I; g.K = H4;
-  g.A = a.dA; g.lda = H4; g.a_vec = (H4 % (bf ? 8 : 4) == 0);
-  g.Bm = ws + L.wp; g.ldb = H4; g.b_vec = (H4 % (bf ? 8 : 4) == 0);
+  g.A = a.dA; g.lda = H4; g.a_vec = (H4 % VE == 0);
+  g.Bm = ws + L.wp; g.ldb = H4; g.b_vec = (H4 % VE == 0) && (I % VE == 0);
   g.C = dx; g.ldc = I;
   g.k_chunk = k_chunk_for(H4, 1);
   (void)esz;

@@ -40,9 +40,26 @@ template <int P, bool KMAJOR> struct Stage {
   uint4 v[NV];
 
   // global tile element (r, c): KMAJOR -> row r in [0,BK) of k, col c in [0,128) of m/n;
-  // otherwise row r in [0,128) of m/n, col c in [0,BK) of k
-  __device__ __forceinline__ void load(const T* __restrict__ base, int ld, int r0, int rlim, int c0, int clim,
-                                       bool vec) {
+  // otherwise row r in [0,128) of m/n, col c in [0,BK) of k. The vector path goes through a
+  // bounds-checked buffer descriptor: an element past the row or column limit is given an
+  // offset beyond the buffer, which reads 0 without a branch or a memory access. It needs
+  // the row stride and both limits to be multiples of VE (checked by the host).
+  __device__ __forceinline__ void load(const T* __restrict__ base, size_t bytes, int ld, int r0, int rlim, int c0,
+                                       int clim, bool vec) {
+    if (vec) {
+      const rsrc_t rs = make_rsrc(base, bytes);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int e = threadIdx.x + 256 * i;
+        int r, c;
+        if (KMAJOR) { r = e / (128 / VE); c = (e % (128 / VE)) * VE; }
+        else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
+        const int gr = r0 + r, gc = c0 + c;
+        const uint32_t off = (gr < rlim && gc < clim) ? (uint32_t)(((size_t)gr * ld + gc) * sizeof(T)) : 0xffffffffu;
+        v[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int e = threadIdx.x + 256 * i;
@@ -50,19 +67,10 @@ template <int P, bool KMAJOR> struct Stage {
       if (KMAJOR) { r = e / (128 / VE); c = (e % (128 / VE)) * VE; }
       else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
       const int gr = r0 + r, gc = c0 + c;
-      uint4 x = uint4{0u, 0u, 0u, 0u};
-      if (gr < rlim) {
-        const T* p = base + (size_t)gr * ld + gc;
-        if (vec && gc + VE <= clim) {
-          x = *(const uint4*)p;
-        } else {
-          T tmp[VE];
+      T tmp[VE];
 #pragma unroll
-          for (int j = 0; j < VE; ++j) tmp[j] = (gc + j < clim) ? p[j] : (T)0;
-          x = *(const uint4*)tmp;
-        }
-      }
-      v[i] = x;
+      for (int j = 0; j < VE; ++j) tmp[j] = (gr < rlim && gc + j < clim) ? base[(size_t)gr * ld + gc + j] : (T)0;
+      v[i] = *(const uint4*)tmp;
     }
   }
 
@@ -110,11 +118,13 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
 
   Stage<P, AKM> sa;
   Stage<P, BKN> sb;
+  const size_t abytes = (AKM ? (size_t)g.K * g.lda : (size_t)g.M * g.lda) * sizeof(T);
+  const size_t bbytes = (BKN ? (size_t)g.K * g.ldb : (size_t)g.N * g.ldb) * sizeof(T);
   auto fetch = [&](int k0) {
-    if (AKM) sa.load(A, g.lda, k0, kend, m0, g.M, g.a_vec);
-    else     sa.load(A, g.lda, m0, g.M, k0, kend, g.a_vec);
-    if (BKN) sb.load(Bp, g.ldb, k0, kend, n0, g.N, g.b_vec);
-    else     sb.load(Bp, g.ldb, n0, g.N, k0, kend, g.b_vec);
+    if (AKM) sa.load(A, abytes, g.lda, k0, kend, m0, g.M, g.a_vec);
+    else     sa.load(A, abytes, g.lda, m0, g.M, k0, kend, g.a_vec);
+    if (BKN) sb.load(Bp, bbytes, g.ldb, k0, kend, n0, g.N, g.b_vec);
+    else     sb.load(Bp, bbytes, g.ldb, n0, g.N, k0, kend, g.b_vec);
   };
 
   f32x4 acc[4][4];
@@ -136,26 +146,30 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
     const T* as = As[buf];
     const T* bs = Bs[buf];
     if constexpr (P == 0) {
-#pragma unroll
-      for (int kc = 0; kc < BK / 4; ++kc) {
-        // one MFMA k-step covers k = 4*kc + lq (A and B use the same k for a lane)
-        float av[4], bv[4];
+      // one MFMA k-step covers k = 4*kc + lq (A and B use the same k for a lane); the
+      // fragments of step kc+1 are read from LDS before the MFMAs of step kc
+      auto rd = [&](int kc, float av[4], float bv[4]) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int m = wm * 64 + i * 16 + l16;
-          if (AKM) av[i] = as[(4 * kc + lq) * GA::LD + m];
-          else     av[i] = as[m * GA::LD + 4 * kc + lq];
+          av[i] = AKM ? as[(4 * kc + lq) * GA::LD + m] : as[m * GA::LD + 4 * kc + lq];
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int n = wn * 64 + j * 16 + l16;
-          if (BKN) bv[j] = bs[(4 * kc + lq) * GB::LD + n];
-          else     bv[j] = bs[n * GB::LD + 4 * kc + lq];
+          bv[j] = BKN ? bs[(4 * kc + lq) * GB::LD + n] : bs[n * GB::LD + 4 * kc + lq];
         }
+      };
+      float av[2][4], bv[2][4];
+      rd(0, av[0], bv[0]);
+#pragma unroll
+      for (int kc = 0; kc < BK / 4; ++kc) {
+        const int cur = kc & 1;
+        if (kc + 1 < BK / 4) rd(kc + 1, av[cur ^ 1], bv[cur ^ 1]);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32_16x16x4(av[i], bv[j], acc[i][j]);
+          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32_16x16x4(av[cur][i], bv[cur][j], acc[i][j]);
       }
     } else {
 #pragma unroll

@@ -18,6 +18,11 @@ constexpr int rec_ntb(int prec, int nt, int ks) {
 constexpr size_t rec_lds_bytes(int prec, int ntb, int ks) {
   return (size_t)16 * ntb * rec_lds_ld(prec, ks) * (prec ? 2 : 4);
 }
+// Backward kernel: LDS for the staged dA rows of the direct path (4 waves x 16 rows of the
+// wave's K range); the direct path is used when this plus the static LDS fits one CU.
+constexpr size_t rec_bwd_lds_bytes(int prec, int ks) { return (size_t)4 * 16 * rec_lds_ld(prec, ks) * (prec ? 2 : 4); }
+constexpr size_t rec_bwd_static_lds(int nt) { return (size_t)4 * nt * 16 * 17 * 4 + 16 * 16 * 4 * 4 + 5 * nt * 16 * 4 + 64; }
+
 // Workgroups per CU the kernel is compiled for: 2 for the bf16 H > 512 case (64
 // workgroups per group), 1 otherwise.
 constexpr int rec_occ(int prec, int ks) { return (prec == 1 && ks == 32) ? 2 : 1; }

@@ -10,6 +10,7 @@ struct RecArgs {
   // (rows not 128-byte multiples): then every exchanged value is read with L1-bypassing
   // loads; with aligned rows a line is never read before its only write, plain loads suffice
   int coh_rows, coh_top;
+  int bwd_direct;        // backward stages dA rows with global_load_lds (host checks the LDS fits)
   const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)

@@ -23,6 +23,9 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;
   constexpr int BG = NT * 16;
   constexpr int PAIRS = BG * 16 / 256;            // (row, unit) pairs per thread
+  // staged dA rows (direct path): per wave 16 compacted rows of its H gate columns
+  constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
+  extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ float red[4][BG][17];
   __shared__ int s_op[BG], s_top[BG], s_src[BG], s_crow[BG], s_cidx[BG], s_nlive;
   __shared__ float s_db[16][16][4];
@@ -95,6 +98,12 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
+  const bool direct = a.bwd_direct != 0;
+  typedef __attribute__((address_space(3))) void* lds_ptr_t;
+  using elem_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
+  elem_t* wbuf = reinterpret_cast<elem_t*>(dsm) + (size_t)wave * 16 * QLD;
+  if (direct)
+    for (int i = threadIdx.x; i < 4 * 16 * QLD * ESZ / 16; i += 256) ((uint4*)dsm)[i] = uint4{0u, 0u, 0u, 0u};
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
@@ -268,6 +277,59 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     constexpr int NG = (KS + CG - 1) / CG;
     const uint32_t kOOB = 0xffffffffu;
     const int nlive = s_nlive;
+    if (direct) {
+      // Each wave copies its own H gate columns of the compacted rows straight into its LDS
+      // slice (global_load_lds, 1 KB row segments), waits for its own loads only, and runs
+      // the tile's MFMAs from LDS with the fragments of the next chunk read ahead.
+      constexpr int SEGQ = KS * KC * ESZ / 1024;          // 1 KB segments per staged row
+      for (int jt = 0; jt < NT; ++jt) {
+        if (jt * 16 >= nlive) break;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int ci = jt * 16 + r;
+          if (ci < nlive) {
+            const int b = row0 + s_crow[ci];
+            const elem_t* rowp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H;
+#pragma unroll
+            for (int sj = 0; sj < SEGQ; ++sj) {
+              const elem_t* gp = rowp + sj * (1024 / ESZ) + lane * (16 / ESZ);
+              lds_ptr_t dst = (lds_ptr_t)(wbuf + r * QLD + sj * (1024 / ESZ));
+              if (a.coh_rows) __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, kSc1);
+              else __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, 0);
+            }
+          }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (PREC == 0) {
+          float4 bcur = *(const float4*)&wbuf[l16 * QLD + 4 * lq], bnxt = bcur;
+#pragma unroll
+          for (int c = 0; c < KS; ++c) {
+            if (c + 1 < KS) bnxt = *(const float4*)&wbuf[l16 * QLD + (c + 1) * 16 + 4 * lq];
+            f32x4& acc = (c & 1) ? acc1 : acc0;
+            acc = mfma_f32_16x16x4(ureg32[c][0], bcur.x, acc);
+            acc = mfma_f32_16x16x4(ureg32[c][1], bcur.y, acc);
+            acc = mfma_f32_16x16x4(ureg32[c][2], bcur.z, acc);
+            acc = mfma_f32_16x16x4(ureg32[c][3], bcur.w, acc);
+            bcur = bnxt;
+          }
+        } else {
+          bf16x8 bcur = *(const bf16x8*)&wbuf[l16 * QLD + 8 * lq], bnxt = bcur;
+#pragma unroll
+          for (int c = 0; c < KS; ++c) {
+            if (c + 1 < KS) bnxt = *(const bf16x8*)&wbuf[l16 * QLD + (c + 1) * 32 + 8 * lq];
+            f32x4& acc = (c & 1) ? acc1 : acc0;
+            acc = mfma_bf16_16x16x32(ureg16[c], bcur, acc);
+            bcur = bnxt;
+          }
+        }
+        const int ci = jt * 16 + l16;
+        if (ci < nlive) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) red[wave][ci][4 * lq + j] = acc0[j] + acc1[j];
+        }
+      }
+    } else
     for (int jt = 0; jt < NT; ++jt) {
       if (jt * 16 >= nlive) break;
       const int ci = jt * 16 + l16;
@@ -386,14 +448,17 @@ template <int P, int NT, int KS>
 static hipError_t launch_bwd_t(const RecArgs& a, dim3 grid, hipStream_t st, int* occ_out) {
   constexpr int OCC = rec_occ(P, KS);
   auto kern = k_bwd<P, NT, KS, OCC>;
+  const size_t shm = a.bwd_direct ? rec_bwd_lds_bytes(P, KS) : 0;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+  if (e != hipSuccess) return e;
   int occ = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, 0);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, shm);
   if (e != hipSuccess) return e;
   if (occ_out) *occ_out = occ;
   if (!grid.x) return hipSuccess;
   RecArgs args = a;
   void* kargs[] = {&args};
-  return hipLaunchCooperativeKernel((const void*)kern, grid, dim3(256), kargs, 0, st);
+  return hipLaunchCooperativeKernel((const void*)kern, grid, dim3(256), kargs, (unsigned)shm, st);
 }
 
 hipError_t launch_bwd(const RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out) {

@@ -139,6 +139,16 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     float cp_nxt[NT];
     int tp_next = 0;
 
+    if constexpr (PREC == 1) {
+      // bf16 steps are short: the next step's input projection (HBM) and producer indices are
+      // requested before the staging loads, so their latency overlaps the staging instead of
+      // following it (vector loads complete in issue order)
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti) src_nxt[ti] = top_at(t, ti);
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
+      asm volatile("" ::: "memory");
+    }
 #pragma unroll
     for (int nb = 0; nb < NPASS; ++nb) {
       // ---- gather this pass's h_prev rows into LDS
@@ -222,10 +232,10 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         }
       }
       asm volatile("" ::: "memory");
-      if (nb == 0) {
-        // producers read at step t+1 (top[t], written one step ago) and the next step's
-        // input projection: in flight during this step; the wait below leaves exactly
-        // these 2*NT loads outstanding
+      if (nb == 0 && PREC == 0) {
+        // fp32 steps are long: producers read at step t+1 (top[t], written one step ago) and
+        // the next step's input projection stay in flight during the MFMAs; the wait below
+        // leaves exactly these 2*NT loads outstanding
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) src_nxt[ti] = top_at(t, ti);
 #pragma unroll
