@@ -19,6 +19,7 @@ __global__ void k_gather_top(const int32_t* top, const float* cellv, const float
 __global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
+__global__ void k_fill_pattern(unsigned char* p, size_t bytes, uint32_t v);
 __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
 __global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const bf16_t* hx, void* out,
@@ -296,6 +297,15 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   RecArgs a = rec_args(d, p, ws, L);
   if (bf) hipLaunchKernelGGL(k_h0_bf16, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, h0, (bf16_t*)a.hx, (size_t)B * H);
   a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
+  // exchange buffers start as "not yet produced": all-one bits in the state rows the
+  // workgroups read from each other, kTopPending in the producer-index table
+  {
+    const size_t ex_bytes = (size_t)T * B * H * (bf ? 2 : 4);
+    unsigned char* ex = bf ? (unsigned char*)(a.hx + (size_t)B * H) : (unsigned char*)h_cell;
+    hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(ex_bytes / 16 + 1)), dim3(256), 0, st, ex, ex_bytes, 0xffffffffu);
+    hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st, (unsigned char*)top,
+                       (size_t)T * B * 4, kTopPending);
+  }
   if ((rc = hip_status(launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
   mark(d, 3, st);
 

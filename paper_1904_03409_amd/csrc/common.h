@@ -82,6 +82,48 @@ __device__ __forceinline__ uint16_t ld_coh_b16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, kSc1);
 }
 
+// Barrier-free exchange of states between the workgroups of one XCC. Before the kernel
+// the exchanged rows are filled with all-one bits (a NaN no producer ever stores: produced
+// NaNs are stored as the canonical quiet NaN) and the producer-index table with
+// kTopPending; a consumer reads a row, and re-reads every 16-byte granule that still holds
+// the fill, with agent-scope atomic loads (never hoisted or merged by the compiler, and
+// they miss in this CU's L1), until the producer's store has reached the XCC's L2.
+constexpr uint32_t kTopPending = 0x80000000u;
+__device__ __forceinline__ bool pending_f32x4(uint4 v) {
+  return v.x == 0xffffffffu || v.y == 0xffffffffu || v.z == 0xffffffffu || v.w == 0xffffffffu;
+}
+__device__ __forceinline__ bool pending_bf16_word(uint32_t w) {
+  return (w & 0xffffu) == 0xffffu || (w >> 16) == 0xffffu;
+}
+__device__ __forceinline__ bool pending_bf16x8(uint4 v) {
+  return pending_bf16_word(v.x) || pending_bf16_word(v.y) || pending_bf16_word(v.z) || pending_bf16_word(v.w);
+}
+template <int PREC>
+__device__ __forceinline__ bool pending_granule(uint4 v) {
+  if constexpr (PREC == 0) return pending_f32x4(v);
+  else return pending_bf16x8(v);
+}
+__device__ __forceinline__ uint4 ld_poll_b128(const void* p) {
+  const uint64_t* q = (const uint64_t*)p;
+  uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return uint4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
+}
+__device__ __forceinline__ float canon_nan(float h) { return h == h ? h : __builtin_nanf(""); }
+
+// Bounded wait: counts failed polls of one wait; gives up (returns true) when the count
+// reaches the limit, raising the abort and time-out flags, or when another workgroup has
+// raised the abort flag.
+__device__ __forceinline__ bool spin_out(int& spins, uint32_t* ctl, int spin_limit) {
+  ++spins;
+  if (spins >= spin_limit) {
+    __hip_atomic_store(&ctl[CTL_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&ctl[CTL_TIMEOUT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+  }
+  return (spins & 255) == 0 && __hip_atomic_load(&ctl[CTL_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Group barrier for workgroups that all run on one XCC (one shared L2).
 // Each wave waits until its own stores are acknowledged by L2, the workgroup meets at
 // s_barrier, one lane adds to the group counter and polls it with L1-bypassing loads.

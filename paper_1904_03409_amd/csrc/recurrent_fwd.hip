@@ -22,6 +22,15 @@
 #include "recurrent.h"
 #include "rec_config.h"
 
+// Source of one staged granule: the state of step src (h0 for src = -1) of batch row b, column k.
+template <int PREC>
+__device__ __forceinline__ const void* staged_src(const RecArgs& a, int src, int b, int k) {
+  if constexpr (PREC == 0)
+    return (src < 0) ? (const void*)(a.h0 + (size_t)b * a.H + k)
+                     : (const void*)(a.hcell + ((size_t)src * a.B + b) * a.H + k);
+  else return (const void*)(a.hx + ((size_t)(src + 1) * a.B + b) * a.H + k);
+}
+
 template <int PREC, int NT, int NTB, int KS, int OCC>
 __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;               // K per chunk
@@ -36,7 +45,8 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   elem_t* hs = reinterpret_cast<elem_t*>(smem);
   __shared__ int s_src[BG];
-  __shared__ int s_g, s_w, s_flag;
+  __shared__ int s_g, s_w;
+  __shared__ int s_abort[2];   // [0]: a staging wait gave up, [1]: a producer-index wait gave up
 
   claim_group_slot(a.ctl + CTL_XCC_SLOT, a.G, a.NW, &s_g, &s_w);
   const int g = s_g, w = s_w;
@@ -84,7 +94,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   const int kmax = ks_eff * KC;                    // staged K (>= H)
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
   const bool direct = vec_ok && kmax == KP && (KP * ESZ) % 1024 == 0;
-  const int seg_per_row = (kmax * ESZ) / 1024;
 
   // rows of this lane in the MFMA output layout: tile ti covers rows ti*16 .. ti*16+15
   int lrow[NT];
@@ -115,6 +124,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     a.top[my_row] = my_top;
   }
   if ((int)threadIdx.x < BG) s_src[threadIdx.x] = -1;
+  if (threadIdx.x < 2) s_abort[threadIdx.x] = 0;
   constexpr int NV = (BG + 63) / 64;
   int vsrc[NV];
 #pragma unroll
@@ -128,9 +138,16 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     xw_cur[ti] = xw_at(0, ti);
     cp_cur[ti] = lok[ti] ? a.c0[(size_t)lrow[ti] * H + u] : 0.f;
   }
-  if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)a.NW, a.ctl, a.spin_limit, &s_flag)) return;
+  __syncthreads();
 
+  // Direct staging: one wave instruction moves one 1 KB segment of one row into LDS, 16 bytes
+  // per lane. Segment i of this wave is row segment wave + 4 i of the pass; the row's producer
+  // comes from lane rr of vsrc (wave-uniform), no LDS round trip.
+  constexpr int SEG = (KP * ESZ) / 1024 > 0 ? (KP * ESZ) / 1024 : 1;
+  constexpr int NSEG_W = (ROWS_B * SEG + 3) / 4;
+  static_assert(NSEG_W <= 32, "segment mask is 32 bits");
   long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
+  bool stop = false;
   for (int t = 0; t < T; ++t) {
     if (clk && threadIdx.x == 0) clk[t * 4 + 0] = wall_clock64();
     const bool more = t + 1 < T;
@@ -151,29 +168,22 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     }
 #pragma unroll
     for (int nb = 0; nb < NPASS; ++nb) {
-      // ---- gather this pass's h_prev rows into LDS
+      // ---- gather this pass's h_prev rows into LDS; granules that still hold the fill are
+      // fetched again until their producers' stores have arrived
       if (direct) {
-        // one wave instruction moves one 1 KB segment of one row (16 bytes per lane);
-        // the row's producer comes from lane rr of vsrc (wave-uniform), no LDS round trip
-        constexpr int SEG = KP * ESZ / 1024;
-        constexpr int NSEG_W = (ROWS_B * SEG + 3) / 4;
 #pragma unroll
         for (int i = 0; i < NSEG_W; ++i) {
           const int sgi = wave + 4 * i;
           if (sgi < ROWS_B * SEG) {
-            const int r = sgi / SEG, sj = sgi % SEG;
-            const int rr = nb * ROWS_B + r;
-            const int b = min(row0 + rr, B - 1);  // rows past B: any finite row (columns masked)
+            const int r = sgi / SEG, sj = sgi % SEG, rr = nb * ROWS_B + r;
             const int src = __builtin_amdgcn_readlane(vsrc[rr >> 6], rr & 63);
             int k = sj * (1024 / ESZ) + lane * (16 / ESZ);
             if (k >= H) k = 0;                    // finite filler; the U registers are 0 there
-            const elem_t* gp;
-            if constexpr (PREC == 0) gp = (src < 0) ? (const elem_t*)(a.h0 + (size_t)b * H + k)
-                                                    : (const elem_t*)(a.hcell + ((size_t)src * B + b) * H + k);
-            else gp = (const elem_t*)(a.hx + ((size_t)(src + 1) * B + b) * H + k);
-            lds_ptr_t dst = (lds_ptr_t)(hs + r * LDS_LD + sj * (1024 / ESZ));
-            if (a.coh_rows) __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, kSc1);
-            else __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, 0);
+            elem_t* lp = hs + r * LDS_LD + sj * (1024 / ESZ);
+            // rows past B: any finite row (their columns are masked)
+            const void* gp = staged_src<PREC>(a, src, min(row0 + rr, B - 1), k);
+            if (a.coh_rows) __builtin_amdgcn_global_load_lds(gp, (lds_ptr_t)lp, 16, 0, kSc1);
+            else __builtin_amdgcn_global_load_lds(gp, (lds_ptr_t)lp, 16, 0, 0);
           }
         }
       } else {
@@ -184,24 +194,42 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
           const int n_el = ROWS_B * per_row;
           for (int e0 = 0; e0 < n_el; e0 += 4 * 256) {
             uint4 buf[4];
+            const void* pp[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int e = e0 + threadIdx.x + 256 * i;
               buf[i] = uint4{0u, 0u, 0u, 0u};
+              pp[i] = nullptr;
               if (e >= n_el) continue;
               const int r = e / per_row, k = (e - r * per_row) * VW;
               const int rr = nb * ROWS_B + r, b = row0 + rr;
               if (b >= B || k >= H) continue;
               const int src = s_src[rr];
               if constexpr (PREC == 0) {
+                if (src < 0) {
+                  buf[i] = *(const uint4*)(a.h0 + (size_t)b * H + k);
+                  continue;
+                }
                 const size_t e2 = ((size_t)src * B + b) * H + k;
-                if (src < 0) buf[i] = *(const uint4*)(a.h0 + (size_t)b * H + k);
-                else if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 4));
+                pp[i] = a.hcell + e2;
+                if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 4));
                 else buf[i] = *(const uint4*)(a.hcell + e2);
               } else {
                 const size_t e2 = ((size_t)(src + 1) * B + b) * H + k;
+                if (src >= 0) pp[i] = a.hx + e2;
                 if (a.coh_rows) buf[i] = ld_coh_b128(r_h, (uint32_t)(e2 * 2));
                 else buf[i] = *(const uint4*)(a.hx + e2);
+              }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              int spins = 0;
+              while (pp[i] && pending_granule<PREC>(buf[i])) {
+                if (spin_out(spins, a.ctl, a.spin_limit)) {
+                  s_abort[0] = 1;
+                  break;
+                }
+                buf[i] = ld_poll_b128(pp[i]);
               }
             }
 #pragma unroll
@@ -219,11 +247,36 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
             float v = 0.f;
             if (b < B && k < H) {
               const int src = s_src[rr];
+              int spins = 0;
               if constexpr (PREC == 0) {
-                if (src < 0) v = a.h0[(size_t)b * H + k];
-                else v = __uint_as_float(ld_coh_b32(r_h, (uint32_t)((((size_t)src * B + b) * H + k) * 4)));
+                if (src < 0) {
+                  v = a.h0[(size_t)b * H + k];
+                } else {
+                  const size_t e2 = ((size_t)src * B + b) * H + k;
+                  uint32_t bits = ld_coh_b32(r_h, (uint32_t)(e2 * 4));
+                  while (bits == 0xffffffffu) {
+                    if (spin_out(spins, a.ctl, a.spin_limit)) {
+                      s_abort[0] = 1;
+                      break;
+                    }
+                    bits = __hip_atomic_load((uint32_t*)(a.hcell + e2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                  }
+                  v = __uint_as_float(bits);
+                }
               } else {
-                v = bf16_bits_to_f32(ld_coh_b16(r_h, (uint32_t)((((size_t)(src + 1) * B + b) * H + k) * 2)));
+                const size_t e2 = ((size_t)(src + 1) * B + b) * H + k;
+                uint32_t bits = ld_coh_b16(r_h, (uint32_t)(e2 * 2));
+                while (src >= 0 && bits == 0xffffu) {
+                  if (spin_out(spins, a.ctl, a.spin_limit)) {
+                    s_abort[0] = 1;
+                    break;
+                  }
+                  // the aligned word that holds the element
+                  const uint32_t wv = __hip_atomic_load((uint32_t*)(a.hx + (e2 & ~(size_t)1)), __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+                  bits = (e2 & 1) ? (wv >> 16) : (wv & 0xffffu);
+                }
+                v = bf16_bits_to_f32((bf16_t)bits);
               }
             }
             if constexpr (PREC == 0) hs[r * LDS_LD + k] = v;
@@ -231,23 +284,68 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
           }
         }
       }
-      asm volatile("" ::: "memory");
-      if (nb == 0 && PREC == 0) {
-        // fp32 steps are long: producers read at step t+1 (top[t], written one step ago) and
-        // the next step's input projection stay in flight during the MFMAs; the wait below
-        // leaves exactly these 2*NT loads outstanding
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (direct) {
+        // granules that still hold the fill: the wave fetches their 1 KB segments again,
+        // bypassing L1, until every producer's store has arrived
+        uint32_t bad = 0;
+#pragma unroll
+        for (int i = 0; i < NSEG_W; ++i) {
+          const int sgi = wave + 4 * i;
+          if (sgi < ROWS_B * SEG) {
+            const int r = sgi / SEG, sj = sgi % SEG, rr = nb * ROWS_B + r;
+            const int src = __builtin_amdgcn_readlane(vsrc[rr >> 6], rr & 63);
+            const elem_t* lp = hs + r * LDS_LD + sj * (1024 / ESZ);
+            if (src >= 0 && pending_granule<PREC>(*(const uint4*)(lp + lane * (16 / ESZ)))) bad |= 1u << i;
+          }
+        }
+        int spins = 0;
+        while (__builtin_amdgcn_ballot_w64(bad != 0u)) {
+          if (spin_out(spins, a.ctl, a.spin_limit)) {
+            s_abort[0] = 1;
+            break;
+          }
+#pragma unroll
+          for (int i = 0; i < NSEG_W; ++i) {
+            const int sgi = wave + 4 * i;
+            if (sgi < ROWS_B * SEG && __builtin_amdgcn_ballot_w64(((bad >> i) & 1u) != 0u)) {
+              const int r = sgi / SEG, sj = sgi % SEG, rr = nb * ROWS_B + r;
+              const int src = __builtin_amdgcn_readlane(vsrc[rr >> 6], rr & 63);
+              int k = sj * (1024 / ESZ) + lane * (16 / ESZ);
+              if (k >= H) k = 0;                      // finite filler; the U registers are 0 there
+              elem_t* lp = hs + r * LDS_LD + sj * (1024 / ESZ);
+              const void* gp = staged_src<PREC>(a, src, min(row0 + rr, B - 1), k);
+              __builtin_amdgcn_global_load_lds(gp, (lds_ptr_t)lp, 16, 0, kSc1);
+            }
+          }
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+          for (int i = 0; i < NSEG_W; ++i) {
+            const int sgi = wave + 4 * i;
+            if (sgi < ROWS_B * SEG && ((bad >> i) & 1u)) {
+              const int r = sgi / SEG, sj = sgi % SEG;
+              const elem_t* lp = hs + r * LDS_LD + sj * (1024 / ESZ);
+              if (!pending_granule<PREC>(*(const uint4*)(lp + lane * (16 / ESZ)))) bad &= ~(1u << i);
+            }
+          }
+        }
+      }
+      __syncthreads();
+      if (s_abort[0]) {
+        stop = true;
+        break;
+      }
+      if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 1] = wall_clock64();
+      if (PREC == 0 && nb == 0) {
+        // fp32 steps are long: the producer indices read at step t+1 (top[t], published one
+        // step ago) and the next step's input projection are in flight during the MFMAs
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) src_nxt[ti] = top_at(t, ti);
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NT) : "memory");
-      } else {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       }
-      __syncthreads();
-      if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 1] = wall_clock64();
 
-      // trace for step t+1 (stack[p+1] <- t+1, p <- p + op, top <- stack[p]), stored before the barrier
+      // trace for step t+1 (stack[p+1] <- t+1, p <- p + op, top <- stack[p]), published at the end of the step
       if (nb == 0 && tracer && more) {
         int op = op_next;
         op_next = (t + 2 < T) ? a.ops[(size_t)(t + 2) * B + my_row] : 0;
@@ -309,7 +407,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         const float gg = tanhf(acc[nt][2] + xw_cur[ti].z);
         const float go = sigmoidf_(acc[nt][3] + xw_cur[ti].w);
         const float c = gf * cp_cur[ti] + gi * gg;
-        const float h = go * tanhf(c);
+        const float h = canon_nan(go * tanhf(c));     // never the all-ones fill pattern
         const size_t o = ((size_t)t * B + b) * H + u;
         a.hcell[o] = h;
         a.ccell[o] = c;
@@ -319,7 +417,25 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       }
       if (NPASS > 1) __syncthreads();
     }
+    if (stop) break;
 
+    // producers of step t+1: published by the tracer at the end of step t-1
+    if (more) {
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti) {
+        int s = src_nxt[ti];
+        int spins = 0;
+        while (s == (int)kTopPending) {
+          if (spin_out(spins, a.ctl, a.spin_limit)) {
+            s_abort[1] = 1;
+            break;
+          }
+          const int b = lrow[ti] < B ? lrow[ti] : 0;
+          s = (int)__hip_atomic_load((uint32_t*)a.top + (size_t)t * B + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        src_nxt[ti] = s;
+      }
+    }
     // c_prev of step t+1: the state produced now (push at t) or an older one of this workgroup
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) {
@@ -337,7 +453,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       a.top[(size_t)(t + 1) * B + my_row] = tp_next;
       my_top = tp_next;
     }
-    if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_flag)) break;
     if (wave == 0 && lq == 0) {
 #pragma unroll
       for (int ti = 0; ti < NT; ++ti) s_src[ti * 16 + l16] = src_nxt[ti];
@@ -345,6 +460,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) { xw_cur[ti] = xw_nxt[ti]; cp_cur[ti] = cp_nxt[ti]; }
     __syncthreads();
+    if (s_abort[1]) break;
 #pragma unroll
     for (int j = 0; j < NV; ++j) vsrc[j] = (64 * j + lane < BG) ? s_src[64 * j + lane] : -1;
   }

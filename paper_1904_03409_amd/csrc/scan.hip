@@ -93,6 +93,24 @@ __global__ void __launch_bounds__(256) k_fill_f32(float* __restrict__ p, size_t 
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
+// Fills `bytes` bytes at p with the 32-bit pattern v (repeated; p and bytes multiples of 2 when
+// the pattern's halves are equal, of 4 otherwise): 16-byte stores over the aligned middle.
+__global__ void __launch_bounds__(256) k_fill_pattern(unsigned char* __restrict__ p, size_t bytes, uint32_t v) {
+  const uintptr_t a0 = (uintptr_t)p;
+  size_t head = (size_t)((16 - (a0 & 15)) & 15);
+  if (head > bytes) head = bytes;
+  const size_t nvec = (bytes - head) / 16;
+  const size_t tail0 = head + nvec * 16;
+  const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, nth = (size_t)gridDim.x * blockDim.x;
+  uint4* q = (uint4*)(p + head);
+  for (size_t i = tid; i < nvec; i += nth) q[i] = uint4{v, v, v, v};
+  // edges in 16-bit pieces, taken from the pattern at the piece's address
+  for (size_t i = tid * 2; i < head; i += nth * 2)
+    *(uint16_t*)(p + i) = (uint16_t)(v >> (8 * ((a0 + i) & 2)));
+  for (size_t i = tail0 + tid * 2; i < bytes; i += nth * 2)
+    *(uint16_t*)(p + i) = (uint16_t)(v >> (8 * ((a0 + i) & 2)));
+}
+
 __global__ void __launch_bounds__(256) k_zero_u32(uint32_t* __restrict__ p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
 }
