@@ -50,7 +50,8 @@ typedef enum {
   SLSTM_EWORKSPACE = 4,    /* ws_bytes < stacklstm_workspace_bytes(dims) */
   SLSTM_ENORESIDENT = 5,   /* the persistent kernels cannot be made co-resident */
   SLSTM_EDEVICE = 6,       /* a HIP runtime error */
-  SLSTM_ETIMEOUT = 7       /* a group barrier exceeded dims->spin_limit polls */
+  SLSTM_ETIMEOUT = 7       /* a wait for another workgroup's data exceeded dims->spin_limit
+                              failed polls */
 } slstm_status;
 
 typedef enum {
@@ -66,7 +67,8 @@ typedef struct {
   int32_t I;               /* input size */
   int32_t H;               /* hidden size */
   int32_t precision;       /* slstm_precision */
-  int32_t spin_limit;      /* 0 = default barrier spin limit; > 0 = debug limit + final sync */
+  int32_t spin_limit;      /* 0 = default limit of failed polls per wait; > 0 = debug limit +
+                              final sync */
   void* phase_events;      /* NULL, or an array of SLSTM_PHASE_EVENTS hipEvent_t created by the
                               caller; the calls record them on `stream` between their phases:
                               fwd [0] start, [1] after the op scan and its status read-back,
@@ -78,7 +80,7 @@ typedef struct {
                               persistent kernels store 100 MHz wall-clock stamps per workgroup
                               and step, [pass (0 fwd, 1 bwd)][workgroup][t][4], at four points of
                               each step (forward: loop top, h_prev staged, MFMA done, epilogue
-                              done; backward: loop top, epilogue done, barrier passed, dh
+                              done; backward: loop top, epilogue done, row list ready, dh
                               scattered). For profiling only. */
 } slstm_dims;
 
@@ -119,14 +121,16 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                   float* dU, float* db, float* dh0, float* dc0, void* stream);
 
 /* Synchronises `stream` and reports SLSTM_ETIMEOUT if a persistent kernel of the last
- * call on `workspace` gave up on a group barrier, SLSTM_OK otherwise. */
+ * call on `workspace` gave up waiting for data of another workgroup (spin limit),
+ * SLSTM_OK otherwise. */
 int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream);
 
 /* Static text for a status code. */
 const char* stacklstm_status_string(int status);
 
-/* Launch configuration chosen for `d`: fills groups, workgroups per group, rows per
- * group and K chunks; returns a status like the entry points. Informational. */
+/* Launch configuration of the forward recurrent kernel chosen for `d`: fills groups,
+ * workgroups per group, rows per group and K chunks (the backward kernel may use larger
+ * groups); returns a status like the entry points. Informational. */
 int stacklstm_plan(const slstm_dims* d, int32_t* groups, int32_t* wg_per_group, int32_t* rows_per_group,
                    int32_t* k_chunks);
 

@@ -54,8 +54,13 @@ int device_cus() {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Rows per group are chosen per kernel (forward and backward differ in register use and so
+// in how many workgroups share a CU): NT/G/per_xcc for the forward, NTb/Gb/per_xcc_b for
+// the backward.
 struct Plan {
-  int prec, KS, ks_eff, NT, G, NW, per_xcc;
+  int prec, KS, ks_eff, NW;
+  int NT, G, per_xcc;
+  int NTb, Gb, per_xcc_b;
   int splits_w, splits_u;
 };
 
@@ -102,27 +107,35 @@ int make_plan(const slstm_dims* d, Plan* p) {
   p->NW = (d->H + 15) / 16;
   const int cus = device_cus();
   const int cu_per_xcc = cus > 0 ? cus / 8 : 32;
-  for (int NT = 1; NT <= 8; NT *= 2) {
-    int G = (d->B + 16 * NT - 1) / (16 * NT);
-    if (G > MAX_GROUPS) continue;
-    int per_xcc = p->NW * ((G + 7) / 8);
-    int occ_f = 0, occ_b = 0;
-    RecArgs dummy;
-    memset(&dummy, 0, sizeof(dummy));
-    if (launch_fwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ_f) != hipSuccess) return SLSTM_EDEVICE;
-    if (launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ_b) != hipSuccess) return SLSTM_EDEVICE;
-    int occ = std::min(occ_f, occ_b);
-    if (per_xcc <= cu_per_xcc * occ) {
-      p->NT = NT;
-      p->G = G;
-      p->per_xcc = per_xcc;
-      int64_t K = (int64_t)d->T * d->B;
-      p->splits_w = splits_for(d->I, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
-      p->splits_u = splits_for(d->H, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
-      return SLSTM_OK;
+  // smallest row tile count per group whose workgroups (NW per group, groups dealt to the 8
+  // XCCs round-robin) are co-resident on one XCC at the kernel's occupancy
+  auto pick = [&](bool bwd, int* NT_out, int* G_out, int* per_out) -> int {
+    for (int NT = 1; NT <= 8; NT *= 2) {
+      int G = (d->B + 16 * NT - 1) / (16 * NT);
+      if (G > MAX_GROUPS) continue;
+      int per_xcc = p->NW * ((G + 7) / 8);
+      int occ = 0;
+      RecArgs dummy;
+      memset(&dummy, 0, sizeof(dummy));
+      hipError_t e = bwd ? launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
+                         : launch_fwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
+      if (e != hipSuccess) return SLSTM_EDEVICE;
+      if (per_xcc <= cu_per_xcc * occ) {
+        *NT_out = NT;
+        *G_out = G;
+        *per_out = per_xcc;
+        return SLSTM_OK;
+      }
     }
-  }
-  return SLSTM_ENORESIDENT;
+    return SLSTM_ENORESIDENT;
+  };
+  int rc = pick(false, &p->NT, &p->G, &p->per_xcc);
+  if (rc) return rc;
+  if ((rc = pick(true, &p->NTb, &p->Gb, &p->per_xcc_b))) return rc;
+  int64_t K = (int64_t)d->T * d->B;
+  p->splits_w = splits_for(d->I, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
+  p->splits_u = splits_for(d->H, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
+  return SLSTM_OK;
 }
 
 // Work-space layout; splits are bounded by 64 so the layout does not depend on the device.
@@ -184,17 +197,23 @@ int check_timeout(const uint32_t* ctl, hipStream_t st) {
   return v ? SLSTM_ETIMEOUT : SLSTM_OK;
 }
 
-RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L) {
+RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, bool bwd) {
   RecArgs a;
   memset(&a, 0, sizeof(a));
   a.T = d->T; a.B = d->B; a.I = d->I; a.H = d->H;
-  a.G = p.G; a.NW = p.NW; a.ks_eff = p.ks_eff;
+  a.G = bwd ? p.Gb : p.G; a.NW = p.NW; a.ks_eff = p.ks_eff;
   a.spin_limit = d->spin_limit > 0 ? d->spin_limit : kDefaultSpin;
   a.ctl = (uint32_t*)(ws + L.ctl);
   a.stack = (int32_t*)(ws + L.stack);
   a.stash = (float*)(ws + L.stash);
   a.hx = d->precision == SLSTM_BF16_GEMM ? (uint16_t*)(ws + L.hx) : nullptr;
   a.clk = (long long*)d->step_clock;
+  // Exchange protocol (measured on the large parser workload): in bf16 mode a step is short
+  // and a group barrier's fixed cost (store acknowledgement, then an atomic and a poll round
+  // trip) dominates it, so the workgroups poll the fill-marked rows instead; in fp32 mode the
+  // rows are twice as long, checking a staged tile for the fill pattern costs more than the
+  // barrier, and the backward's fill of dA is a large write, so fp32 keeps the barrier.
+  a.poll = d->precision == SLSTM_BF16_GEMM ? 1 : 0;
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
   a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
   a.coh_top = ((size_t)d->B * 4) % 128 != 0;
@@ -202,8 +221,8 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L) 
   // and the LDS slice plus static LDS within one CU (one workgroup per CU)
   const int KC = rec_kc(d->precision);
   a.bwd_direct = ((size_t)d->H * esz) % 1024 == 0 && p.KS * KC == d->H && rec_occ(d->precision, p.KS) == 1 &&
-                 rec_bwd_lds_bytes(d->precision, p.KS) + rec_bwd_static_lds(p.NT) <= 160 * 1024 &&
-                 p.per_xcc <= std::max(1, device_cus() / 8);
+                 rec_bwd_lds_bytes(d->precision, p.KS) + rec_bwd_static_lds(p.NTb) <= 160 * 1024 &&
+                 p.per_xcc_b <= std::max(1, device_cus() / 8);
   return a;
 }
 
@@ -225,7 +244,7 @@ const char* stacklstm_status_string(int s) {
     case SLSTM_EWORKSPACE: return "work space too small";
     case SLSTM_ENORESIDENT: return "persistent kernels cannot be co-resident";
     case SLSTM_EDEVICE: return "HIP runtime error";
-    case SLSTM_ETIMEOUT: return "group barrier spin limit exceeded";
+    case SLSTM_ETIMEOUT: return "a wait for another workgroup's data exceeded the spin limit";
     default: return "unknown status";
   }
 }
@@ -294,12 +313,12 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   mark(d, 2, st);
 
   // a3-a6: persistent recurrent kernel
-  RecArgs a = rec_args(d, p, ws, L);
+  RecArgs a = rec_args(d, p, ws, L, false);
   if (bf) hipLaunchKernelGGL(k_h0_bf16, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, h0, (bf16_t*)a.hx, (size_t)B * H);
   a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
   // exchange buffers start as "not yet produced": all-one bits in the state rows the
   // workgroups read from each other, kTopPending in the producer-index table
-  {
+  if (a.poll) {
     const size_t ex_bytes = (size_t)T * B * H * (bf ? 2 : 4);
     unsigned char* ex = bf ? (unsigned char*)(a.hx + (size_t)B * H) : (unsigned char*)h_cell;
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(ex_bytes / 16 + 1)), dim3(256), 0, st, ex, ex_bytes, 0xffffffffu);
@@ -352,7 +371,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_XCC_SLOT_B, 16);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_BAR_B, 16 * MAX_GROUPS);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_ABORT, 2);
-  RecArgs a = rec_args(d, p, ws, L);
+  RecArgs a = rec_args(d, p, ws, L, true);
   a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0;
   a.hcell = const_cast<float*>(h_cell); a.ccell = const_cast<float*>(c_cell); a.top = const_cast<int32_t*>(top);
   a.dh_top = dh_top; a.dc_top = dc_top;
@@ -361,13 +380,19 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   a.db_part = (float*)(ws + L.dbp);
   a.dh0 = dh0; a.dc0 = dc0;
   if (a.clk) a.clk += (size_t)512 * T * 4;
-  if ((rc = hip_status(launch_bwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
+  // dA rows start as "not yet produced" (all-one bits): the workgroups read them from each other
+  if (a.poll) {
+    const size_t da_bytes = (size_t)T * B * 4 * H * (bf ? 2 : 4);
+    hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(da_bytes / 16 + 1)), dim3(256), 0, st, (unsigned char*)a.dA,
+                       da_bytes, 0xffffffffu);
+  }
+  if ((rc = hip_status(launch_bwd(a, p.prec, p.NTb, p.KS, dim3(8 * p.per_xcc_b), st, nullptr)))) return rc;
   mark(d, 6, st);
 
   // a9: post-loop gradients
   const int H4 = 4 * H;
   float* part = (float*)(ws + L.part);
-  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H4)), dim3(256), 0, st, a.db_part, p.G, (size_t)H4, 1, H4,
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H4)), dim3(256), 0, st, a.db_part, p.Gb, (size_t)H4, 1, H4,
                      H, db);
   const int K = T * B;
   const size_t esz = bf ? 2 : 4;

@@ -11,6 +11,7 @@ struct RecArgs {
   // loads; with aligned rows a line is never read before its only write, plain loads suffice
   int coh_rows, coh_top;
   int bwd_direct;        // backward stages dA rows with global_load_lds (host checks the LDS fits)
+  int poll;              // 1: workgroups exchange rows by polling fill-marked data; 0: group barrier per step
   const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)

@@ -8,12 +8,14 @@
 //   non-push t:  dh_acc[top+1] += dh_top[t], dc_acc[top+1] += dc_top[t]; dA[t] = 0
 //   push t:      dh = dh_acc[t+1] + dh_top[t], dc = dc_acc[t+1] + dc_top[t] + dh o (1 - tanh^2 c)
 //                dA = (dc g i(1-i), dc c_prev f(1-f), dc i (1-g^2), dh tanh(c) o(1-o))
-//                dc_acc[src+1] += dc f;   [group barrier]   dh_acc[src+1] += dA U^T
+//                dc_acc[src+1] += dc f;   dh_acc[src+1] += dA U^T
 // Same work split as the forward: group of 16*NT rows on one XCC, workgroup w owns
 // hidden units [16w, 16w+16). dA U^T needs all 4H gate columns, so dA is exchanged
-// through L2 at the barrier; wave q contracts gate columns [qH, (q+1)H) against its
-// register-resident slice of U and the four partial sums are added in LDS in a fixed
-// order. Every dh_acc/dc_acc element is owned by one thread, so there are no atomics.
+// through L2 without a group barrier: dA starts filled with all-one bits, and a reader
+// fetches again every granule that still holds them. Wave q contracts gate columns
+// [qH, (q+1)H) against its register-resident slice of U and the four partial sums are
+// added in LDS in a fixed order. Every dh_acc/dc_acc element is owned by one thread, so
+// there are no atomics.
 #include "common.h"
 #include "recurrent.h"
 #include "rec_config.h"
@@ -29,7 +31,8 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   __shared__ float red[4][BG][17];
   __shared__ int s_op[BG], s_top[BG], s_src[BG], s_crow[BG], s_cidx[BG], s_nlive;
   __shared__ float s_db[16][16][4];
-  __shared__ int s_g, s_w, s_flag;
+  __shared__ int s_g, s_w;
+  __shared__ int s_abort;                          // a wait for dA rows gave up
 
   claim_group_slot(a.ctl + CTL_XCC_SLOT_B, a.G, a.NW, &s_g, &s_w);
   const int g = s_g, w = s_w;
@@ -104,6 +107,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   elem_t* wbuf = reinterpret_cast<elem_t*>(dsm) + (size_t)wave * 16 * QLD;
   if (direct)
     for (int i = threadIdx.x; i < 4 * 16 * QLD * ESZ / 16; i += 256) ((uint4*)dsm)[i] = uint4{0u, 0u, 0u, 0u};
+  if (threadIdx.x == 0) s_abort = 0;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
@@ -222,10 +226,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         const float dcin = slot_dc[i] + c_gc[i];
         const float tc = tanhf(c_c[i]);
         const float dc = dcin + dh * act.w * (1.f - tc * tc);
-        dA4.x = dc * act.z * act.x * (1.f - act.x);
-        dA4.y = dc * c_cp[i] * act.y * (1.f - act.y);
-        dA4.z = dc * act.x * (1.f - act.z * act.z);
-        dA4.w = dh * tc * act.w * (1.f - act.w);
+        // never the all-ones fill pattern: a NaN is stored as the canonical quiet NaN
+        dA4.x = canon_nan(dc * act.z * act.x * (1.f - act.x));
+        dA4.y = canon_nan(dc * c_cp[i] * act.y * (1.f - act.y));
+        dA4.z = canon_nan(dc * act.x * (1.f - act.z * act.z));
+        dA4.w = canon_nan(dh * tc * act.w * (1.f - act.w));
         add_dc = dc * act.y;
         if (pok[i]) { dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w; }
       } else {
@@ -255,7 +260,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     }
 
     if (clk && threadIdx.x == 0) clk[t * 4 + 1] = wall_clock64();
-    if (group_barrier(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_flag)) break;
+    if (a.poll) {
+      __syncthreads();
+    } else if (group_barrier(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_abort)) {
+      break;
+    }
     if (clk && threadIdx.x == 0) clk[t * 4 + 2] = wall_clock64();
     // c_prev of step t-1 (its producer index arrived with the prefetch above)
     if (t > 0) {
@@ -300,6 +309,46 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
           }
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (a.poll) {
+          // granules whose producer's store has not arrived yet are fetched again (only the lanes
+          // that hold one take part in the copy), bypassing L1, until complete
+          static_assert(16 * SEGQ <= 32, "segment mask is 32 bits");
+          uint32_t bad = 0;
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+#pragma unroll
+            for (int sj = 0; sj < SEGQ; ++sj)
+              if (jt * 16 + r < nlive &&
+                  pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
+                bad |= 1u << (r * SEGQ + sj);
+          int spins = 0;
+          while (__builtin_amdgcn_ballot_w64(bad != 0u)) {
+            if (spin_out(spins, a.ctl, a.spin_limit)) {
+              s_abort = 1;
+              break;
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+#pragma unroll
+              for (int sj = 0; sj < SEGQ; ++sj) {
+                if ((bad >> (r * SEGQ + sj)) & 1u) {
+                  const int b = row0 + s_crow[jt * 16 + r];
+                  const elem_t* gp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H +
+                                     sj * (1024 / ESZ) + lane * (16 / ESZ);
+                  __builtin_amdgcn_global_load_lds((const void*)gp, (lds_ptr_t)(wbuf + r * QLD + sj * (1024 / ESZ)),
+                                                   16, 0, kSc1);
+                }
+              }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+#pragma unroll
+              for (int sj = 0; sj < SEGQ; ++sj)
+                if (((bad >> (r * SEGQ + sj)) & 1u) &&
+                    !pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
+                  bad &= ~(1u << (r * SEGQ + sj));
+          }
+        }
         f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
         if constexpr (PREC == 0) {
           float4 bcur = *(const float4*)&wbuf[l16 * QLD + 4 * lq], bnxt = bcur;
@@ -357,6 +406,34 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         }
         return raw;
       };
+      // the same granule through agent-scope atomic loads (re-read on every call, L1 bypassed)
+      auto fetch_poll = [&](int c) -> uint4 {
+        const int kk = c * KC + (PREC ? 8 : 4) * lq;
+        const size_t el = rowo + kk;
+        const char* base = (const char*)a.dA;
+        uint4 raw = uint4{0u, 0u, 0u, 0u};
+        if (!lv) return raw;
+        if (vec_ok) {
+          if (kk < H) raw = ld_poll_b128(base + el * ESZ);
+          return raw;
+        }
+        uint32_t* rw = (uint32_t*)&raw;
+        if constexpr (PREC == 0) {
+          for (int j = 0; j < 4; ++j)
+            if (kk + j < H)
+              rw[j] = __hip_atomic_load((uint32_t*)(base + (el + j) * 4), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+          for (int j = 0; j < 8; ++j) {
+            if (kk + j >= H) continue;
+            const size_t e = el + j;
+            const uint32_t wv = __hip_atomic_load((uint32_t*)(base + (e & ~(size_t)1) * 2), __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+            const uint32_t hv = (e & 1) ? (wv >> 16) : (wv & 0xffffu);
+            rw[j >> 1] |= hv << (16 * (j & 1));
+          }
+        }
+        return raw;
+      };
       f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
       uint4 bufA[CG], bufB[CG];
 #pragma unroll
@@ -368,6 +445,28 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         if (gi + 1 < NG) {
 #pragma unroll
           for (int j = 0; j < CG; ++j) nxt[j] = ((gi + 1) * CG + j < KS) ? fetch((gi + 1) * CG + j) : uint4{0u, 0u, 0u, 0u};
+        }
+        if (a.poll) {
+          // granules whose producer's store has not arrived yet are fetched again
+          bool any = false;
+#pragma unroll
+          for (int j = 0; j < CG; ++j)
+            if (gi * CG + j < KS && pending_granule<PREC>(cur[j])) any = true;
+          if (__builtin_amdgcn_ballot_w64(any)) {
+#pragma unroll
+            for (int j = 0; j < CG; ++j) {
+              const int c = gi * CG + j;
+              if (c >= KS) continue;
+              int spins = 0;
+              while (pending_granule<PREC>(cur[j])) {
+                if (spin_out(spins, a.ctl, a.spin_limit)) {
+                  s_abort = 1;
+                  break;
+                }
+                cur[j] = fetch_poll(c);
+              }
+            }
+          }
         }
 #pragma unroll
         for (int j = 0; j < CG; ++j) {
@@ -392,6 +491,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       }
     }
     __syncthreads();
+    if (s_abort) break;
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
       if (c_op[i] == 1) {

@@ -138,7 +138,11 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     xw_cur[ti] = xw_at(0, ti);
     cp_cur[ti] = lok[ti] ? a.c0[(size_t)lrow[ti] * H + u] : 0.f;
   }
-  __syncthreads();
+  if (!a.poll) {
+    if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)a.NW, a.ctl, a.spin_limit, &s_abort[1])) return;
+  } else {
+    __syncthreads();
+  }
 
   // Direct staging: one wave instruction moves one 1 KB segment of one row into LDS, 16 bytes
   // per lane. Segment i of this wave is row segment wave + 4 i of the pass; the row's producer
@@ -285,9 +289,9 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         }
       }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (direct) {
-        // granules that still hold the fill: the wave fetches their 1 KB segments again,
-        // bypassing L1, until every producer's store has arrived
+      if (direct && a.poll) {
+        // granules that still hold the fill are fetched again (only the lanes that hold one take
+        // part in the copy), bypassing L1, until every producer's store has arrived
         uint32_t bad = 0;
 #pragma unroll
         for (int i = 0; i < NSEG_W; ++i) {
@@ -308,7 +312,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
 #pragma unroll
           for (int i = 0; i < NSEG_W; ++i) {
             const int sgi = wave + 4 * i;
-            if (sgi < ROWS_B * SEG && __builtin_amdgcn_ballot_w64(((bad >> i) & 1u) != 0u)) {
+            if (sgi < ROWS_B * SEG && ((bad >> i) & 1u)) {
               const int r = sgi / SEG, sj = sgi % SEG, rr = nb * ROWS_B + r;
               const int src = __builtin_amdgcn_readlane(vsrc[rr >> 6], rr & 63);
               int k = sj * (1024 / ESZ) + lane * (16 / ESZ);
@@ -459,7 +463,13 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     }
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) { xw_cur[ti] = xw_nxt[ti]; cp_cur[ti] = cp_nxt[ti]; }
-    __syncthreads();
+    if (!a.poll) {
+      // barrier mode: the tracer's index and every state of step t are complete past this point
+      if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_abort[1]))
+        break;
+    } else {
+      __syncthreads();
+    }
     if (s_abort[1]) break;
 #pragma unroll
     for (int j = 0; j < NV; ++j) vsrc[j] = (64 * j + lane < BG) ? s_src[64 * j + lane] : -1;

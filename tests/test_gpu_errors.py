@@ -70,6 +70,25 @@ def test_spin_limit_timeout_reported():
     assert s.stacklstm_sync_status(r2.workspace) == 0
 
 
+def test_spin_limit_timeout_reported_polling():
+    """bf16 mode exchanges rows by polling fill-marked data: with a one-poll limit the first
+    wait that finds a row not yet written gives up (some wait of the deep workload always
+    does), the kernels leave their loops and the call reports SLSTM_ETIMEOUT; the same
+    buffers then run normally and match the oracle's trace."""
+    need_gpu()
+    wl = wk.make("deep")
+    r, rc = _run(wl, precision=1, spin_limit=1)
+    assert rc == 7
+    torch.cuda.synchronize()
+    from paper_1904_03409_amd import stacklstm as s
+    r2, rc2 = _run(wl, precision=1)
+    assert rc2 == 0
+    assert s.stacklstm_sync_status(r2.workspace) == 0
+    r2.backward()
+    torch.cuda.synchronize()
+    assert s.stacklstm_sync_status(r2.workspace) == 0
+
+
 def test_empty_T():
     need_gpu()
     wl = wk.custom(T=0, B=3, I=2, H=4, seed=0, ops=np.zeros((0, 3), np.int8))
