@@ -59,7 +59,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // the backward.
 struct Plan {
   int prec, KS, ks_eff, NW;
-  int NT, G, per_xcc;
+  int NT, G, per_xcc, pipe;   // pipe: the forward runs the pipelined kernel
   int NTb, Gb, per_xcc_b;
   int splits_w, splits_u;
 };
@@ -109,29 +109,34 @@ int make_plan(const slstm_dims* d, Plan* p) {
   const int cu_per_xcc = cus > 0 ? cus / 8 : 32;
   // smallest row tile count per group whose workgroups (NW per group, groups dealt to the 8
   // XCCs round-robin) are co-resident on one XCC at the kernel's occupancy
-  auto pick = [&](bool bwd, int* NT_out, int* G_out, int* per_out) -> int {
+  // the pipelined forward needs whole 1 KB row segments (vector rows, every K chunk in use)
+  const bool pipe_ok = d->H % (prec ? 8 : 4) == 0 && p->ks_eff == p->KS && p->KS >= 16;
+  auto pick = [&](bool bwd, int* NT_out, int* G_out, int* per_out, int* pipe_out) -> int {
     for (int NT = 1; NT <= 8; NT *= 2) {
       int G = (d->B + 16 * NT - 1) / (16 * NT);
       if (G > MAX_GROUPS) continue;
       int per_xcc = p->NW * ((G + 7) / 8);
       int occ = 0;
+      const bool pipe = !bwd && pipe_ok && NT >= 2 && rec_pipe_built(prec, NT, p->KS);
       RecArgs dummy;
       memset(&dummy, 0, sizeof(dummy));
-      hipError_t e = bwd ? launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
-                         : launch_fwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
+      hipError_t e = bwd    ? launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
+                     : pipe ? launch_fwd_pipe(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
+                            : launch_fwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
       if (e != hipSuccess) return SLSTM_EDEVICE;
       if (per_xcc <= cu_per_xcc * occ) {
         *NT_out = NT;
         *G_out = G;
         *per_out = per_xcc;
+        if (pipe_out) *pipe_out = pipe ? 1 : 0;
         return SLSTM_OK;
       }
     }
     return SLSTM_ENORESIDENT;
   };
-  int rc = pick(false, &p->NT, &p->G, &p->per_xcc);
+  int rc = pick(false, &p->NT, &p->G, &p->per_xcc, &p->pipe);
   if (rc) return rc;
-  if ((rc = pick(true, &p->NTb, &p->Gb, &p->per_xcc_b))) return rc;
+  if ((rc = pick(true, &p->NTb, &p->Gb, &p->per_xcc_b, nullptr))) return rc;
   int64_t K = (int64_t)d->T * d->B;
   p->splits_w = splits_for(d->I, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
   p->splits_u = splits_for(d->H, 4 * d->H, (int)std::min<int64_t>(K, 1 << 30));
@@ -214,6 +219,8 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   // rows are twice as long, checking a staged tile for the fill pattern costs more than the
   // barrier, and the backward's fill of dA is a large write, so fp32 keeps the barrier.
   a.poll = d->precision == SLSTM_BF16_GEMM ? 1 : 0;
+  // the pipelined forward has no barrier: it always polls
+  if (!bwd && p.pipe) a.poll = 1;
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
   a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
   a.coh_top = ((size_t)d->B * 4) % 128 != 0;
@@ -325,7 +332,9 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st, (unsigned char*)top,
                        (size_t)T * B * 4, kTopPending);
   }
-  if ((rc = hip_status(launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)))) return rc;
+  if ((rc = hip_status(p.pipe ? launch_fwd_pipe(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
+                              : launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr))))
+    return rc;
   mark(d, 3, st);
 
   // a7: Algorithm 1's return values

@@ -49,11 +49,15 @@ __device__ __forceinline__ f32x4 mfma_bf16_16x16x32(bf16x8 a, bf16x8 b, f32x4 c)
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Gate nonlinearities from the hardware base-2 exponential and reciprocal (about one ulp
+// each): sigma(z) = 1 / (1 + 2^(-z log2 e)); tanh(x) = 2 sigma(2x) - 1. Absolute error is
+// a few 1e-7 over the whole range; both saturate correctly (2^(+inf) = inf gives 0, 2^(-inf)
+// = 0 gives 1) and need no branch.
 __device__ __forceinline__ float sigmoidf_(float z) {
-  // logistic, in the form that cannot overflow
-  if (z >= 0.f) return 1.f / (1.f + expf(-z));
-  float e = expf(z);
-  return e / (1.f + e);
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
+__device__ __forceinline__ float tanhf_(float x) {
+  return 2.f * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-2.8853900817779268f * x)) - 1.f;
 }
 
 __device__ __forceinline__ unsigned xcc_id() {

@@ -37,5 +37,18 @@ constexpr int rec_occ(int prec, int ks) { return (prec == 1 && ks == 32) ? 2 : 1
   X(1, 4, 2) X(1, 4, 4) X(1, 4, 8) X(1, 4, 16) X(1, 4, 32) \
   X(1, 8, 2) X(1, 8, 4) X(1, 8, 8) X(1, 8, 16) X(1, 8, 32)
 
+// Pipelined forward kernel (two LDS tile buffers, whole 1 KB row segments: K of at least
+// 16 chunks, an even number of row tiles per group). Only the variants that compile without
+// register spills are built; the others run the plain forward kernel.
+constexpr size_t rec_pipe_lds_bytes(int prec, int ks) { return (size_t)2 * 16 * rec_lds_ld(prec, ks) * (prec ? 2 : 4); }
+#define REC_PIPE_CASES(X) \
+  X(0, 2, 16) X(0, 2, 32) X(0, 4, 16) X(0, 4, 32) X(0, 8, 16) \
+  X(1, 2, 16) X(1, 4, 16) X(1, 8, 16)
+constexpr bool rec_pipe_built(int prec, int nt, int ks) {
+  return prec == 0 ? (ks == 16 || (ks == 32 && nt <= 4)) : ks == 16;
+}
+
 hipError_t launch_fwd(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);
+hipError_t launch_fwd_pipe(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st,
+                           int* occ_out);
 hipError_t launch_bwd(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);

@@ -224,7 +224,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         const float4 act = c_act[i];
         const float dh = slot_dh[i] + c_gh[i];
         const float dcin = slot_dc[i] + c_gc[i];
-        const float tc = tanhf(c_c[i]);
+        const float tc = tanhf_(c_c[i]);
         const float dc = dcin + dh * act.w * (1.f - tc * tc);
         // never the all-ones fill pattern: a NaN is stored as the canonical quiet NaN
         dA4.x = canon_nan(dc * act.z * act.x * (1.f - act.x));

@@ -21,15 +21,7 @@
 #include "common.h"
 #include "recurrent.h"
 #include "rec_config.h"
-
-// Source of one staged granule: the state of step src (h0 for src = -1) of batch row b, column k.
-template <int PREC>
-__device__ __forceinline__ const void* staged_src(const RecArgs& a, int src, int b, int k) {
-  if constexpr (PREC == 0)
-    return (src < 0) ? (const void*)(a.h0 + (size_t)b * a.H + k)
-                     : (const void*)(a.hcell + ((size_t)src * a.B + b) * a.H + k);
-  else return (const void*)(a.hx + ((size_t)(src + 1) * a.B + b) * a.H + k);
-}
+#include "rec_device.h"
 
 template <int PREC, int NT, int NTB, int KS, int OCC>
 __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
@@ -65,28 +57,10 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   // whose slot 0 holds h0 and slot s+1 the state of step s
   const rsrc_t r_h = PREC ? make_rsrc(a.hx, TBH * 2 + (size_t)B * H * 2) : make_rsrc(a.hcell, TBH * 4);
 
-  // ---- U slice into registers: A operand, row m = l16 -> (unit_base + m/4, gate m%4), K permuted per chunk
-  const int a_unit = unit_base + (l16 >> 2), a_gate = l16 & 3;
-  const bool a_ok = a_unit < H;
-  const float* Ucol = a.U + (size_t)a_gate * H + a_unit;
+  // ---- U slice into registers (MFMA A operand), resident for the whole kernel
   float ureg32[PREC ? 1 : KS][4];
   bf16x8 ureg16[PREC ? KS : 1];
-#pragma unroll
-  for (int c = 0; c < KS; ++c) {
-    if constexpr (PREC == 0) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int k = c * 16 + 4 * lq + j;
-        ureg32[c][j] = (a_ok && k < H) ? Ucol[(size_t)k * H4] : 0.f;
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        int k = c * 32 + 8 * lq + j;
-        ureg16[c][j] = f32_to_bf16((a_ok && k < H) ? Ucol[(size_t)k * H4] : 0.f);
-      }
-    }
-  }
+  fwd_load_u<PREC, KS>(a, unit_base, l16, lq, ureg32, ureg16);
 
   const bool tracer = (w == 0) && ((int)threadIdx.x < BG) && (row0 + (int)threadIdx.x < B);
   const int my_row = row0 + (int)threadIdx.x;
@@ -405,19 +379,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       for (int nt = 0; nt < NTB; ++nt) {
         const int ti = nb * NTB + nt;
         if (!lok[ti]) continue;
-        const int b = lrow[ti];
-        const float gi = sigmoidf_(acc[nt][0] + xw_cur[ti].x);
-        const float gf = sigmoidf_(acc[nt][1] + xw_cur[ti].y);
-        const float gg = tanhf(acc[nt][2] + xw_cur[ti].z);
-        const float go = sigmoidf_(acc[nt][3] + xw_cur[ti].w);
-        const float c = gf * cp_cur[ti] + gi * gg;
-        const float h = canon_nan(go * tanhf(c));     // never the all-ones fill pattern
-        const size_t o = ((size_t)t * B + b) * H + u;
-        a.hcell[o] = h;
-        a.ccell[o] = c;
-        if constexpr (PREC == 1) a.hx[o + (size_t)B * H] = f32_to_bf16_bits(h);
-        *(float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * u) = float4{gi, gf, gg, go};
-        cp_cur[ti] = c;                            // the state this step produced
+        cp_cur[ti] = fwd_cell<PREC>(a, acc[nt], xw_cur[ti], cp_cur[ti], t, lrow[ti], u);   // the state this step produced
       }
       if (NPASS > 1) __syncthreads();
     }

@@ -46,6 +46,26 @@ def test_odd_shapes(oracle_mod, shape, precision):
     _check(oracle_mod, wl, precision)
 
 
+PIPE_SHAPES = [
+    # (T, B, I, H, precision): batches that need two or more 16-row tiles per group, with
+    # whole 1 KB state rows, so the forward runs the pipelined kernel
+    (20, 600, 24, 256, 0),
+    (16, 600, 20, 252, 0),    # copied row segments reach past H
+    (12, 300, 16, 512, 1),
+]
+
+
+@pytest.mark.parametrize("shape", PIPE_SHAPES)
+def test_pipelined_forward(oracle_mod, shape):
+    T, B, I, H, precision = shape
+    from paper_1904_03409_amd.stacklstm import make_dims, stacklstm_plan
+    need_gpu()
+    plan = stacklstm_plan(make_dims(T, B, I, H, precision, 0))
+    assert plan["rows_per_group"] >= 32, plan
+    wl = wk.custom(T=T, B=B, I=I, H=H, seed=B + H, wscale=0.3, random_state=True, dc_top=True)
+    _check(oracle_mod, wl, precision)
+
+
 def _streams(kind, T, B, rng):
     if kind == "all_push":
         return np.ones((T, B), np.int8)
