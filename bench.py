@@ -67,8 +67,8 @@ def timed_run(wl, precision, steps, warmup, torch):
     total_ms = start.elapsed_time(stop)
     phase = {}
     f = ctypes.c_float()
-    pairs = [(0, 1, "scan+sync"), (1, 2, "xw_gemm"), (2, 3, "rec_fwd"), (3, 4, "top_gather"), (5, 6, "rec_bwd"),
-             (6, 7, "dW+db"), (7, 8, "dU"), (8, 9, "dx"), (4, 5, "fwd_to_bwd")]
+    pairs = [(0, 1, "scan+sync"), (1, 2, "xw_gemm+prep"), (2, 3, "rec_fwd"), (3, 4, "top_gather"),
+             (5, 6, "rec_bwd"), (6, 7, "dW+db"), (7, 8, "dU"), (8, 9, "dx"), (4, 5, "bwd_prep")]
     for a, b, name in pairs:
         acc = 0.0
         for k in range(steps):
@@ -84,8 +84,52 @@ def timed_run(wl, precision, steps, warmup, torch):
 def flops(wl):
     T, B, I, H = wl.T, wl.B, wl.I, wl.H
     rec = 2.0 * T * B * H * 4 * H                 # one recurrent contraction (h_prev U or dA U^T)
-    return {"rec_fwd": rec, "rec_bwd": rec, "xw_gemm": 2.0 * T * B * I * 4 * H, "dW+db": 2.0 * T * B * I * 4 * H,
+    return {"rec_fwd": rec, "rec_bwd": rec, "xw_gemm+prep": 2.0 * T * B * I * 4 * H, "dW+db": 2.0 * T * B * I * 4 * H,
             "dU": 2.0 * T * B * H * 4 * H, "dx": 2.0 * T * B * I * 4 * H}
+
+
+def kernel_sources_sha1():
+    """Hash of every HIP source and header of the library: a stored counter reading is
+    valid only for the kernels it was taken from."""
+    import glob
+    import hashlib
+    h = hashlib.sha1()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_1904_03409_amd", "csrc", "*"))):
+        if f.endswith((".hip", ".h")):
+            h.update(os.path.basename(f).encode())
+            with open(f, "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(config, dname, phase):
+    """HBM bytes per launch of a phase's kernel from the committed rocprofv3 counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or None when the
+    summary is missing or was taken from other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha1") != kernel_sources_sha1():
+        return None
+    e = t.get("entries", {}).get(f"{config}/{dname}/{phase}")
+    return None if e is None else e.get("hbm_bytes_per_launch")
+
+
+def copy_probe(torch, nbytes=256 << 20, reps=3):
+    """A plain copy kernel of known size (one elementwise kernel reading nbytes and writing
+    nbytes, b = a * 1): its FETCH_SIZE / WRITE_SIZE readings calibrate the counters of the
+    other kernels. (A device-to-device memcpy is not used: the runtime splits it into several
+    blit dispatches.)"""
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        torch.mul(a, 1.0, out=b)
+    torch.cuda.synchronize()
+    print(f"[bench] copy probe: {reps} x {nbytes} bytes (elementwise b = a * 1)", file=sys.stderr, flush=True)
 
 
 def cpu_baseline(wl, target_s=12.0):
@@ -115,6 +159,8 @@ def main():
     ap.add_argument("--precision", choices=["fp32", "bf16"], default=None)
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-GEMM run of the same shape")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 256 MiB device copy (counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the StackLSTM step is measured on one MI355X "
@@ -147,7 +193,7 @@ def main():
                                f"arc-standard op streams, {dname} GEMM operands",
                    "global_batch": wl.B, "seq_len": wl.T, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "mfma", "kernel": kern, "achieved": achieved, "peak": PEAK[dname], "unit": "TFLOP/s",
-                     "frac": achieved / PEAK[dname], "traffic": None},
+                     "frac": achieved / PEAK[dname], "traffic": stored_traffic(args.config, dname, kern)},
         "phases_ms": {k: round(v, 4) for k, v in phase.items()},
         "recurrent_mfma_frac": rec_util, "overall_mfma_frac": all_util,
         "push_steps_per_s": st["push_steps"] / (ms / 1e3), "op_stats": st, "wall_s_timed": wall,
@@ -162,6 +208,8 @@ def main():
                             "recurrent_mfma_frac": r2, "overall_mfma_frac": sum(fl.values()) / (ms2 / 1e3) / 1e12 / PEAK["bf16"],
                             "phases_ms": {k: round(v, 4) for k, v in ph2.items()}}
         del run2
+    if args.copy_probe:
+        copy_probe(torch)
     if not args.no_cpu:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl)

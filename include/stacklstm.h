@@ -72,10 +72,13 @@ typedef struct {
   void* phase_events;      /* NULL, or an array of SLSTM_PHASE_EVENTS hipEvent_t created by the
                               caller; the calls record them on `stream` between their phases:
                               fwd [0] start, [1] after the op scan and its status read-back,
-                              [2] after the input projection, [3] after the persistent forward
-                              kernel, [4] after the h_top/c_top gathers; bwd [5] start, [6] after
-                              the persistent backward kernel, [7] after dW and db, [8] after dU,
-                              [9] after dx. For profiling only. */
+                              [2] after the input projection and the preparation of the exchange
+                              buffers, [3] after the persistent forward kernel, [4] after the
+                              h_top/c_top gathers; bwd [5] after the backward's preparation
+                              (control words, exchange buffer), right before the persistent
+                              backward kernel, [6] after it, [7] after dW and db, [8] after dU,
+                              [9] after dx. [2]-[3] and [5]-[6] time the persistent kernels
+                              alone. For profiling only. */
   void* step_clock;        /* NULL, or a device int64 buffer of 2 * 512 * T * 4 entries: the
                               persistent kernels store 100 MHz wall-clock stamps per workgroup
                               and step, [pass (0 fwd, 1 bwd)][workgroup][t][4], at four points of

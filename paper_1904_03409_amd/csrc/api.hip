@@ -317,7 +317,6 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   g.C = xw; g.ldc = 4 * H; g.bias = b; g.bias_H = H;
   g.k_chunk = k_chunk_for(I, 1); g.split_stride = 0;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_KN, g, 1, st))) return rc;
-  mark(d, 2, st);
 
   // a3-a6: persistent recurrent kernel
   RecArgs a = rec_args(d, p, ws, L, false);
@@ -332,6 +331,7 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st, (unsigned char*)top,
                        (size_t)T * B * 4, kTopPending);
   }
+  mark(d, 2, st);
   if ((rc = hip_status(p.pipe ? launch_fwd_pipe(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
                               : launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr))))
     return rc;
@@ -376,7 +376,6 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   }
 
   // a8: persistent reverse loop
-  mark(d, 5, st);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_XCC_SLOT_B, 16);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_BAR_B, 16 * MAX_GROUPS);
   hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_ABORT, 2);
@@ -395,6 +394,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(da_bytes / 16 + 1)), dim3(256), 0, st, (unsigned char*)a.dA,
                        da_bytes, 0xffffffffu);
   }
+  mark(d, 5, st);
   if ((rc = hip_status(launch_bwd(a, p.prec, p.NTb, p.KS, dim3(8 * p.per_xcc_b), st, nullptr)))) return rc;
   mark(d, 6, st);
 
