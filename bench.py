@@ -75,6 +75,11 @@ def timed_run(wl, precision, steps, warmup, torch):
             lib.hipEventElapsedTime(ctypes.byref(f), evs[k][a], evs[k][b])
             acc += f.value
         phase[name] = acc / steps
+    per_step = []
+    for k in range(steps):
+        lib.hipEventElapsedTime(ctypes.byref(f), evs[k][0], evs[k][9])
+        per_step.append(f.value)
+    phase["_per_step_ms"] = per_step
     for arr in evs:
         for i in range(SLSTM_PHASE_EVENTS):
             lib.hipEventDestroy(arr[i])
@@ -118,6 +123,34 @@ def stored_traffic(config, dname, phase):
     return None if e is None else e.get("hbm_bytes_per_launch")
 
 
+def stored_step_traffic(config, dname):
+    """HBM bytes of one whole fwd+bwd step (every kernel) from the committed counter
+    summary, or None (see stored_traffic)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha1") != kernel_sources_sha1():
+        return None
+    e = t.get("entries", {}).get(f"{config}/{dname}/step")
+    return None if e is None else e.get("hbm_bytes_per_launch")
+
+
+def host_cpu():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
 def copy_probe(torch, nbytes=256 << 20, reps=3):
     """A plain copy kernel of known size (one elementwise kernel reading nbytes and writing
     nbytes, b = a * 1): its FETCH_SIZE / WRITE_SIZE readings calibrate the counters of the
@@ -136,18 +169,66 @@ def cpu_baseline(wl, target_s=12.0):
     """The oracle (float32 instantiation, OpenMP over batch elements) on a bounded sample."""
     import oracle
     th = oracle.max_threads()
-    n = min(wl.B, max(th, 8))
+    n0 = min(wl.B, max(th, 8))
     t0 = time.perf_counter()
-    oracle.run(wl, sel=np.arange(n, dtype=np.int32), mode="f32", threads=th)
-    dt = time.perf_counter() - t0
-    if dt < target_s / 4 and n < wl.B:
-        n = int(min(wl.B, max(n, n * target_s / max(dt, 1e-3))))
+    oracle.run(wl, sel=np.arange(n0, dtype=np.int32), mode="f32", threads=th)
+    dt0 = time.perf_counter() - t0
+    # sample size for about target_s of CPU work, then the median of three runs of it
+    # (one run when a single run already takes more than a third of that)
+    n = n0 if dt0 >= target_s / 4 else int(min(wl.B, max(n0, n0 * target_s / max(dt0, 1e-3))))
+    est = dt0 * n / n0
+    times = []
+    for _ in range(3 if 3 * est <= 1.5 * target_s else 1):
         t0 = time.perf_counter()
         oracle.run(wl, sel=np.arange(n, dtype=np.int32), mode="f32", threads=th)
-        dt = time.perf_counter() - t0
+        times.append(time.perf_counter() - t0)
+    dt = float(np.median(times))
+    pushes = int((wl.ops[:, :n] == 1).sum())
+    model, ncpu = host_cpu()
     return {"value": n * wl.T / dt, "unit": "element-steps/s", "cores": th, "kind": "oracle",
-            "sample": f"fwd+bwd of the first {n} of {wl.B} batch elements (all T={wl.T} steps), float32 oracle, "
-                      f"{dt:.1f} s"}
+            "push_steps_per_s": pushes / dt, "host_cpus": ncpu, "cpu_model": model,
+            "sample": f"fwd+bwd of the first {n} of {wl.B} batch elements (all T={wl.T} steps), float32 oracle "
+                      f"(-O3 -march=native -fopenmp, {th} threads), median of {len(times)} runs: {dt:.2f} s"}
+
+
+def amdahl_fit(batches, speedups):
+    """Parallel fraction P of Amdahl's law S(b) = 1 / ((1 - P) + P / b): the least-squares
+    fit of 1/S - 1 = P (1/b - 1) over the points with b > 1, and P from each point alone."""
+    y = np.array([1.0 / s - 1.0 for b, s in zip(batches, speedups) if b > 1])
+    z = np.array([1.0 / b - 1.0 for b in batches if b > 1])
+    p_fit = float((y * z).sum() / (z * z).sum()) if len(z) else None
+    each = {int(b): float((1.0 - 1.0 / s) / (1.0 - 1.0 / b)) for b, s in zip(batches, speedups) if b > 1}
+    return p_fit, each
+
+
+def sweep(args, torch):
+    """Batch-scaling sweep (the analogue of the paper's Figure 1 on synthetic streams):
+    element-steps/s of the parser-shaped workload (H=256, I=128) at B = 1, 2, 4, .., 1024
+    with T fixed, speed-up S(B) = throughput(B) / throughput(1), and the Amdahl parallel
+    fraction fitted to it (the paper reports 99.92% at a batch of 64)."""
+    from paper_1904_03409_amd import workloads
+    prec = 0 if (args.precision or "fp32") == "fp32" else 1
+    pts = []
+    for B in [1 << k for k in range(11)]:
+        wl = workloads.make("parser", B=B, T=120, precision=prec)
+        run, total_ms, _, phase = timed_run(wl, prec, args.steps, args.warmup, torch)
+        per = phase.pop("_per_step_ms")
+        ms = total_ms / args.steps
+        pts.append({"B": B, "T": wl.T, "ms_per_step": ms, "step_ms_median": float(np.median(per)),
+                    "element_steps_per_s": B * wl.T / (ms / 1e3), "rec_fwd_ms": phase["rec_fwd"],
+                    "rec_bwd_ms": phase["rec_bwd"]})
+        print(f"[sweep] B={B} {ms:.3f} ms/step", file=sys.stderr, flush=True)
+        del run
+        torch.cuda.empty_cache()
+    base = pts[0]["element_steps_per_s"]
+    for p in pts:
+        p["speedup"] = p["element_steps_per_s"] / base
+    p_fit, each = amdahl_fit([p["B"] for p in pts], [p["speedup"] for p in pts])
+    return {"metric": "batch-scaling sweep: fwd+bwd element-steps/s vs batch size, Amdahl fit",
+            "unit": "element-steps/s", "dtype": "f32" if prec == 0 else "bf16", "data": "synthetic",
+            "config": {"workload": "parser-shaped arc-standard streams, I=128, H=256, T=120 (hold-padded)",
+                       "steps": args.steps, "warmup": args.warmup},
+            "points": pts, "amdahl": {"P_fit": p_fit, "P_from_each_B": each, "paper_P_at_64": 0.9992}}
 
 
 def main():
@@ -159,6 +240,8 @@ def main():
     ap.add_argument("--precision", choices=["fp32", "bf16"], default=None)
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-GEMM run of the same shape")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--sweep", action="store_true",
+                    help="batch-scaling sweep B = 1..1024 of the parser shape and its Amdahl fit (one JSON line)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -170,12 +253,16 @@ def main():
     import torch
     from paper_1904_03409_amd import workloads
     assert torch.cuda.is_available(), "bench.py needs the GPU"
+    if args.sweep:
+        print(json.dumps(sweep(args, torch)), flush=True)
+        return
     wl = workloads.make(args.config)
     prec = wl.precision if args.precision is None else (0 if args.precision == "fp32" else 1)
     dname = "f32" if prec == 0 else "bf16"
     print(f"[bench] {args.config} T={wl.T} B={wl.B} I={wl.I} H={wl.H} {dname} steps={args.steps} "
           f"warmup={args.warmup}", file=sys.stderr, flush=True)
     run, total_ms, wall, phase = timed_run(wl, prec, args.steps, args.warmup, torch)
+    per_step = phase.pop("_per_step_ms")
     ms = total_ms / args.steps
     value = wl.B * wl.T / (ms / 1e3)
     fl = flops(wl)
@@ -195,16 +282,23 @@ def main():
         "roofline": {"bound": "mfma", "kernel": kern, "achieved": achieved, "peak": PEAK[dname], "unit": "TFLOP/s",
                      "frac": achieved / PEAK[dname], "traffic": stored_traffic(args.config, dname, kern)},
         "phases_ms": {k: round(v, 4) for k, v in phase.items()},
+        "step_ms_median": float(np.median(per_step)), "step_ms_min": float(np.min(per_step)),
         "recurrent_mfma_frac": rec_util, "overall_mfma_frac": all_util,
         "push_steps_per_s": st["push_steps"] / (ms / 1e3), "op_stats": st, "wall_s_timed": wall,
     }
+    step_bytes = stored_step_traffic(args.config, dname)
+    out["hbm_gb_s_whole_run"] = None if step_bytes is None else step_bytes / (ms / 1e3) / 1e9
     del run
     torch.cuda.empty_cache()
     if not args.no_bf16 and prec == 0 and wl.H <= 1024:
         run2, tot2, _, ph2 = timed_run(wl, 1, args.steps, args.warmup, torch)
+        ps2 = ph2.pop("_per_step_ms")
         ms2 = tot2 / args.steps
         r2 = (fl["rec_fwd"] + fl["rec_bwd"]) / ((ph2["rec_fwd"] + ph2["rec_bwd"]) / 1e3) / 1e12 / PEAK["bf16"]
+        sb2 = stored_step_traffic(args.config, "bf16")
         out["bf16_gemm"] = {"value": wl.B * wl.T / (ms2 / 1e3), "ms_per_step": ms2,
+                            "step_ms_median": float(np.median(ps2)), "step_ms_min": float(np.min(ps2)),
+                            "hbm_gb_s_whole_run": None if sb2 is None else sb2 / (ms2 / 1e3) / 1e9,
                             "recurrent_mfma_frac": r2, "overall_mfma_frac": sum(fl.values()) / (ms2 / 1e3) / 1e12 / PEAK["bf16"],
                             "phases_ms": {k: round(v, 4) for k, v in ph2.items()}}
         del run2

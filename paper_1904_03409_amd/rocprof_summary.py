@@ -5,14 +5,15 @@
       (a `rocprofv3 --kernel-trace --output-format csv` run), as a markdown table.
 
   python -m paper_1904_03409_amd.rocprof_summary traffic --fetch DIR1 --write DIR2 \\
-          --copy-bytes N --key CONFIG [--json OUT]
+          --copy-bytes N --key CONFIG [--json OUT] [--steps-per-run K]
       HBM bytes per dispatch of every kernel from a FETCH_SIZE run (DIR1) and a WRITE_SIZE
       run (DIR2). Both counters are read in KiB per dispatch and scaled by what they read
       for the plain copy kernel of N bytes in the same run (the elementwise b = a * 1 kernel
       that bench.py --copy-probe launches). With --json, the persistent kernels' entries are
       merged into OUT keyed CONFIG/dtype/phase (dtype from the kernel's precision argument),
       together with the hash of the kernel sources they were taken from (bench.py reports
-      them only while that hash still matches).
+      them only while that hash still matches). The totals of one whole fwd+bwd step per
+      precision (every kernel, K steps per run) are stored as CONFIG/dtype/step.
 """
 from __future__ import annotations
 
@@ -48,26 +49,47 @@ def stats(d):
     return "\n".join(lines)
 
 
-def _per_dispatch(d, counter):
-    """Counter value per dispatch (summed over the instances of one dispatch), averaged per kernel."""
+def _dispatches(d, counter):
+    """[(dispatch id, kernel name, counter value summed over the dispatch's instances)] in
+    dispatch order."""
     per = collections.defaultdict(float)
     names = {}
     for r in _rows(d, "counter_collection.csv"):
         if r["Counter_Name"] != counter:
             continue
-        key = r["Dispatch_Id"]
+        key = int(r["Dispatch_Id"])
         per[key] += float(r["Counter_Value"])
         names[key] = r["Kernel_Name"]
+    return [(k, names[k], per[k]) for k in sorted(per)]
+
+
+def _per_dispatch(d, counter):
+    """Counter value per dispatch, averaged per kernel."""
     out = collections.defaultdict(list)
-    for key, v in per.items():
-        out[names[key]].append(v)
+    for _, name, v in _dispatches(d, counter):
+        out[name].append(v)
     return {k: sum(v) / len(v) for k, v in out.items()}
+
+
+def _step_bytes(d, counter, scale, steps_per_run):
+    """Scaled bytes of one fwd+bwd step for the fp32 run and for the bf16 run that bench.py
+    starts after it (the bf16 run begins at its first bf16 kernel); the copy probe's kernels
+    are left out."""
+    seg = {"f32": 0.0, "bf16": 0.0}
+    cur = "f32"
+    for _, name, v in _dispatches(d, counter):
+        if "<1," in name:
+            cur = "bf16"
+        if "MulFunctor" in name or "FillFunctor" in name:
+            continue
+        seg[cur] += v * 1024.0 * scale
+    return {k: v / steps_per_run for k, v in seg.items()}
 
 
 PHASE_OF = (("void k_fwd", "rec_fwd"), ("void k_bwd", "rec_bwd"))
 
 
-def traffic(fetch_dir, write_dir, copy_bytes, key, json_out):
+def traffic(fetch_dir, write_dir, copy_bytes, key, json_out, steps_per_run):
     fetch = _per_dispatch(fetch_dir, "FETCH_SIZE")
     write = _per_dispatch(write_dir, "WRITE_SIZE")
     probe = "MulFunctor"
@@ -92,6 +114,13 @@ def traffic(fetch_dir, write_dir, copy_bytes, key, json_out):
                 dtype = "f32" if k.split("<", 1)[1].startswith("0") else "bf16"
                 entries[f"{key}/{dtype}/{phase}"] = {"kernel": k, "fetch_kib": fb, "write_kib": wb,
                                                      "hbm_bytes_per_launch": hbm}
+    fs = _step_bytes(fetch_dir, "FETCH_SIZE", f_scale, steps_per_run)
+    ws = _step_bytes(write_dir, "WRITE_SIZE", w_scale, steps_per_run)
+    lines += ["", f"Whole fwd+bwd step (every kernel, {steps_per_run} steps per run): fp32 "
+              f"{(fs['f32'] + ws['f32']) / 1e9:.3f} GB, bf16-GEMM {(fs['bf16'] + ws['bf16']) / 1e9:.3f} GB."]
+    for dt in ("f32", "bf16"):
+        entries[f"{key}/{dt}/step"] = {"kernel": "all kernels of one fwd+bwd step",
+                                       "hbm_bytes_per_launch": fs[dt] + ws[dt]}
     if json_out:
         sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
         from bench import kernel_sources_sha1
@@ -121,11 +150,12 @@ def main():
     t.add_argument("--copy-bytes", type=int, default=256 << 20)
     t.add_argument("--key", required=True)
     t.add_argument("--json", default=None)
+    t.add_argument("--steps-per-run", type=int, default=3, help="warm-up + timed steps of each precision's run")
     a = ap.parse_args()
     if a.cmd == "stats":
         print(stats(a.dir))
     else:
-        print(traffic(a.fetch, a.write, a.copy_bytes, a.key, a.json))
+        print(traffic(a.fetch, a.write, a.copy_bytes, a.key, a.json, a.steps_per_run))
 
 
 if __name__ == "__main__":

@@ -174,17 +174,20 @@ CONFIGS = {
 }
 
 
-def make(name: str, seed: Optional[int] = None, precision: Optional[int] = None, B: Optional[int] = None) -> Workload:
+def make(name: str, seed: Optional[int] = None, precision: Optional[int] = None, B: Optional[int] = None,
+         T: Optional[int] = None) -> Workload:
     """Build one of the named workloads. ``precision`` overrides the GEMM precision
     (e.g. the large shape in bf16-GEMM mode); ``B`` overrides the batch size (used
-    by the batch-size sweep), keeping the rest of the recipe."""
+    by the batch-size sweep), keeping the rest of the recipe; ``T`` pads the
+    arc-standard streams with holds to at least T steps (a fixed length across the
+    sweep, so every batch size does the same work per element)."""
     c = dict(CONFIGS[name])
     if B is not None:
         c["B"] = int(B)
     rng = np.random.default_rng(c["seed"] if seed is None else seed)
     Bn, I, H = c["B"], c["I"], c["H"]
     if c["kind"] == "tiny":
-        T = c["T"]
+        T = max(c["T"], T or 0)
         ops = np.stack([ops_tiny_stream(rng, T, c["lo"], c["hi"]) for _ in range(Bn)], axis=1)
     elif c["kind"] == "arc":
         streams, lengths = [], []
@@ -192,12 +195,12 @@ def make(name: str, seed: Optional[int] = None, precision: Optional[int] = None,
             n = int(rng.integers(c["nlo"], c["nhi"] + 1))
             lengths.append(n)
             streams.append(ops_arc_standard_stream(rng, n))
-        T = 2 * max(lengths)
+        T = max(2 * max(lengths), T or 0)
         ops = np.zeros((T, Bn), dtype=np.int8)
         for j, s in enumerate(streams):
             ops[: len(s), j] = s
     elif c["kind"] == "deep":
-        T = c["T"]
+        T = max(c["T"], T or 0)
         ops = np.stack([ops_deep_stream(rng, T) for _ in range(Bn)], axis=1)
     else:
         raise ValueError(c["kind"])
