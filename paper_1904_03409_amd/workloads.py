@@ -20,6 +20,13 @@ transition sequences with the same stack-op shape:
   T = 2 * max n.
 * ``deep``   -- bursty runs: push runs of 100..300, pop runs of 100..200
   clamped to the current depth, alternating, truncated at T = 1024.
+* ``hybrid`` -- the arc-hybrid parser's two StackLSTMs (paper, section 3 and its
+  transition table): per sentence of n words a random arc-hybrid transition
+  sequence (n shifts, n-1 left/right arcs, each chosen uniformly among the valid
+  ones) drives a stack StackLSTM (shift = push, either arc = pop) and a buffer
+  StackLSTM (the n words pushed first, then shift = pop, either arc = hold); both
+  run as one doubled batch (rows 0..E-1 the stacks, E..2E-1 the buffers of the E
+  sentences) with shared weights, padded with hold to T = 3 * max n - 1.
 
 Every draw comes from one ``numpy.random.default_rng(seed)`` in the fixed order
 ops (element by element), x, W, U, b, h0, c0, R (the upstream gradient).
@@ -107,6 +114,35 @@ def ops_arc_standard_stream(rng: np.random.Generator, n: int) -> np.ndarray:
     return np.asarray(out, dtype=np.int8)
 
 
+def ops_arc_hybrid_streams(rng: np.random.Generator, n: int) -> tuple:
+    """Stack and buffer op streams of one sentence of n words (3n - 1 steps each): the
+    buffer first receives the n words (n pushes while the stack holds), then a random
+    arc-hybrid transition sequence runs. Valid transitions: shift needs a non-empty
+    buffer, left-arc a non-empty stack and a non-empty buffer, right-arc two stack
+    items; the sequence ends with an empty buffer and one item on the stack."""
+    stack = [HOLD] * n
+    buf = [PUSH] * n
+    s, b = 0, n
+    while b > 0 or s > 1:
+        valid = []
+        if b > 0:
+            valid.append("shift")
+        if s >= 1 and b > 0:
+            valid.append("left")
+        if s >= 2:
+            valid.append("right")
+        tr = valid[int(rng.integers(len(valid)))]
+        if tr == "shift":
+            stack.append(PUSH)
+            buf.append(POP)
+            s, b = s + 1, b - 1
+        else:
+            stack.append(POP)
+            buf.append(HOLD)
+            s -= 1
+    return np.asarray(stack, dtype=np.int8), np.asarray(buf, dtype=np.int8)
+
+
 def ops_deep_stream(rng: np.random.Generator, T: int, push_run=(100, 300), pop_run=(100, 200)) -> np.ndarray:
     out = np.zeros(T, dtype=np.int8)
     t = 0
@@ -171,6 +207,8 @@ CONFIGS = {
     "large": dict(B=256, I=256, H=512, precision=FP32, seed=103, kind="arc", nlo=20, nhi=120, wscale=0.08, bias_zero=False),
     "deep": dict(B=128, I=256, H=512, precision=FP32, seed=104, kind="deep", T=1024, wscale=0.08, bias_zero=False),
     "thru": dict(B=1024, I=512, H=1024, precision=BF16_GEMM, seed=105, kind="arc", nlo=10, nhi=128, wscale=0.08, bias_zero=False),
+    # B counts sentences; the workload has 2B rows (stack StackLSTMs, then buffer StackLSTMs)
+    "hybrid": dict(B=128, I=256, H=512, precision=FP32, seed=106, kind="hybrid", nlo=20, nhi=80, wscale=0.08, bias_zero=False),
 }
 
 
@@ -199,6 +237,14 @@ def make(name: str, seed: Optional[int] = None, precision: Optional[int] = None,
         ops = np.zeros((T, Bn), dtype=np.int8)
         for j, s in enumerate(streams):
             ops[: len(s), j] = s
+    elif c["kind"] == "hybrid":
+        pairs = [ops_arc_hybrid_streams(rng, int(rng.integers(c["nlo"], c["nhi"] + 1))) for _ in range(Bn)]
+        T = max(max(len(st) for st, _ in pairs), T or 0)
+        ops = np.zeros((T, 2 * Bn), dtype=np.int8)
+        for j, (st, bu) in enumerate(pairs):
+            ops[: len(st), j] = st
+            ops[: len(bu), Bn + j] = bu
+        Bn = 2 * Bn
     elif c["kind"] == "deep":
         T = max(c["T"], T or 0)
         ops = np.stack([ops_deep_stream(rng, T) for _ in range(Bn)], axis=1)

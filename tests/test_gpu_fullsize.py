@@ -67,3 +67,8 @@ def test_deep(oracle_mod):
 
 def test_thru(oracle_mod):
     _full(oracle_mod, "thru", 1, 2)
+
+
+def test_hybrid(oracle_mod):
+    # 128 sentences: rows 0..127 stack StackLSTMs, 128..255 buffer StackLSTMs (sampled: two of each)
+    _full(oracle_mod, "hybrid", 0, 4)

@@ -66,6 +66,22 @@ def test_pipelined_forward(oracle_mod, shape):
     _check(oracle_mod, wl, precision)
 
 
+def test_arc_hybrid_two_stacks(oracle_mod):
+    """The arc-hybrid parser's stack and buffer StackLSTMs of 12 sentences as one doubled
+    batch with shared weights (one launch per direction)."""
+    rng = np.random.default_rng(11)
+    E = 12
+    pairs = [wk.ops_arc_hybrid_streams(rng, int(rng.integers(3, 18))) for _ in range(E)]
+    T = max(len(s) for s, _ in pairs)
+    ops = np.zeros((T, 2 * E), np.int8)
+    for j, (st, bu) in enumerate(pairs):
+        ops[: len(st), j] = st
+        ops[: len(bu), E + j] = bu
+    for precision in (0, 1):
+        wl = wk.custom(T=T, B=2 * E, I=24, H=48, seed=12, ops=ops, wscale=0.3, random_state=True, dc_top=True)
+        _check(oracle_mod, wl, precision)
+
+
 def _streams(kind, T, B, rng):
     if kind == "all_push":
         return np.ones((T, B), np.int8)

@@ -62,3 +62,33 @@ def test_same_seed_same_bytes():
         assert getattr(a, k).tobytes() == getattr(b, k).tobytes()
     c = wk.make("parser", seed=7)
     assert c.x.tobytes() != a.x.tobytes()
+
+
+def test_arc_hybrid_streams_follow_the_transition_table():
+    """Stack and buffer streams of one sentence: the n words enter the buffer first (the
+    stack holds), then every shift is a stack push and a buffer pop, every arc a stack pop
+    and a buffer hold; neither stack underflows; the buffer ends empty and one item stays
+    on the stack."""
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        n = int(rng.integers(1, 30))
+        st, bu = wk.ops_arc_hybrid_streams(rng, n)
+        assert len(st) == len(bu) == 3 * n - 1
+        assert np.all(bu[:n] == 1) and np.all(st[:n] == 0)
+        tr_s, tr_b = st[n:], bu[n:]
+        assert np.all((tr_s == 1) == (tr_b == -1))      # shift
+        assert np.all((tr_s == -1) == (tr_b == 0))      # left-arc / right-arc
+        assert (tr_s == 1).sum() == n and (tr_s == -1).sum() == n - 1
+        ds, db = np.cumsum(st.astype(int)), np.cumsum(bu.astype(int))
+        assert ds.min() >= 0 and db.min() >= 0
+        assert ds[-1] == 1 and db[-1] == 0
+
+
+def test_hybrid_workload_is_a_doubled_batch():
+    w = wk.make("hybrid", B=6)
+    assert w.B == 12 and w.ops.shape == (w.T, 12)
+    depth = np.cumsum(w.ops.astype(np.int64), axis=0)
+    assert depth.min() >= 0
+    assert np.all(depth[-1, :6] == 1) and np.all(depth[-1, 6:] == 0)
+    # the buffer half starts with pushes while the stack half holds
+    assert np.all(w.ops[0, :6] == 0) and np.all(w.ops[0, 6:] == 1)
