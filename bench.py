@@ -86,6 +86,33 @@ def timed_run(wl, precision, steps, warmup, torch):
     return run, total_ms, wall, phase
 
 
+def timed_layers(wl, L, precision, steps, warmup, torch):
+    """fwd + bwd of L stacked layers on the workload's op streams (chained single-layer
+    calls, every step on the GPU), timed with events per step."""
+    from paper_1904_03409_amd.stacklstm import multilayer_runs
+    from paper_1904_03409_amd.workloads import layer_params
+    layers, h0, c0 = layer_params(wl, L)
+    runs = multilayer_runs(wl.ops, wl.x, layers, h0, c0, wl.dh_top, None, precision=precision)
+
+    def step():
+        for r in runs:
+            r.forward()
+        for r in reversed(runs):
+            r.backward()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs:
+        a.record()
+        step()
+        b.record()
+    torch.cuda.synchronize()
+    per = [a.elapsed_time(b) for a, b in evs]
+    del runs
+    return per
+
+
 def flops(wl):
     T, B, I, H = wl.T, wl.B, wl.I, wl.H
     rec = 2.0 * T * B * H * 4 * H                 # one recurrent contraction (h_prev U or dA U^T)
@@ -240,6 +267,8 @@ def main():
     ap.add_argument("--precision", choices=["fp32", "bf16"], default=None)
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-GEMM run of the same shape")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--layers", type=int, default=1,
+                    help="stacked StackLSTM layers sharing the op streams (the stack element holds every layer)")
     ap.add_argument("--sweep", action="store_true",
                     help="batch-scaling sweep B = 1..1024 of the parser shape and its Amdahl fit (one JSON line)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -255,6 +284,23 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     if args.sweep:
         print(json.dumps(sweep(args, torch)), flush=True)
+        return
+    if args.layers > 1:
+        wl = workloads.make(args.config)
+        prec = wl.precision if args.precision is None else (0 if args.precision == "fp32" else 1)
+        per = timed_layers(wl, args.layers, prec, args.steps, args.warmup, torch)
+        ms = float(np.mean(per))
+        T, B, I, H = wl.T, wl.B, wl.I, wl.H
+        fl = 3 * 2.0 * T * B * 4 * H * (I + H) + (args.layers - 1) * 3 * 2.0 * T * B * 4 * H * (2 * H)
+        dname = "f32" if prec == 0 else "bf16"
+        print(json.dumps({
+            "metric": "fwd+bwd batch·timesteps/sec, stacked StackLSTM layers", "value": B * T / (ms / 1e3),
+            "unit": "element-steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+            "step_ms_median": float(np.median(per)), "step_ms_min": float(np.min(per)), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": dname, "data": "synthetic",
+            "config": {"workload": f"{args.config}: {args.layers} stacked layers, B={B} T={T} I={I} H={H}",
+                       "layers": args.layers, "global_batch": B, "seq_len": T, "parallelism": "none (1 GPU)"},
+            "overall_mfma_frac": fl / (ms / 1e3) / 1e12 / PEAK[dname]}), flush=True)
         return
     wl = workloads.make(args.config)
     prec = wl.precision if args.precision is None else (0 if args.precision == "fp32" else 1)

@@ -12,6 +12,7 @@ import os
 from dataclasses import dataclass
 from typing import Optional
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -212,3 +213,47 @@ class DeviceRun:
             if v is not None:
                 out[k] = v.cpu().numpy()
         return out
+
+
+def multilayer_runs(ops, x, layers, h0, c0, dh_top, dc_top=None, device="cuda", precision: int = 0,
+                    want_top: bool = True) -> list:
+    """Device buffers for L stacked StackLSTM layers driven by one op stream: the stack
+    element holds every layer's state, so layer l (l > 0) reads as its input at step t
+    the state at the top of layer l-1 after that step (on push steps the state layer l-1
+    just produced; on pop and hold steps the written state is discarded and its
+    gradient is exactly zero). Layer l's input buffer is layer l-1's h_top buffer, and
+    in the backward layer l-1's dh_top buffer is layer l's dx buffer, so running
+    [r.forward() for r in runs] and then [r.backward() for r in reversed(runs)] is the
+    multi-layer forward and backward (every step on the GPU; this only wires buffers).
+
+    ops [T, B] int8, x [T, B, I], layers = [(W_l, U_l, b_l)] with W_1 [I, 4H] and W_l
+    [H, 4H] after, h0/c0 = per layer [B, H], dh_top/dc_top [T, B, H] on the last layer.
+    """
+    T, B = ops.shape
+    H = layers[0][1].shape[0]
+    dev = torch.device(device)
+    up = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    e = lambda *sh: torch.empty(*sh, dtype=torch.float32, device=dev)
+    ops_d = up(np.asarray(ops, dtype=np.int8))
+    runs = []
+    prev_top = up(np.asarray(x, dtype=np.float32))
+    for l, (W, U, bias) in enumerate(layers):
+        I = W.shape[0]
+        dims = make_dims(T, B, I, H, precision, 0)
+        ws = stacklstm_workspace_bytes(dims)
+        if ws == 0:
+            raise StackLSTMError(1, "stacklstm_workspace_bytes")
+        last = l == len(layers) - 1
+        r = DeviceRun(dims=dims, x=prev_top, ops=ops_d, W=up(W), U=up(U), b=up(bias), h0=up(h0[l]), c0=up(c0[l]),
+                      dh_top=up(dh_top) if last else None, dc_top=up(dc_top) if last else None,
+                      h_cell=e(T, B, H), c_cell=e(T, B, H), h_top=e(T, B, H),
+                      c_top=e(T, B, H) if (want_top or not last) else None,
+                      ptr=torch.empty(T + 1, B, dtype=torch.int32, device=dev),
+                      top=torch.empty(T, B, dtype=torch.int32, device=dev),
+                      workspace=torch.empty(ws, dtype=torch.uint8, device=dev), dx=e(T, B, I), dW=e(I, 4 * H),
+                      dU=e(H, 4 * H), db=e(4 * H), dh0=e(B, H), dc0=e(B, H))
+        if l > 0:
+            runs[-1].dh_top = r.dx
+        runs.append(r)
+        prev_top = r.h_top
+    return runs

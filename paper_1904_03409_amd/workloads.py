@@ -209,7 +209,28 @@ CONFIGS = {
     "thru": dict(B=1024, I=512, H=1024, precision=BF16_GEMM, seed=105, kind="arc", nlo=10, nhi=128, wscale=0.08, bias_zero=False),
     # B counts sentences; the workload has 2B rows (stack StackLSTMs, then buffer StackLSTMs)
     "hybrid": dict(B=128, I=256, H=512, precision=FP32, seed=106, kind="hybrid", nlo=20, nhi=80, wscale=0.08, bias_zero=False),
+    # the paper's cell size (hidden dimension 200 for every LSTM, section 4.1) on the
+    # arc-hybrid stack + buffer streams of a batch of 64 sentences
+    "paper": dict(B=64, I=200, H=200, precision=FP32, seed=107, kind="hybrid", nlo=10, nhi=60, wscale=0.08, bias_zero=False),
 }
+
+
+def layer_params(wl: Workload, L: int) -> tuple:
+    """Parameters of L stacked layers for a workload: layer 1 is the workload's own (W, U,
+    b, h0, c0); layers 2..L (input size H) are drawn from default_rng(seed + 1000 + l) with
+    the workload's recipe (weights and bias U(-0.08, 0.08), zero initial state)."""
+    seed = int(wl.meta.get("seed", 0))
+    layers = [(wl.W, wl.U, wl.b)]
+    h0, c0 = [wl.h0], [wl.c0]
+    for l in range(1, L):
+        rng = np.random.default_rng(seed + 1000 + l)
+        H = wl.H
+        layers.append((rng.uniform(-0.08, 0.08, (H, 4 * H)).astype(np.float32),
+                       rng.uniform(-0.08, 0.08, (H, 4 * H)).astype(np.float32),
+                       rng.uniform(-0.08, 0.08, 4 * H).astype(np.float32)))
+        h0.append(np.zeros((wl.B, H), np.float32))
+        c0.append(np.zeros((wl.B, H), np.float32))
+    return layers, h0, c0
 
 
 def make(name: str, seed: Optional[int] = None, precision: Optional[int] = None, B: Optional[int] = None,
