@@ -22,10 +22,12 @@ __global__ void k_zero_u32(uint32_t* p, int n);
 __global__ void k_fill_pattern(unsigned char* p, size_t bytes, uint32_t v);
 __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
-__global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const bf16_t* hx, void* out,
-                               int T, int B, int H);
-__global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int rows, int cols, const int32_t* gtop, int B,
-                                 bf16_t* out);
+__global__ void k_push_rows(const int8_t* ops, int n, int32_t* rows, uint32_t* count);
+__global__ void k_zero_nonpush_rows(const int8_t* ops, float* out, size_t n, int cols);
+__global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const int32_t* prow,
+                               const uint32_t* count, float* out, int T, int B, int H);
+__global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int cols, const int32_t* prow,
+                                 const uint32_t* count, int ldo, const int32_t* gtop, int B, bf16_t* out);
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
@@ -65,8 +67,11 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, total;
+  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, prow, total;
 };
+
+// Push-row count padded to the K tile: leading dimension of the transposed bf16 operands
+size_t padded_rows(const slstm_dims* d) { return ((size_t)d->T * d->B + 63) / 64 * 64; }
 
 bool dims_ok(const slstm_dims* d) {
   if (!d) return false;
@@ -147,6 +152,7 @@ int make_plan(const slstm_dims* d, Plan* p) {
 Layout layout(const slstm_dims* d) {
   const size_t T = d->T, B = d->B, I = d->I, H = d->H;
   const bool bf = d->precision == SLSTM_BF16_GEMM;
+  const size_t KP = padded_rows(d);
   Layout L;
   size_t o = 0;
   L.ctl = o; o += align256(CTL_WORDS * 4);
@@ -156,13 +162,15 @@ Layout layout(const slstm_dims* d) {
   L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
   L.hx = o; o += bf ? align256((T + 1) * B * H * 2) : 0;
   L.xb = o; o += bf ? align256(T * B * I * 2) : 0;                    // x in bf16 (bf16 mode)
-  L.xbt = o; o += bf ? align256(T * B * I * 2) : 0;                   // x^T in bf16 (bf16 mode)
-  L.hp = o; o += align256(std::max<size_t>(T * B * H * (bf ? 2 : 4), 16));   // Hprev (bf16 mode: Hprev^T)
-  L.dat = o; o += bf ? align256(T * B * 4 * H * 2) : 0;               // dA^T in bf16 (bf16 mode)
+  // post-loop operands over the push rows (at most T*B of them; KP with the K-tile padding)
+  L.xbt = o; o += bf ? align256(KP * I * 2) : 0;                      // x^T in bf16 (bf16 mode)
+  L.hp = o; o += align256(std::max<size_t>(bf ? KP * H * 2 : T * B * H * 4, 16));   // Hprev (bf16 mode: Hprev^T)
+  L.dat = o; o += bf ? align256(KP * 4 * H * 2) : 0;                  // dA^T in bf16 (bf16 mode)
   L.dh = o; o += align256((T + 1) * B * H * 4);
   L.dc = o; o += align256((T + 1) * B * H * 4);
   L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
   L.part = o; o += align256((size_t)64 * std::max(I, H) * 4 * H * 4);
+  L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
   L.total = o;
   return L;
 }
@@ -388,6 +396,10 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   a.db_part = (float*)(ws + L.dbp);
   a.dh0 = dh0; a.dc0 = dc0;
   if (a.clk) a.clk += (size_t)512 * T * 4;
+  // rows of the push steps, for the post-loop gradients (dA is exactly zero on other rows)
+  int32_t* prow = (int32_t*)(ws + L.prow);
+  const uint32_t* npush = ctl + CTL_NPUSH;
+  hipLaunchKernelGGL(k_push_rows, dim3(1), dim3(1024), 0, st, ops, T * B, prow, ctl + CTL_NPUSH);
   // dA rows start as "not yet produced" (all-one bits): the workgroups read them from each other
   if (a.poll) {
     const size_t da_bytes = (size_t)T * B * 4 * H * (bf ? 2 : 4);
@@ -398,65 +410,69 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if ((rc = hip_status(launch_bwd(a, p.prec, p.NTb, p.KS, dim3(8 * p.per_xcc_b), st, nullptr)))) return rc;
   mark(d, 6, st);
 
-  // a9: post-loop gradients
+  // a9: post-loop gradients, contracted over the push rows only (rows prow[0 .. *npush))
   const int H4 = 4 * H;
   float* part = (float*)(ws + L.part);
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H4)), dim3(256), 0, st, a.db_part, p.Gb, (size_t)H4, 1, H4,
                      H, db);
   const int K = T * B;
-  const size_t esz = bf ? 2 : 4;
-  const void* xa = bf ? (const void*)(ws + L.xb) : (const void*)x;
-  GemmArgs g;
-  // dW = x^T dA and dU = Hprev^T dA. In bf16 mode both operands are first written
-  // transposed (k = step*B + element contiguous), so the GEMM reads k-contiguous rows.
+  const int KP = (int)padded_rows(d);
   void* hp = ws + L.hp;
-  const void* dAt = a.dA;
+  GemmArgs g;
+  auto gemm_base = [&]() {
+    memset(&g, 0, sizeof(g));
+    g.dyn = npush;
+    g.dyn_round = bf ? 64 : 1;
+  };
+  // dW = x^T dA and dU = Hprev^T dA over the push rows. fp32: the GEMM gathers x and dA rows
+  // through prow, Hprev is gathered first; bf16: the three operands are written transposed
+  // and compacted (k = push index contiguous, zero up to the next multiple of 64).
   if (bf) {
-    const dim3 tg4((H4 + 63) / 64, (K + 63) / 64), tgI((I + 63) / 64, (K + 63) / 64), tgH((H + 63) / 64, (K + 63) / 64);
-    hipLaunchKernelGGL(k_transpose_bf16, tg4, dim3(256), 0, st, a.dA, 0, H4, K, H4, (const int32_t*)nullptr, B,
-                       (bf16_t*)(ws + L.dat));
-    hipLaunchKernelGGL(k_transpose_bf16, tgI, dim3(256), 0, st, x, 1, I, K, I, (const int32_t*)nullptr, B,
-                       (bf16_t*)(ws + L.xbt));
-    hipLaunchKernelGGL(k_transpose_bf16, tgH, dim3(256), 0, st, ws + L.hx, 0, H, K, H, top, B, (bf16_t*)hp);
-    dAt = ws + L.dat;
+    const dim3 tg4((H4 + 63) / 64, KP / 64), tgI((I + 63) / 64, KP / 64), tgH((H + 63) / 64, KP / 64);
+    hipLaunchKernelGGL(k_transpose_bf16, tg4, dim3(256), 0, st, a.dA, 0, H4, H4, prow, npush, KP,
+                       (const int32_t*)nullptr, B, (bf16_t*)(ws + L.dat));
+    hipLaunchKernelGGL(k_transpose_bf16, tgI, dim3(256), 0, st, x, 1, I, I, prow, npush, KP, (const int32_t*)nullptr,
+                       B, (bf16_t*)(ws + L.xbt));
+    hipLaunchKernelGGL(k_transpose_bf16, tgH, dim3(256), 0, st, ws + L.hx, 0, H, H, prow, npush, KP, top, B,
+                       (bf16_t*)hp);
   } else {
-    hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0,
-                       (const bf16_t*)nullptr, hp, T, B, H);
+    hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0, prow, npush,
+                       (float*)hp, T, B, H);
   }
-  memset(&g, 0, sizeof(g));
-  g.M = I; g.N = H4; g.K = K;
-  const int VE = bf ? 8 : 4;
-  if (bf) { g.A = ws + L.xbt; g.lda = K; g.a_vec = (K % 8 == 0); g.Bm = dAt; g.ldb = K; g.b_vec = (K % 8 == 0); }
-  else    { g.A = x; g.lda = I; g.a_vec = (I % 4 == 0) && (K % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (K % 4 == 0); }
+  gemm_base();
+  g.M = I; g.N = H4; g.dyn_axis = 1;
+  if (bf) { g.K = KP; g.A = ws + L.xbt; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1; }
+  else    { g.K = K; g.A = x; g.lda = I; g.a_vec = (I % 4 == 0); g.a_rows = prow;
+            g.Bm = a.dA; g.ldb = H4; g.b_vec = 1; g.b_rows = prow; }
   g.C = part; g.ldc = H4;
-  g.k_chunk = k_chunk_for(K, p.splits_w);
-  int sw = (K + g.k_chunk - 1) / g.k_chunk;
   g.split_stride = (size_t)I * H4;
-  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, sw, st))) return rc;
-  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, sw, g.split_stride, I,
-                     H4, H, dW);
+  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, p.splits_w, st))) return rc;
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, p.splits_w,
+                     g.split_stride, I, H4, H, dW);
   mark(d, 7, st);
-  memset(&g, 0, sizeof(g));
-  g.M = H; g.N = H4; g.K = K;
-  if (bf) { g.A = hp; g.lda = K; g.a_vec = (K % 8 == 0); g.Bm = dAt; g.ldb = K; g.b_vec = (K % 8 == 0); }
-  else    { g.A = hp; g.lda = H; g.a_vec = (H % 4 == 0) && (K % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = (K % 4 == 0); }
+  gemm_base();
+  g.M = H; g.N = H4; g.dyn_axis = 1;
+  if (bf) { g.K = KP; g.A = hp; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1; }
+  else    { g.K = K; g.A = hp; g.lda = H; g.a_vec = (H % 4 == 0); g.Bm = a.dA; g.ldb = H4; g.b_vec = 1;
+            g.b_rows = prow; }
   g.C = part; g.ldc = H4;
-  g.k_chunk = k_chunk_for(K, p.splits_u);
-  int su = (K + g.k_chunk - 1) / g.k_chunk;
   g.split_stride = (size_t)H * H4;
-  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, su, st))) return rc;
-  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, su, g.split_stride, H,
-                     H4, H, dU);
+  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, p.splits_u, st))) return rc;
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, p.splits_u,
+                     g.split_stride, H, H4, H, dU);
   mark(d, 8, st);
-  // dx = dA Wp^T
-  memset(&g, 0, sizeof(g));
+  // dx = dA Wp^T on the push rows (gathered from dA, scattered into dx); 0 on the others
+  gemm_base();
+  g.dyn_round = 1; g.dyn_axis = 0;
   g.M = K; g.N = I; g.K = H4;
-  g.A = a.dA; g.lda = H4; g.a_vec = (H4 % VE == 0);
+  const int VE = bf ? 8 : 4;
+  g.A = a.dA; g.lda = H4; g.a_vec = (H4 % VE == 0); g.a_rows = prow;
   g.Bm = ws + L.wp; g.ldb = H4; g.b_vec = (H4 % VE == 0) && (I % VE == 0);
-  g.C = dx; g.ldc = I;
+  g.C = dx; g.ldc = I; g.c_rows = prow;
   g.k_chunk = k_chunk_for(H4, 1);
-  (void)esz;
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, 1, st))) return rc;
+  hipLaunchKernelGGL(k_zero_nonpush_rows, dim3(grid1d((size_t)K * I / 4 + 1)), dim3(256), 0, st, ops, dx, (size_t)K,
+                     I);
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 9, st);
   if (d->spin_limit > 0) return check_timeout(ctl, st);

@@ -13,4 +13,14 @@ struct GemmArgs {
   float* C; int ldc;                   // C[m*ldc+n] (+ split index * split_stride)
   const float* bias; int bias_H;       // + bias[caller column of n] when non-null
   int k_chunk; size_t split_stride;
+  // Row gathers (null = identity). A stored row j of A (MK: j = m, KM: j = k) is row
+  // a_rows[j] of the array; likewise b_rows for B (KN: j = k, NK: j = n); C row m is
+  // written to row c_rows[m]. Indices must lie within the array's static extent.
+  const int32_t* a_rows;
+  const int32_t* b_rows;
+  const int32_t* c_rows;
+  // Device-side extent (null = none): M (dyn_axis 0) or K (dyn_axis 1) becomes
+  // min(static extent, *dyn rounded up to a multiple of dyn_round). With a device K the
+  // K range is cut into gridDim.z slices at run time (k_chunk is then ignored).
+  const uint32_t* dyn; int dyn_axis; int dyn_round;
 };

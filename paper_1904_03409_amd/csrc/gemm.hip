@@ -8,6 +8,9 @@
 // 128x128 block tile, four 64x64 wave tiles, K slices of BK; the next slice is fetched
 // into registers while the current one is multiplied (two LDS buffers, one barrier per
 // slice). Split K writes partials that k_reduce_splits adds in a fixed order.
+// The gradient GEMMs run over the push rows only (dA is exactly zero elsewhere): rows of
+// A, B and C can be gathered through index tables, and M or K can come from a device-side
+// count, so the host launches them without knowing how many rows are pushes.
 #include "common.h"
 #include "gemm.h"
 
@@ -38,6 +41,20 @@ template <int P, bool KMAJOR> struct Stage {
   static constexpr int BK = Cfg<P>::BK, VE = Cfg<P>::VE;
   static constexpr int NV = 128 * BK / VE / 256;
   uint4 v[NV];
+  int prow[KMAJOR ? 1 : NV];   // array rows of this thread's vectors in an [m/n][k] tile (fixed over k)
+
+  // Array row of tile row gr: the gather table's entry, or gr itself. Tiles stored [m/n][k]
+  // keep the same rows for every K slice, so they are resolved once (set_rows); k-major
+  // tiles look their rows up per slice.
+  __device__ __forceinline__ void set_rows(const int32_t* __restrict__ rows, int r0, int rlim) {
+    if constexpr (!KMAJOR) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int gr = r0 + (threadIdx.x + 256 * i) / (BK / VE);
+        prow[i] = (rows && gr < rlim) ? rows[gr] : gr;
+      }
+    }
+  }
 
   // global tile element (r, c): KMAJOR -> row r in [0,BK) of k, col c in [0,128) of m/n;
   // otherwise row r in [0,128) of m/n, col c in [0,BK) of k. The vector path goes through a
@@ -45,7 +62,7 @@ template <int P, bool KMAJOR> struct Stage {
   // offset beyond the buffer, which reads 0 without a branch or a memory access. It needs
   // the row stride and both limits to be multiples of VE (checked by the host).
   __device__ __forceinline__ void load(const T* __restrict__ base, size_t bytes, int ld, int r0, int rlim, int c0,
-                                       int clim, bool vec) {
+                                       int clim, bool vec, const int32_t* __restrict__ rows) {
     if (vec) {
       const rsrc_t rs = make_rsrc(base, bytes);
 #pragma unroll
@@ -55,7 +72,11 @@ template <int P, bool KMAJOR> struct Stage {
         if (KMAJOR) { r = e / (128 / VE); c = (e % (128 / VE)) * VE; }
         else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
         const int gr = r0 + r, gc = c0 + c;
-        const uint32_t off = (gr < rlim && gc < clim) ? (uint32_t)(((size_t)gr * ld + gc) * sizeof(T)) : 0xffffffffu;
+        const bool ok = gr < rlim && gc < clim;
+        int pr;
+        if constexpr (KMAJOR) pr = (rows && gr < rlim) ? rows[gr] : gr;
+        else pr = prow[i];
+        const uint32_t off = ok ? (uint32_t)(((size_t)pr * ld + gc) * sizeof(T)) : 0xffffffffu;
         v[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
       }
       return;
@@ -67,9 +88,12 @@ template <int P, bool KMAJOR> struct Stage {
       if (KMAJOR) { r = e / (128 / VE); c = (e % (128 / VE)) * VE; }
       else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
       const int gr = r0 + r, gc = c0 + c;
+      int pr;
+      if constexpr (KMAJOR) pr = (rows && gr < rlim) ? rows[gr] : gr;
+      else pr = prow[i];
       T tmp[VE];
 #pragma unroll
-      for (int j = 0; j < VE; ++j) tmp[j] = (gr < rlim && gc + j < clim) ? base[(size_t)gr * ld + gc + j] : (T)0;
+      for (int j = 0; j < VE; ++j) tmp[j] = (gr < rlim && gc + j < clim) ? base[(size_t)pr * ld + gc + j] : (T)0;
       v[i] = *(const uint4*)tmp;
     }
   }
@@ -108,8 +132,19 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
   __shared__ __align__(16) T As[2][GA::ELEMS];
   __shared__ __align__(16) T Bs[2][GB::ELEMS];
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kbeg = blockIdx.z * g.k_chunk;
-  const int kend = min(g.K, kbeg + g.k_chunk);
+  int M = g.M, K = g.K, kchunk = g.k_chunk;
+  if (g.dyn) {
+    const int ext = (int)((*g.dyn + (uint32_t)g.dyn_round - 1u) / (uint32_t)g.dyn_round * (uint32_t)g.dyn_round);
+    if (g.dyn_axis == 0) {
+      M = min(M, ext);
+    } else {
+      K = min(K, ext);
+      kchunk = ((K + (int)gridDim.z - 1) / (int)gridDim.z + 63) / 64 * 64;
+    }
+  }
+  if (m0 >= M) return;                              // a whole block past a device-side M
+  const int kbeg = blockIdx.z * kchunk;
+  const int kend = min(K, kbeg + kchunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int l16 = lane & 15, lq = lane >> 4;
@@ -118,13 +153,16 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
 
   Stage<P, AKM> sa;
   Stage<P, BKN> sb;
+  // buffer extents: the arrays' static sizes (gathered rows index within them)
   const size_t abytes = (AKM ? (size_t)g.K * g.lda : (size_t)g.M * g.lda) * sizeof(T);
   const size_t bbytes = (BKN ? (size_t)g.K * g.ldb : (size_t)g.N * g.ldb) * sizeof(T);
+  if (!AKM) sa.set_rows(g.a_rows, m0, M);
+  if (!BKN) sb.set_rows(g.b_rows, n0, g.N);
   auto fetch = [&](int k0) {
-    if (AKM) sa.load(A, abytes, g.lda, k0, kend, m0, g.M, g.a_vec);
-    else     sa.load(A, abytes, g.lda, m0, g.M, k0, kend, g.a_vec);
-    if (BKN) sb.load(Bp, bbytes, g.ldb, k0, kend, n0, g.N, g.b_vec);
-    else     sb.load(Bp, bbytes, g.ldb, n0, g.N, k0, kend, g.b_vec);
+    if (AKM) sa.load(A, abytes, g.lda, k0, kend, m0, M, g.a_vec, g.a_rows);
+    else     sa.load(A, abytes, g.lda, m0, M, k0, kend, g.a_vec, g.a_rows);
+    if (BKN) sb.load(Bp, bbytes, g.ldb, k0, kend, n0, g.N, g.b_vec, g.b_rows);
+    else     sb.load(Bp, bbytes, g.ldb, n0, g.N, k0, kend, g.b_vec, g.b_rows);
   };
 
   f32x4 acc[4][4];
@@ -205,7 +243,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm * 64 + i * 16 + 4 * lq + r;
-        if (m < g.M) C[(size_t)m * g.ldc + n] = acc[i][j][r] + bv;
+        if (m < M) C[(size_t)(g.c_rows ? g.c_rows[m] : m) * g.ldc + n] = acc[i][j][r] + bv;
       }
     }
 }

@@ -127,48 +127,121 @@ __global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ in, b
     out[i] = f32_to_bf16_bits(in[i]);
 }
 
-// Hprev[t][b][:] = the state read at step t: h0[b] for t = 0, else the state produced at step
-// top[t-1][b] (-1 = h0). fp32 rows from h_cell, or bf16 rows from the bf16 state copy (slot
-// s+1 = step s, slot 0 = h0) in bf16-GEMM mode.
+// Push-row list: rows[k] = t*B + b of the k-th push (op = +1) in increasing row order, and
+// *count = the number of pushes. Only push steps have a non-zero gate gradient dA (the
+// states other steps write are never read, section 3, Observation 2), so the post-loop
+// gradients dW, dU and dx contract over these rows only. One workgroup: tiles of 32 K ops
+// go through LDS, each thread counts and writes 32 consecutive ops, offsets from a
+// workgroup scan of the counts.
+__global__ void __launch_bounds__(1024) k_push_rows(const int8_t* __restrict__ ops, int n, int32_t* __restrict__ rows,
+                                                    uint32_t* __restrict__ count) {
+  constexpr int TILE = 32768, PER = 32;
+  __shared__ __align__(16) int8_t s_ops[TILE];
+  __shared__ int s_wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int base = 0;
+  for (int t0 = 0; t0 < n; t0 += TILE) {
+    const int len = min(TILE, n - t0);
+    for (int i = tid; i < TILE; i += 1024) s_ops[i] = i < len ? ops[(size_t)t0 + i] : (int8_t)0;
+    __syncthreads();
+    const uint4 q0 = *(const uint4*)&s_ops[tid * PER], q1 = *(const uint4*)&s_ops[tid * PER + 16];
+    const uint32_t w[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+    uint32_t mask = 0;                               // bit j: op j of this thread is a push
+#pragma unroll
+    for (int j = 0; j < PER; ++j) mask |= (((w[j >> 2] >> (8 * (j & 3))) & 0xffu) == 1u ? 1u : 0u) << j;
+    const int cnt = __popc(mask);
+    int incl = cnt;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(incl, d, 64);
+      if (lane >= d) incl += v;
+    }
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int wbase = 0, total = 0;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int x = s_wsum[v];
+      wbase += v < wave ? x : 0;
+      total += x;
+    }
+    int pos = base + wbase + incl - cnt;
+    while (mask) {
+      const int j = __builtin_ctz(mask);
+      mask &= mask - 1;
+      rows[pos++] = t0 + tid * PER + j;
+    }
+    base += total;
+    __syncthreads();
+  }
+  if (tid == 0) *count = (uint32_t)base;
+}
+
+// Zeroes the rows of out [n][cols] whose op is not a push (dx is exactly 0 there).
+__global__ void __launch_bounds__(256) k_zero_nonpush_rows(const int8_t* __restrict__ ops, float* __restrict__ out,
+                                                           size_t n, int cols) {
+  const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, nth = (size_t)gridDim.x * blockDim.x;
+  if ((cols & 3) == 0 && ((uintptr_t)out & 15) == 0) {
+    const int cv = cols >> 2;
+    const size_t nv = n * cv;
+    for (size_t i = tid; i < nv; i += nth)
+      if (ops[i / cv] != 1) ((float4*)out)[i] = float4{0.f, 0.f, 0.f, 0.f};
+    return;
+  }
+  for (size_t i = tid; i < n * cols; i += nth)
+    if (ops[i / cols] != 1) out[i] = 0.f;
+}
+
+// Hprev rows of the push steps: out[k][:] = the state read at the step of row prow[k] =
+// t*B + b, for k < *count: h0[b] for t = 0, else the state produced at step top[t-1][b]
+// (-1 = h0), from h_cell (fp32).
 __global__ void __launch_bounds__(256) k_gather_hprev(const int32_t* __restrict__ top, const float* __restrict__ hcell,
-                                                      const float* __restrict__ h0, const bf16_t* __restrict__ hx,
-                                                      void* __restrict__ out, int T, int B, int H) {
-  const size_t n = (size_t)T * B * H;
+                                                      const float* __restrict__ h0, const int32_t* __restrict__ prow,
+                                                      const uint32_t* __restrict__ count, float* __restrict__ out,
+                                                      int T, int B, int H) {
+  const size_t n = (size_t)min(*count, (uint32_t)T * (uint32_t)B) * H;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-    size_t tb = i / H;
-    int u = (int)(i - tb * H);
-    int t = (int)(tb / B), b = (int)(tb - (size_t)t * B);
+    const size_t k = i / H;
+    const int u = (int)(i - k * H);
+    const int tb = prow[k];
+    const int t = tb / B, b = tb - t * B;
     int s = (t == 0) ? -1 : top[tb - B];
     if (s < -1 || s >= t) s = -1;                 // only a valid producer is ever indexed
-    if (hx) ((bf16_t*)out)[i] = hx[((size_t)(s + 1) * B + b) * H + u];
-    else ((float*)out)[i] = (s < 0) ? h0[(size_t)b * H + u] : hcell[((size_t)s * B + b) * H + u];
+    out[i] = (s < 0) ? h0[(size_t)b * H + u] : hcell[((size_t)s * B + b) * H + u];
   }
 }
 
-// Tiled transpose to bf16: out[c][r] = bf16(row r, column c) for r < rows, c < cols, where
-// row r is src + r*ld (fp32 or bf16). With a producer table (gtop != null) row r = t*B + b is
-// the state read at step t (Hprev): h0[b] for t = 0, else the state produced at top[t-1][b]
-// (-1 = h0), taken from the bf16 state copy (slot s+1 = step s, slot 0 = h0).
+// Gathering transpose to bf16 over the push rows: out[c][k] = bf16(row prow[k], column c)
+// for k < *count, and 0 for *count <= k < (*count rounded up to 64), so a GEMM over the
+// rounded K adds nothing past the last push; columns beyond are not written. The source row
+// r is src + r*ld (fp32 or bf16); with a producer table (gtop != null) row r = t*B + b is
+// the state read at step t (Hprev): h0[b] for t = 0, else the state produced at
+// top[t-1][b] (-1 = h0), taken from the bf16 state copy (slot s+1 = step s, slot 0 = h0).
 // 64x64 tiles through LDS: reads and writes are both along contiguous rows.
-__global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__ src, int src_f32, int ld, int rows,
-                                                        int cols, const int32_t* __restrict__ gtop, int B,
+__global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__ src, int src_f32, int ld, int cols,
+                                                        const int32_t* __restrict__ prow,
+                                                        const uint32_t* __restrict__ count, int ldo,
+                                                        const int32_t* __restrict__ gtop, int B,
                                                         bf16_t* __restrict__ out) {
   __shared__ bf16_t tile[64][66];
+  const int rows = (int)min(*count, (uint32_t)ldo);
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  if (r0 >= rows + ((64 - (rows & 63)) & 63)) return;      // past the rounded extent
   const int tc = threadIdx.x & 63, tr = threadIdx.x >> 6;   // 4 rows per pass
   for (int i = tr; i < 64; i += 4) {
     const int r = r0 + i, c = c0 + tc;
     bf16_t v = 0;
     if (r < rows && c < cols) {
+      const int pr = prow[r];
       if (gtop) {
-        const int t = r / B, b = r - t * B;
-        int s = (t == 0) ? -1 : gtop[(size_t)r - B];
+        const int t = pr / B, b = pr - t * B;
+        int s = (t == 0) ? -1 : gtop[(size_t)pr - B];
         if (s < -1 || s >= t) s = -1;                        // only a valid producer is ever indexed
         v = ((const bf16_t*)src)[((size_t)(s + 1) * B + b) * ld + c];
       } else if (src_f32) {
-        v = f32_to_bf16_bits(((const float*)src)[(size_t)r * ld + c]);
+        v = f32_to_bf16_bits(((const float*)src)[(size_t)pr * ld + c]);
       } else {
-        v = ((const bf16_t*)src)[(size_t)r * ld + c];
+        v = ((const bf16_t*)src)[(size_t)pr * ld + c];
       }
     }
     tile[i][tc] = v;
@@ -176,6 +249,6 @@ __global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__
   __syncthreads();
   for (int i = tr; i < 64; i += 4) {
     const int c = c0 + i, r = r0 + tc;
-    if (c < cols && r < rows) out[(size_t)c * rows + r] = tile[tc][i];
+    if (c < cols && r < ldo) out[(size_t)c * ldo + r] = tile[tc][i];
   }
 }
