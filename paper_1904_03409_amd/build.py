@@ -10,7 +10,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libstacklstm.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "scan.hip", "gemm.hip", "recurrent_fwd.hip", "recurrent_fwd_pipe.hip", "recurrent_bwd.hip"]
+SOURCES = ["api.hip", "scan.hip", "gemm.hip", "recurrent_fwd.hip", "recurrent_fwd_pipe.hip", "recurrent_bwd.hip",
+           "recurrent_fwd_wide.hip"]
+# per-file flags: the wide forward keeps its U slice in AGPRs and its accumulators in VGPRs
+EXTRA = {"recurrent_fwd_wide.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # packed fp32 instructions stay off: only scalar fp32 ALU code is generated
@@ -19,7 +22,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)

@@ -15,7 +15,8 @@
 __global__ void k_init_ctl(uint32_t* ctl);
 __global__ void k_scan(const int8_t* ops, int T, int B, int32_t* ptr, uint32_t* ctl);
 __global__ void k_gather_top(const int32_t* top, const float* cellv, const float* init, float* out, int T, int B,
-                             int H);
+                             int H, int skip_push);
+__global__ void k_trace(const int8_t* ops, int T, int B, int cap, int32_t* top);
 __global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
@@ -62,6 +63,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct Plan {
   int prec, KS, ks_eff, NW;
   int NT, G, per_xcc, pipe;   // pipe: the forward runs the pipelined kernel
+  int wide, NWw;              // wide: the forward runs the 32-unit kernel (NWw workgroups per group)
   int NTb, Gb, per_xcc_b;
   int splits_w, splits_u;
 };
@@ -139,7 +141,25 @@ int make_plan(const slstm_dims* d, Plan* p) {
     }
     return SLSTM_ENORESIDENT;
   };
-  int rc = pick(false, &p->NT, &p->G, &p->per_xcc, &p->pipe);
+  // bf16 with H > 512: 16-unit workgroups would need two per CU and spill their U slice;
+  // the wide forward gives each CU one workgroup of 32 units (groups of 128 rows, one per XCC)
+  p->wide = 0;
+  p->NWw = (d->H + 31) / 32;
+  if (prec == SLSTM_BF16_GEMM && d->H > 512 && d->H % 8 == 0 && p->KS == 32 && p->NWw <= cu_per_xcc &&
+      (d->B + 127) / 128 <= 8) {
+    int occ = 0;
+    RecArgs dummy;
+    memset(&dummy, 0, sizeof(dummy));
+    if (launch_fwd_wide(dummy, 8, 32, dim3(0), nullptr, &occ) != hipSuccess) return SLSTM_EDEVICE;
+    if (occ >= 1) {
+      p->wide = 1;
+      p->NT = 8;
+      p->G = (d->B + 127) / 128;
+      p->per_xcc = p->NWw;
+      p->pipe = 0;
+    }
+  }
+  int rc = p->wide ? SLSTM_OK : pick(false, &p->NT, &p->G, &p->per_xcc, &p->pipe);
   if (rc) return rc;
   if ((rc = pick(true, &p->NTb, &p->Gb, &p->per_xcc_b, nullptr))) return rc;
   int64_t K = (int64_t)d->T * d->B;
@@ -270,7 +290,7 @@ int stacklstm_plan(const slstm_dims* d, int32_t* groups, int32_t* wg_per_group, 
   int rc = make_plan(d, &p);
   if (rc) return rc;
   if (groups) *groups = p.G;
-  if (wg_per_group) *wg_per_group = p.NW;
+  if (wg_per_group) *wg_per_group = p.wide ? p.NWw : p.NW;
   if (rows_per_group) *rows_per_group = 16 * p.NT;
   if (k_chunks) *k_chunks = p.ks_eff;
   return SLSTM_OK;
@@ -301,6 +321,15 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if (hipMemcpyAsync(hs, ctl + CTL_STATUS, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
   if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
   if (hs[0] != 0x7fffffffu) return (int)(hs[0] & 7u);
+  if (T > 0 && p.wide) {
+    // producer trace from the ops (the wide forward keeps no integer stack): one thread per
+    // element, its stack in LDS (odd slot count: no bank conflicts between neighbours)
+    const int cap = (int)std::min<uint32_t>(hs[1] + 2u, (uint32_t)T + 1u) | 1;
+    int R = 64;
+    while (R > 1 && (size_t)R * cap * 4 > 48 * 1024) R /= 2;
+    if ((size_t)R * cap * 4 > 48 * 1024) return SLSTM_EINVAL;   // stack deeper than 12 K slots
+    hipLaunchKernelGGL(k_trace, dim3((B + R - 1) / R), dim3(R), (size_t)R * cap * 4, st, ops, T, B, cap, top);
+  }
   mark(d, 1, st);
   if (T == 0) return SLSTM_OK;
 
@@ -332,23 +361,30 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
   // exchange buffers start as "not yet produced": all-one bits in the state rows the
   // workgroups read from each other, kTopPending in the producer-index table
-  if (a.poll) {
+  if (a.poll || p.wide) {
     const size_t ex_bytes = (size_t)T * B * H * (bf ? 2 : 4);
     unsigned char* ex = bf ? (unsigned char*)(a.hx + (size_t)B * H) : (unsigned char*)h_cell;
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(ex_bytes / 16 + 1)), dim3(256), 0, st, ex, ex_bytes, 0xffffffffu);
-    hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st, (unsigned char*)top,
-                       (size_t)T * B * 4, kTopPending);
+    if (!p.wide)                                   // the wide forward reads the finished trace
+      hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st,
+                         (unsigned char*)top, (size_t)T * B * 4, kTopPending);
   }
+  a.htop = p.wide ? h_top : nullptr;
+  a.ctop = p.wide ? c_top : nullptr;
+  if (p.wide) a.NW = p.NWw;
   mark(d, 2, st);
-  if ((rc = hip_status(p.pipe ? launch_fwd_pipe(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
-                              : launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr))))
+  if ((rc = hip_status(p.wide   ? launch_fwd_wide(a, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
+                       : p.pipe ? launch_fwd_pipe(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
+                                : launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr))))
     return rc;
   mark(d, 3, st);
 
-  // a7: Algorithm 1's return values
+  // a7: Algorithm 1's return values (the wide forward writes c_top and the h_top of push steps)
   size_t n = (size_t)T * B * H;
-  if (h_top) hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H);
-  if (c_top) hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, c_top, T, B, H);
+  if (h_top)
+    hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H, p.wide);
+  if (c_top && !p.wide)
+    hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, c_top, T, B, H, 0);
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 4, st);
   if (d->spin_limit > 0) return check_timeout(ctl, st);

@@ -48,7 +48,15 @@ constexpr bool rec_pipe_built(int prec, int nt, int ks) {
   return prec == 0 ? (ks == 16 || (ks == 32 && nt <= 4)) : ks == 16;
 }
 
+// Wide forward (bf16, H > 512): three 16-row tile buffers of K = 32*KS bf16 columns, the
+// per-tile recurrence state (NT tiles x 4 floats x 256 lanes) and three input-projection
+// slots (2 float4 x 256 lanes).
+constexpr size_t rec_wide_lds_bytes(int ks, int nt) {
+  return (size_t)3 * 16 * (ks * 32 + 8) * 2 + (size_t)nt * 4 * 256 * 4 + (size_t)3 * 2 * 256 * 16;
+}
+
 hipError_t launch_fwd(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);
 hipError_t launch_fwd_pipe(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st,
                            int* occ_out);
+hipError_t launch_fwd_wide(const struct RecArgs& a, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);
 hipError_t launch_bwd(const struct RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out);

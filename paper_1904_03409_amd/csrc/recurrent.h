@@ -23,6 +23,8 @@ struct RecArgs {
   float* stash;          // [T][B][4H] gate activations i, f, g, o, gate-interleaved
   int32_t* top;          // [T][B]     producer step of the state returned at step t (-1 = initial)
   int32_t* stack;        // [B][T+1]   step index written to each stack slot
+  float* htop;           // [T][B][H] or null: state at the top after step t (wide forward writes it)
+  float* ctop;           // [T][B][H] (with htop)
   uint32_t* ctl;         // control block (status, barrier counters)
   // backward
   const float* dh_top;   // [T][B][H]

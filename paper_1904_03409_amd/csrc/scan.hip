@@ -59,11 +59,50 @@ __global__ void __launch_bounds__(256) k_scan(const int8_t* __restrict__ ops, in
   if (threadIdx.x == 0) atomicMax(&ctl[CTL_MAXDEPTH], (uint32_t)s_maxd);
 }
 
+// Producer trace from the ops alone (section 3: the unified update p <- p + op on an
+// integer stack of step indices): top[t][b] = the step that produced the state at the
+// pointer after step t, -1 for the initial state. One thread per batch element keeps its
+// stack of cap slots in LDS (slot 0 = the initial state); the ops of CH steps are staged in
+// LDS at a time. Ops were validated by k_scan, and cap exceeds the deepest pointer.
+__global__ void __launch_bounds__(64) k_trace(const int8_t* __restrict__ ops, int T, int B, int cap,
+                                              int32_t* __restrict__ top) {
+  constexpr int CH = 64;
+  extern __shared__ int s_stk[];                  // [blockDim.x][cap]
+  __shared__ int8_t s_ops[CH][64];
+  const int R = blockDim.x;
+  const int b = blockIdx.x * R + threadIdx.x;
+  int* stk = s_stk + threadIdx.x * cap;
+  int p = 0, tp = -1;
+  stk[0] = -1;
+  for (int t0 = 0; t0 < T; t0 += CH) {
+    const int n = min(CH, T - t0);
+    __syncthreads();
+    for (int i = 0; i < n; ++i) s_ops[i][threadIdx.x] = b < B ? ops[(size_t)(t0 + i) * B + b] : (int8_t)0;
+    __syncthreads();
+    if (b < B) {
+      for (int i = 0; i < n; ++i) {
+        const int op = s_ops[i][threadIdx.x];
+        if (op == 1) {
+          ++p;
+          if (p < cap) stk[p] = t0 + i;
+          tp = t0 + i;
+        } else if (op == -1) {
+          p = p > 0 ? p - 1 : 0;
+          tp = stk[min(p, cap - 1)];
+        }
+        top[(size_t)(t0 + i) * B + b] = tp;
+      }
+    }
+  }
+}
+
 // h_top / c_top materialisation: the state returned at step t (Algorithm 1's return value)
 // is the one produced at step top[t][b], or the initial state when top is -1.
+// With skip_push, rows whose step produced the returned state (top[t] = t) are left as they
+// are (the wide forward kernel writes them).
 __global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ top, const float* __restrict__ cellv,
                                                     const float* __restrict__ init, float* __restrict__ out, int T,
-                                                    int B, int H) {
+                                                    int B, int H, int skip_push) {
   const size_t n = (size_t)T * B * H;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     size_t tb = i / H;
@@ -71,6 +110,7 @@ __global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ 
     int b = (int)(tb % B);
     int s = top[tb];
     int t = (int)(tb / B);
+    if (skip_push && s == t) continue;
     if (s < -1 || s > t) { out[i] = __builtin_nanf(""); continue; }   // not a valid producer
     out[i] = (s < 0) ? init[(size_t)b * H + u] : cellv[((size_t)s * B + b) * H + u];
   }

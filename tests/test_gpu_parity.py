@@ -120,3 +120,31 @@ def test_deterministic(precision):
     b, _ = run_gpu(wl, precision=precision)
     for k in a:
         assert np.array_equal(a[k], b[k]), k
+
+
+WIDE_SHAPES = [
+    # (T, B, I, H): bf16 with H > 512 runs the wide forward (32 units per workgroup, groups of
+    # 128 rows); units past H (544, 776) and rows past B are masked
+    (20, 40, 24, 544),
+    (14, 150, 16, 1024),
+    (9, 8, 8, 776),
+]
+
+
+@pytest.mark.parametrize("shape", WIDE_SHAPES)
+def test_wide_forward(oracle_mod, shape):
+    T, B, I, H = shape
+    from paper_1904_03409_amd.stacklstm import make_dims, stacklstm_plan
+    need_gpu()
+    plan = stacklstm_plan(make_dims(T, B, I, H, 1, 0))
+    assert plan["rows_per_group"] == 128 and plan["wg_per_group"] == (H + 31) // 32, plan
+    wl = wk.custom(T=T, B=B, I=I, H=H, seed=B + H, wscale=0.3, random_state=True, dc_top=True)
+    _check(oracle_mod, wl, 1)
+
+
+@pytest.mark.parametrize("kind", ["all_push", "all_hold", "alternate", "deep"])
+def test_wide_forward_streams(oracle_mod, kind):
+    rng = np.random.default_rng(9)
+    T, B = 48, 24
+    wl = wk.custom(T=T, B=B, I=16, H=640, seed=4, ops=_streams(kind, T, B, rng), wscale=0.2, random_state=True)
+    _check(oracle_mod, wl, 1)
