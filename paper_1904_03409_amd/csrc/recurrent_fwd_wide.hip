@@ -15,7 +15,8 @@
 // Schedule: the NT tiles of a step are independent batch rows and run one pass each; pass
 // q = t*NT + p computes tile p of step t from LDS buffer q%3 while the h_prev rows of tile
 // q+2 are copied into buffer (q+2)%3 (global_load_lds, 1 KB row segments, L1 bypassed).
-// A tile's cell update runs in the next pass, interleaved with that pass's MFMAs. The
+// A tile's cell update runs at the start of the next pass (its stores complete under that
+// pass's MFMAs). The
 // copy of tile q is complete when at most kAfter vector loads are outstanding: every pass
 // issues the same sequence of loads, at least kAfter of them after the copy of tile q,
 // and loads complete in issue order. No barrier waits for memory: workgroup barriers are
@@ -58,28 +59,26 @@ __device__ __forceinline__ void order() { asm volatile("" ::: "memory"); }
 __device__ __forceinline__ uint32_t f2u(float f) { return __float_as_uint(f); }
 // LDS DMA written as inline assembly: the compiler then does not order every later LDS
 // read behind it with a vmcnt(0) wait (this kernel counts its own waits). M0 holds the
-// wave's LDS destination; lane i writes at M0 + i * size. Writing M0 needs one wait state
-// before the DMA.
-__device__ __forceinline__ void dma16_sc1(const void* gp, const void* lds) {
-  const uint32_t m = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off sc1" ::"s"(m), "v"(gp) : "memory", "m0");
+// wave's LDS destination (lane i writes at M0 + i * size); writing M0 needs one wait state
+// before the DMA. Buffer form: address = descriptor base + soff (wave-uniform) + voff (the
+// lane's offset, the only part the descriptor's range check covers).
+__device__ __forceinline__ void bdma16_sc1(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
+               ::"s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
 }
-__device__ __forceinline__ void dma16(const void* gp, const void* lds) {
-  const uint32_t m = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m), "v"(gp) : "memory", "m0");
+__device__ __forceinline__ void bdma16(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               ::"s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
 }
-__device__ __forceinline__ void dma4(const void* gp, const void* lds) {
-  const uint32_t m = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off" ::"s"(m), "v"(gp) : "memory", "m0");
+__device__ __forceinline__ void dma4(const void* gp, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(gp) : "memory", "m0");
 }
-// An opaque copy of v: addresses derived from it are computed where they are used instead
-// of being hoisted out of the step loop for every unrolled pass (register pressure).
-__device__ __forceinline__ int opaque(int v) {
-  asm volatile("" : "+v"(v));
-  return v;
-}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+// Wave-uniform value kept in a scalar register.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t umax3(uint32_t a, uint32_t b, uint32_t c) { return max(max(a, b), c); }
 
-constexpr uint32_t kOOB = 0xffffffffu;   // buffer offset past every record: the store is dropped
+constexpr uint32_t kOOB = 0xffffffffu;   // buffer offset past every record: the access is dropped
 
 }  // namespace
 
@@ -94,16 +93,14 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
   constexpr int NXS = 3;                          // input-projection slots (tile q in slot q % 3)
   constexpr int CPW = 16 * SEG / 4;               // copy instructions per wave and tile
   constexpr int BG = 16 * NT;                     // rows per group
-  constexpr int PD = 2;                           // B fragments read ahead in the MFMA loop
+  constexpr int PD = 6;                           // B fragments read ahead in the MFMA loop
   // Every pass issues, in this order: the copy of tile q+2 (CPW loads), the next update's
-  // c source (2 loads, inside the cell update) and the input projection of tile q+2 (2
-  // loads); the first pass of a step also fetches producer indices before its copy. The copy
-  // of tile q is complete once no more than the loads after it (rest of pass q-2, pass q-1)
-  // are pending.
+  // c source (2 loads) and the input projection of tile q+2 (2 loads); the last pass of a
+  // step also fetches producer indices before its copy. The copy of tile q is complete once
+  // no more than the loads after it (rest of pass q-2, pass q-1) are pending.
   constexpr int kTail = 4, kPass = kTail + CPW;
   constexpr int kAfter = kTail + (DIST - 1) * kPass;
-  static_assert(SEG >= 1 && NT >= DIST + 4 && BG <= 256, "wide forward: 1 KB segments, 6+ tiles");
-  static_assert(16 * SEG <= 32 && CPW <= 32, "segment mask");
+  static_assert(SEG == 2 && NT >= DIST + 4 && BG <= 256, "wide forward: 2 KB rows, 6+ tiles");
   extern __shared__ __align__(16) unsigned char smem[];
   bf16_t* hs = reinterpret_cast<bf16_t*>(smem);
   // per tile and lane: c_prev of the tile's next update ([0] x, [1] y) and the c of the state
@@ -117,12 +114,12 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
   __shared__ int s_g, s_w, s_abort;
 
   claim_group_slot(a.ctl + CTL_XCC_SLOT, a.G, a.NW, &s_g, &s_w);
-  const int g = s_g, w = s_w;
+  const int g = uni(s_g), w = uni(s_w);
   if (g < 0) return;
 
   const int T = a.T, B = a.B, H = a.H, H4 = 4 * H;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = uni(tid >> 6);
   const int l16 = lane & 15, lq = lane >> 4;
   const int row0 = g * BG;
   const int ub = w * 32 + wave * 8;
@@ -161,8 +158,6 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
     }
   }
 
-  // rows of this lane: tile p covers rows row0 + 16p .. +15; lane row l16
-  auto lrow = [&](int p) { return opaque(row0 + 16 * p + l16); };
   auto slot = [](int s) { return (s + 3) % 3; };
 
   // producer indices of steps -1 (the initial state), 0 and 1; initial recurrence state
@@ -173,102 +168,110 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
     s_top[slot(1)][i] = T > 1 ? a.top[(size_t)B + b] : -1;
   }
   for (int p = 0; p < NT; ++p) {
-    const int b = min(lrow(p), B - 1);
+    const int b = min(row0 + 16 * p + l16, B - 1);
     const float2 c0v = *(const float2*)(a.c0 + (size_t)b * H + uc);
     stp(p, 0)[tid] = c0v.x; stp(p, 1)[tid] = c0v.y;
     stp(p, 2)[tid] = c0v.x; stp(p, 3)[tid] = c0v.y;   // top after step 0: produced there or initial
   }
   if (tid == 0) s_abort = 0;
 
-  // input projection of tile (t, p) into slot sl: this lane's 8 gate pre-activations
-  auto xw_fetch = [&](int t, int p, int sl) {
-    const int tt = min(t, T - 1), b = min(lrow(p), B - 1);
-    const float* src = a.xw + ((size_t)tt * B + b) * H4 + 4 * uc;
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // earlier reads of the slot have returned
-    dma16(src, xsp(sl, 0) + wave * 64);
-    dma16(src + 4, xsp(sl, 1) + wave * 64);
-  };
-#pragma unroll
-  for (int p = 0; p < DIST; ++p) xw_fetch(0, p, p % NXS);
-
-  // ---- copy of tile (tc, ptile) into buffer bi: segment i of this wave is row segment
-  // wave + 4i; the row's producer comes from the staged trace (src = top[tc-1], -1 at tc = 0;
-  // a copy for a step past the end reads the initial rows and is never used)
-  auto seg_src = [&](int tc, int ptile, int r) -> int {
-    return (tc == 0 || tc >= T) ? -1 : s_top[slot(tc - 1)][16 * ptile + r];
-  };
-  auto seg_copy = [&](int src, int ptile, int r, int sj, bf16_t* buf) {
-    int k = sj * 512 + lane * 8;
-    if (k >= H) k = 0;                            // finite filler; U registers are 0 there
-    const int b = min(opaque(row0 + 16 * ptile + r), B - 1);
-    const bf16_t* gp = a.hx + ((size_t)(src + 1) * B + b) * H + k;
-    dma16_sc1(gp, buf + r * LDS_LD + sj * 512);
-  };
+  // ---- descriptors and per-lane constant offsets
+  const rsrc_t r_hx = make_rsrc(a.hx, (size_t)(T + 1) * BH * 2);
+  // copy segment i of this wave: row (wave >> 1) + 2i, half wave & 1 of the 2 KB row; the
+  // lane's 16 bytes (a column past H reads column 0: finite filler, U registers are 0 there)
+  const int sj = wave & 1;
+  const uint32_t koff = (uint32_t)((sj * 512 + lane * 8 < H) ? (sj * 512 + lane * 8) * 2 : 0);
+  const int rbase = wave >> 1;
   auto copy_tile = [&](int tc, int ptile, int bi) {
-    bf16_t* buf = hs + bi * BUF;
+    // row r's producer (src = top[tc-1], -1 at tc = 0 and past the last step) in lane r
+    const int srcv = (tc == 0 || tc >= T) ? -1 : s_top[slot(tc - 1)][16 * ptile + l16];
+    const uint32_t lbuf = lds_addr(hs + bi * BUF + sj * 512);
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
-      const int sgi = wave + 4 * i;
-      const int r = sgi / SEG, sj = sgi % SEG;
-      seg_copy(seg_src(tc, ptile, r), ptile, r, sj, buf);
+      const int r = rbase + 2 * i;
+      const int src = __builtin_amdgcn_readlane(srcv, r);
+      const int b = min(row0 + 16 * ptile + r, B - 1);
+      const uint32_t soff = (uint32_t)(((src + 1) * B + b) * H) * 2u;
+      bdma16_sc1(r_hx, koff, soff, lbuf + (uint32_t)(r * LDS_LD * 2));
     }
   };
   // granules of tile (tc, ptile) in buffer bi that still hold the fill are copied again
-  // until every producer's store has arrived; false when the wait gave up
+  // until every producer's store has arrived; false when the wait gave up. A produced word
+  // (two bf16 written by one 4-byte store) is never all-ones, so a granule is pending when
+  // its largest word is.
+  auto granule = [&](int bi, int i) -> uint4 {
+    return *(const uint4*)(hs + bi * BUF + (rbase + 2 * i) * LDS_LD + sj * 512 + lane * 8);
+  };
+  auto gmax = [](uint4 v) -> uint32_t { return max(umax3(v.x, v.y, v.z), v.w); };
   auto complete_tile = [&](int tc, int ptile, int bi) -> bool {
-    bf16_t* buf = hs + bi * BUF;
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) m = max(m, gmax(granule(bi, i)));
+    if (!__builtin_amdgcn_ballot_w64(m == 0xffffffffu)) return true;   // the usual case
+    const int srcv = tc == 0 ? -1 : s_top[slot(tc - 1)][16 * ptile + l16];
+    const uint32_t lbuf = lds_addr(hs + bi * BUF + sj * 512);
     uint32_t bad = 0;
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const int sgi = wave + 4 * i;
-      const int r = sgi / SEG, sj = sgi % SEG;
-      const uint4 v = *(const uint4*)(buf + r * LDS_LD + sj * 512 + lane * 8);
-      if (pending_bf16x8(v) && seg_src(tc, ptile, r) >= 0) bad |= 1u << i;
-    }
+    for (int i = 0; i < CPW; ++i)
+      if (gmax(granule(bi, i)) == 0xffffffffu && __builtin_amdgcn_readlane(srcv, rbase + 2 * i) >= 0) bad |= 1u << i;
     int spins = 0;
     while (__builtin_amdgcn_ballot_w64(bad != 0u)) {
       if (spin_out(spins, a.ctl, a.spin_limit)) return false;
 #pragma unroll
       for (int i = 0; i < CPW; ++i) {
         if ((bad >> i) & 1u) {
-          const int sgi = wave + 4 * i;
-          const int r = sgi / SEG, sj = sgi % SEG;
-          seg_copy(seg_src(tc, ptile, r), ptile, r, sj, buf);
+          const int r = rbase + 2 * i;
+          const int src = __builtin_amdgcn_readlane(srcv, r);
+          const int b = min(row0 + 16 * ptile + r, B - 1);
+          bdma16_sc1(r_hx, koff, (uint32_t)(((src + 1) * B + b) * H) * 2u, lbuf + (uint32_t)(r * LDS_LD * 2));
         }
       }
       wait_vm0();
 #pragma unroll
-      for (int i = 0; i < CPW; ++i) {
-        if ((bad >> i) & 1u) {
-          const int sgi = wave + 4 * i;
-          const int r = sgi / SEG, sj = sgi % SEG;
-          if (!pending_bf16x8(*(const uint4*)(buf + r * LDS_LD + sj * 512 + lane * 8))) bad &= ~(1u << i);
-        }
-      }
+      for (int i = 0; i < CPW; ++i)
+        if (((bad >> i) & 1u) && gmax(granule(bi, i)) != 0xffffffffu) bad &= ~(1u << i);
     }
     return true;
   };
 
+  // input projection of tile (t, p) into slot sl: this lane's 8 gate pre-activations
+  auto xw_fetch = [&](int t, int p, int sl) {
+    const int tt = min(t, T - 1);
+    const rsrc_t rx = make_rsrc(a.xw + (size_t)tt * B * H4, (size_t)B * H4 * 4);
+    const int b = min(row0 + 16 * p + l16, B - 1);
+    const uint32_t vo = (uint32_t)(b * H4 + 4 * uc) * 4u;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // earlier reads of the slot have returned
+    bdma16(rx, vo, 0u, lds_addr(xsp(sl, 0) + wave * 64));
+    bdma16(rx, vo + 16u, 0u, lds_addr(xsp(sl, 1) + wave * 64));
+  };
   // the c of the state at the top after step ts+1 when that step does not produce it:
   // produced at a step <= ts by this lane (already stored) or the initial state
   auto c_fetch = [&](int ts, int pe, int topn) {
-    const int bc = min(lrow(pe), B - 1);
+    const int bc = min(row0 + 16 * pe + l16, B - 1);
     const int sn = (topn < -1 || topn > ts) ? -1 : topn;
-    const size_t off = (size_t)bc * H + uc;
-    const float* cs = sn < 0 ? a.c0 + off : a.ccell + (size_t)sn * BH + off;
+    const float* cs = (sn < 0 ? a.c0 : a.ccell) + (uint32_t)((max(sn, 0) * B + bc) * H + uc);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // earlier reads of the slot have returned
-    dma4(cs, stp(pe, 2) + wave * 64);
-    dma4(cs + 1, stp(pe, 3) + wave * 64);
+    dma4(cs, lds_addr(stp(pe, 2) + wave * 64));
+    dma4(cs + 1, lds_addr(stp(pe, 3) + wave * 64));
   };
 
   // ---- cell update of tile (te, pe) from its gates; stores through bounds-checked
-  // descriptors (a lane outside the batch or the units stores nothing)
-  auto epilogue = [&](int te, int pe, const f32x4 (&acc)[2], int sl) {
-    const int b = lrow(pe);
-    const bool ok = uok && b < B;
+  // descriptors (a lane outside the batch or the units stores nothing). Returns top[te+1]
+  // of the lane's row for the fetch of the next update's state.
+  const rsrc_t r_h = make_rsrc(a.hcell, (size_t)T * BH * 4);
+  const rsrc_t r_c = make_rsrc(a.ccell, (size_t)T * BH * 4);
+  const rsrc_t r_ht = make_rsrc(a.htop, a.htop ? (size_t)T * BH * 4 : 0);
+  const rsrc_t r_ct = make_rsrc(a.ctop, a.ctop ? (size_t)T * BH * 4 : 0);
+  auto epilogue = [&](int te, int pe, const f32x4 (&acc)[2], int sl, bool live) -> int {
+    const int b = row0 + 16 * pe + l16;
+    const bool ok = live && uok && b < B;
     const int topv = s_top[slot(te)][16 * pe + l16];
     const int topn = s_top[slot(te + 1)][16 * pe + l16];
-    const float cp[2] = {stp(pe, 0)[tid], stp(pe, 1)[tid]};
+    float cp[2] = {stp(pe, 0)[tid], stp(pe, 1)[tid]};
+    float pc[2] = {stp(pe, 2)[tid], stp(pe, 3)[tid]};
+    // materialised here: a load feeding only a select would become a branch around the load,
+    // which would cut the MFMA loop's scheduling region
+    asm volatile("" : "+v"(pc[0]), "+v"(pc[1]));
     const float4 xw[2] = {xsp(sl, 0)[tid], xsp(sl, 1)[tid]};
     float hv[2], cv[2], act[2][4];
 #pragma unroll
@@ -280,105 +283,106 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
       cv[j] = act[j][1] * cp[j] + act[j][0] * act[j][2];
       hv[j] = canon_nan(act[j][3] * tanhf_(cv[j]));
     }
-    const uint32_t e0 = (uint32_t)b * (uint32_t)H + (uint32_t)u0;   // element of (b, u0)
+    const uint32_t e0 = (uint32_t)b * (uint32_t)H + (uint32_t)u0;   // element of (b, u0) within a step
     const uint32_t o4 = ok ? e0 * 4u : kOOB;
-    const uint32_t o2 = ok ? e0 * 2u : kOOB;
-    const uint32_t o16 = ok ? e0 * 16u : kOOB;
-    const rsrc_t rh = make_rsrc(a.hcell + (size_t)te * BH, BH * 4);
-    const rsrc_t rc = make_rsrc(a.ccell + (size_t)te * BH, BH * 4);
+    const uint32_t so4 = (uint32_t)te * (uint32_t)BH * 4u;         // step offsets (< 4 GB)
     const rsrc_t rx = make_rsrc(a.hx + (size_t)(te + 1) * BH, BH * 2);
     const rsrc_t rs = make_rsrc(a.stash + (size_t)te * BH * 4, BH * 16);
-    __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(hv[0]), f2u(hv[1])}, rh, o4, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(cv[0]), f2u(cv[1])}, rc, o4, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(hv[0]), f2u(hv[1])}, r_h, o4, so4, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(cv[0]), f2u(cv[1])}, r_c, o4, so4, 0);
     __builtin_amdgcn_raw_buffer_store_b32((uint32_t)f32_to_bf16_bits(hv[0]) | ((uint32_t)f32_to_bf16_bits(hv[1]) << 16),
-                                          rx, o2, 0, 0);
+                                          rx, ok ? e0 * 2u : kOOB, 0, 0);
     __builtin_amdgcn_raw_buffer_store_b128(v4u{f2u(act[0][0]), f2u(act[0][1]), f2u(act[0][2]), f2u(act[0][3])}, rs,
-                                           o16, 0, 0);
+                                           ok ? e0 * 16u : kOOB, 0, 0);
     __builtin_amdgcn_raw_buffer_store_b128(v4u{f2u(act[1][0]), f2u(act[1][1]), f2u(act[1][2]), f2u(act[1][3])}, rs,
-                                           ok ? o16 + 16u : kOOB, 0, 0);
+                                           ok ? e0 * 16u + 16u : kOOB, 0, 0);
     // Algorithm 1's return value: the state at the pointer after step te. c_top here; h_top
     // of a push here, of the other steps by a gather after the kernel
     const bool push = topv == te;
-    const float ct0 = push ? cv[0] : stp(pe, 2)[tid], ct1 = push ? cv[1] : stp(pe, 3)[tid];
-    if (a.htop) {
-      const rsrc_t rht = make_rsrc(a.htop + (size_t)te * BH, BH * 4);
-      __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(hv[0]), f2u(hv[1])}, rht, push ? o4 : kOOB, 0, 0);
-    }
-    if (a.ctop) {
-      const rsrc_t rct = make_rsrc(a.ctop + (size_t)te * BH, BH * 4);
-      __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(ct0), f2u(ct1)}, rct, o4, 0, 0);
-    }
-    stp(pe, 0)[tid] = ct0;                          // step te+1 reads the state at the top
-    stp(pe, 1)[tid] = ct1;
-    c_fetch(te, pe, topn);
+    const float ct0 = push ? cv[0] : pc[0], ct1 = push ? cv[1] : pc[1];
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(hv[0]), f2u(hv[1])}, r_ht, push ? o4 : kOOB, so4, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(ct0), f2u(ct1)}, r_ct, o4, so4, 0);
+    stp(pe, 0)[tid] = live ? ct0 : cp[0];           // step te+1 reads the state at the top
+    stp(pe, 1)[tid] = live ? ct1 : cp[1];
+    return topn;
   };
 
-  // prologue: copies of tiles 0 .. DIST-1 of step 0 (initial state rows)
+  // prologue: copies and input projections of tiles 0 .. DIST-1 of step 0
 #pragma unroll
-  for (int p = 0; p < DIST; ++p) copy_tile(0, p, p);
+  for (int p = 0; p < DIST; ++p) {
+    copy_tile(0, p, p);
+    xw_fetch(0, p, p % NXS);
+  }
 
   f32x4 acc_pend[2];
   acc_pend[0] = acc_pend[1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bool stop = false;
   long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
-  for (int t = 0; t < T && !stop; ++t) {
-#pragma unroll
-    for (int p = 0; p < NT; ++p) {
-      const int q = t * NT + p;
-      // ---- tile (t, p) in LDS: loads issued after its copy bound what may still be pending
-      if (t == 0 && p < DIST) wait_vm0();
-      else wait_vm<kAfter>();
-      if (!complete_tile(t, p, q % NBUF)) s_abort = 1;
-      lds_barrier();
-      if (s_abort) {
-        stop = true;
-        break;
-      }
-      if (clk && tid == 0 && p < 2) clk[t * 4 + 2 * p] = wall_clock64();
-      // producer indices of step t+2 into slot t-1, whose last readers (the copies of this
-      // step's tiles and the check above) are done once the last pass of the step starts
-      if (p == NT - 1 && tid < BG) {
-        const int b = min(row0 + tid, B - 1);
-        dma4(a.top + (size_t)min(t + 2, T - 1) * B + b, &s_top[slot(t + 2)][wave * 64]);
-      }
-      // ---- copy of tile q + DIST into the buffer that tile q-1 used
-      {
-        const int pn = p + DIST;
-        copy_tile(pn < NT ? t : t + 1, pn % NT, (q + DIST) % NBUF);
-      }
-      // ---- gates^T = U^T h_prev^T for tile (t, p): two A tiles share each B fragment
-      const bf16_t* buf = hs + (q % NBUF) * BUF;
-      f32x4 acc[2];
-      acc[0] = acc[1] = f32x4{0.f, 0.f, 0.f, 0.f};
-      bf16x8 fr[PD + 1];
-#pragma unroll
-      for (int c = 0; c < PD; ++c) fr[c] = *(const bf16x8*)&buf[l16 * LDS_LD + c * KC + 8 * lq];
-#pragma unroll
-      for (int c = 0; c < KS; ++c) {
-        if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&buf[l16 * LDS_LD + (c + PD) * KC + 8 * lq];
-        const bf16x8 bv = fr[c % (PD + 1)];
-        acc[0] = mfma_bf16_16x16x32(ureg[0][c], bv, acc[0]);
-        acc[1] = mfma_bf16_16x16x32(ureg[1][c], bv, acc[1]);
-        if (c == 2) {
-          // cell update of the previous tile, under this tile's matrix work
-          if (p > 0) epilogue(t, p - 1, acc_pend, (q - 1) % NXS);
-          else if (t > 0) epilogue(t - 1, NT - 1, acc_pend, (q - 1) % NXS);
-          else c_fetch(0, NT - 1, -1);            // same loads as every pass (values unused)
-        }
-      }
-      acc_pend[0] = acc[0];
-      acc_pend[1] = acc[1];
-      if (clk && tid == 0 && p < 2) clk[t * 4 + 2 * p + 1] = wall_clock64();
-      // ---- input projection of tile q + DIST (its slot held tile q-1, read by the update above)
-      {
-        const int pn = p + DIST;
-        xw_fetch(pn < NT ? t : t + 1, pn % NT, (q + DIST) % NXS);
-      }
+  // One pass per tile, not unrolled: every per-tile value lives in LDS, so the pass body is
+  // the same code for every tile.
+  const int nq = T * NT;
+  int q = 0;
+#pragma unroll 1
+  for (; q < nq; ++q) {
+    const int t = q / NT, p = q - t * NT;
+    // ---- tile (t, p) in LDS: loads issued after its copy bound what may still be pending
+    if (q < DIST) wait_vm0();
+    else wait_vm<kAfter>();
+    if (!complete_tile(t, p, q % NBUF)) s_abort = 1;
+    lds_barrier();
+    if (s_abort) break;
+    if (clk && tid == 0 && p == 1) clk[t * 4 + 0] = wall_clock64();
+    // producer indices of step t+2 into slot t-1, whose last readers (the copies of this
+    // step's tiles and the check above) are done once the last pass of the step starts
+    if (p == NT - 1 && tid < BG) {
+      const int b = min(row0 + tid, B - 1);
+      dma4(a.top + (size_t)min(t + 2, T - 1) * B + b, lds_addr(&s_top[slot(t + 2)][wave * 64]));
     }
+    // ---- copy of tile q + DIST into the buffer that tile q-1 used
+    {
+      const int qn = q + DIST, tn = qn / NT;
+      copy_tile(tn, qn - tn * NT, qn % NBUF);
+    }
+    if (clk && tid == 0 && p == 1) clk[t * 4 + 1] = wall_clock64();
+    // ---- gates^T = U^T h_prev^T for tile (t, p), two A tiles per B fragment, interleaved
+    // with the cell update of the previous tile (its gates are in acc_pend)
+    const bf16_t* buf = hs + (q % NBUF) * BUF;
+    f32x4 acc[2];
+    acc[0] = acc[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bf16x8 fr[PD + 1];
+#pragma unroll
+    for (int c = 0; c < PD; ++c) fr[c] = *(const bf16x8*)&buf[l16 * LDS_LD + c * KC + 8 * lq];
+    // (the first pass runs it on the initial values with every store dropped: no branch, so
+    // the scheduler can interleave it with the MFMAs)
+    const bool live = q > 0;
+    const int qe = live ? q - 1 : NT - 1, te = qe / NT, pe = qe - te * NT;
+    const int topn = epilogue(te, pe, acc_pend, qe % NXS, live);
+    // the scheduler keeps PD fragment reads in flight: PD reads, then one read per MFMA pair
+    __builtin_amdgcn_sched_group_barrier(0x100, PD, 0);
+#pragma unroll
+    for (int c = 0; c < KS; ++c) {
+      if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&buf[l16 * LDS_LD + (c + PD) * KC + 8 * lq];
+      const bf16x8 bv = fr[c % (PD + 1)];
+      acc[0] = mfma_bf16_16x16x32(ureg[0][c], bv, acc[0]);
+      acc[1] = mfma_bf16_16x16x32(ureg[1][c], bv, acc[1]);
+      if (c + PD < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // cell-update ALU work between MFMAs
+    }
+    acc_pend[0] = acc[0];
+    acc_pend[1] = acc[1];
+    if (clk && tid == 0 && p == 1) clk[t * 4 + 2] = wall_clock64();
+    // ---- the next update's c source for the tile just updated, then the input projection
+    // of tile q + DIST (its slot held tile q-1, read by the update above)
+    c_fetch(te, pe, live ? topn : -1);            // the first pass fetches the initial c (unused)
+    {
+      const int qn = q + DIST, tn = qn / NT;
+      xw_fetch(tn, qn - tn * NT, qn % NXS);
+    }
+    if (clk && tid == 0 && p == 1) clk[t * 4 + 3] = wall_clock64();
   }
-  if (!stop && T > 0) {
+  if (q == nq && nq > 0) {
     wait_vm0();
-    epilogue(T - 1, NT - 1, acc_pend, (T * NT - 1) % NXS);
+    epilogue(T - 1, NT - 1, acc_pend, (nq - 1) % NXS, true);
   }
   // loads started for passes past the last step are never read; let them land
   wait_vm0();
