@@ -13,7 +13,7 @@
 #include "recurrent.h"
 
 __global__ void k_init_ctl(uint32_t* ctl);
-__global__ void k_scan(const int8_t* ops, int T, int B, int32_t* ptr, uint32_t* ctl);
+__global__ void k_scan(const int8_t* ops, int T, int B, int32_t* ptr, int32_t* depth_end, uint32_t* ctl);
 __global__ void k_gather_top(const int32_t* top, const float* cellv, const float* init, float* out, int T, int B,
                              int H, int skip_push);
 __global__ void k_trace(const int8_t* ops, int T, int B, int cap, int32_t* top);
@@ -69,7 +69,7 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, prow, total;
+  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, prow, dep, total;
 };
 
 // Push-row count padded to the K tile: leading dimension of the transposed bf16 operands
@@ -191,6 +191,7 @@ Layout layout(const slstm_dims* d) {
   L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
   L.part = o; o += align256((size_t)64 * std::max(I, H) * 4 * H * 4);
   L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
+  L.dep = o; o += align256(B * 4);                                     // pointer after the last step
   L.total = o;
   return L;
 }
@@ -316,7 +317,7 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   // a1: validate ops and scan the pointer (the call's one host synchronisation)
   mark(d, 0, st);
   hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl);
-  hipLaunchKernelGGL(k_scan, dim3((B + 15) / 16), dim3(256), 0, st, ops, T, B, ptr, ctl);
+  hipLaunchKernelGGL(k_scan, dim3((B + 15) / 16), dim3(256), 0, st, ops, T, B, ptr, (int32_t*)(ws + L.dep), ctl);
   uint32_t hs[2] = {0, 0};
   if (hipMemcpyAsync(hs, ctl + CTL_STATUS, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
   if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
@@ -430,6 +431,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   a.dA = ws + L.r1;
   a.dh_acc = (float*)(ws + L.dh); a.dc_acc = (float*)(ws + L.dc);
   a.db_part = (float*)(ws + L.dbp);
+  a.depth_end = (const int32_t*)(ws + L.dep);
   a.dh0 = dh0; a.dc0 = dc0;
   if (a.clk) a.clk += (size_t)512 * T * 4;
   // rows of the push steps, for the post-loop gradients (dA is exactly zero on other rows)

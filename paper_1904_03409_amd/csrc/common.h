@@ -183,3 +183,18 @@ __device__ __forceinline__ void claim_group_slot(uint32_t* slot_ctrs, int G, int
   }
   __syncthreads();
 }
+
+// LDS DMA (global memory -> LDS, 16 bytes or 4 bytes per lane) written as inline assembly:
+// the compiler then does not order every later LDS read behind it with a vmcnt(0) wait; a
+// kernel that uses these counts its own waits. M0 holds the wave's LDS destination (lane i
+// writes at M0 + i * size); writing M0 needs one wait state before the DMA. The buffer
+// forms address descriptor base + soff (wave-uniform) + voff (the lane's offset, the only
+// part the descriptor's range check covers).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+__device__ __forceinline__ void dma16_global(const void* gp, uint32_t lds, bool sc1) {
+  lds = __builtin_amdgcn_readfirstlane(lds);   // wave-uniform by contract; keeps it in an SGPR
+  if (sc1)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off sc1" ::"s"(lds), "v"(gp) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(gp) : "memory", "m0");
+}

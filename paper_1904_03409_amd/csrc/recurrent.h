@@ -30,9 +30,10 @@ struct RecArgs {
   const float* dh_top;   // [T][B][H]
   const float* dc_top;   // [T][B][H] or null
   void* dA;              // [T][B][4H] fp32 or bf16: gradient w.r.t. the gate pre-activations
-  float* dh_acc;         // [T+1][B][H] gradient w.r.t. each produced state (slot 0 = initial)
+  float* dh_acc;         // [T+1][B][H] spilled gradient of the state at each stack depth (backward)
   float* dc_acc;         // [T+1][B][H]
   float* db_part;        // [G][4H] per-group bias gradient (gate-interleaved)
+  const int32_t* depth_end;   // [B] stack pointer after the last step (written by k_scan)
   float* dh0;            // [B][H]
   float* dc0;            // [B][H]
   long long* clk;        // optional per-step wall-clock stamps [grid][T][4] (profiling)

@@ -2,23 +2,39 @@
 // time over the stack (paper, section 5: the gradient keeps reaching states that were
 // popped and later overwritten, because every produced state is kept once).
 //
-// The state read at step t is the one produced at step src[t] (src[t] = top[t-1]), and
-// the state returned at step t is the one produced at step top[t]. Reverse sweep, with
-// dh_acc/dc_acc[s+1] the gradient w.r.t. the state produced at step s (slot 0 = h0/c0):
-//   non-push t:  dh_acc[top+1] += dh_top[t], dc_acc[top+1] += dc_top[t]; dA[t] = 0
-//   push t:      dh = dh_acc[t+1] + dh_top[t], dc = dc_acc[t+1] + dc_top[t] + dh o (1 - tanh^2 c)
-//                dA = (dc g i(1-i), dc c_prev f(1-f), dc i (1-g^2), dh tanh(c) o(1-o))
-//                dc_acc[src+1] += dc f;   dh_acc[src+1] += dA U^T
+// The reverse sweep walks the stack backwards. Per (row, unit) pair the gradient of the
+// state at the top (after step t) is kept in registers, (Gh, Gc); step t's upstream
+// gradient dh_top[t], dc_top[t] is added to it. Then, by the op of step t:
+//   hold: nothing more (the same state was on top before the step);
+//   pop:  the state below came back to the top in forward order, so in reverse the popped
+//         state comes back: (Gh, Gc) is stored at the depth of the top, S[p], and the popped
+//         state's gradient starts at 0;
+//   push: (Gh, Gc) is the produced state's whole gradient. The cell backward gives
+//         dA = (dc g i(1-i), dc c_prev f(1-f), dc i (1-g^2), dh tanh(c) o(1-o)) and the
+//         parent (depth p-1) becomes the top: (Gh, Gc) = S[p-1] + (dA U^T, dc f).
+// S[d] of a state that stays on the stack to the end is 0 (zeroed before the sweep); every
+// other S[d] read was stored by the pop of the state above it, at a later step. The most
+// recent store is forwarded in registers, older ones are prefetched a step ahead; no
+// accumulator is read and written in the same step.
+//
 // Same work split as the forward: group of 16*NT rows on one XCC, workgroup w owns
 // hidden units [16w, 16w+16). dA U^T needs all 4H gate columns, so dA is exchanged
-// through L2 without a group barrier: dA starts filled with all-one bits, and a reader
-// fetches again every granule that still holds them. Wave q contracts gate columns
-// [qH, (q+1)H) against its register-resident slice of U and the four partial sums are
-// added in LDS in a fixed order. Every dh_acc/dc_acc element is owned by one thread, so
-// there are no atomics.
+// through L2: with a group barrier per step, or without one (dA starts filled with all-one
+// bits, and a reader fetches again every granule that still holds them). Wave q contracts
+// gate columns [qH, (q+1)H) against its register-resident slice of U and the four partial
+// sums are added in LDS in a fixed order. Every gradient element is owned by one thread,
+// so there are no atomics. Workgroup barriers that only order LDS accesses do not wait for
+// outstanding global loads.
 #include "common.h"
 #include "recurrent.h"
 #include "rec_config.h"
+
+#pragma clang diagnostic ignored "-Winline-asm"   // M0 is written by the LDS DMA blocks
+
+namespace {
+// Workgroup barrier for LDS data only: it does not wait for global loads or stores.
+__device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+}  // namespace
 
 template <int PREC, int NT, int KS, int OCC>
 __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
@@ -29,7 +45,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ float red[4][BG][17];
-  __shared__ int s_op[BG], s_top[BG], s_src[BG], s_crow[BG], s_cidx[BG], s_nlive;
+  __shared__ int s_op[BG], s_crow[BG], s_cidx[BG], s_nlive;
   __shared__ float s_db[16][16][4];
   __shared__ int s_g, s_w;
   __shared__ int s_abort;                          // a wait for dA rows gave up
@@ -42,7 +58,6 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l16 = lane & 15, lq = lane >> 4;
   const int row0 = g * BG;
-  const int ks_eff = a.ks_eff;
   constexpr int ESZ = PREC ? 2 : 4;
   const rsrc_t r_dA = make_rsrc(a.dA, (size_t)T * B * H4 * ESZ);
 
@@ -80,29 +95,22 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     prow[i] = (threadIdx.x >> 4) + 16 * i;
     pok[i] = (row0 + prow[i] < B) && (u < H);
   }
-  // zero this workgroup's accumulator slots ([T+1] slots x group rows x its 16 units) with
-  // 16-byte stores; slot 0 is the initial state
-  {
-    const int n4 = (T + 1) * BG * 4;
-    for (int i = threadIdx.x; i < n4; i += 256) {
-      const int slot = i / (BG * 4), rem = i - slot * (BG * 4);
-      const int r = rem >> 2, q = rem & 3;
-      const int b = row0 + r, u0 = w * 16 + 4 * q;
-      if (b >= B) continue;
-      const size_t o = ((size_t)slot * B + b) * H + u0;
-      if (u0 + 3 < H && (H & 3) == 0) {
-        *(float4*)(a.dh_acc + o) = float4{0.f, 0.f, 0.f, 0.f};
-        *(float4*)(a.dc_acc + o) = float4{0.f, 0.f, 0.f, 0.f};
-      } else {
-        for (int j = 0; j < 4; ++j)
-          if (u0 + j < H) { a.dh_acc[o + j] = 0.f; a.dc_acc[o + j] = 0.f; }
-      }
+  // depth after the last step, per pair; the spill slots S[0 .. depth) of the states that
+  // stay on the stack to the end start at 0
+  int dep[PAIRS];
+#pragma unroll
+  for (int i = 0; i < PAIRS; ++i) {
+    const int b = pok[i] ? row0 + prow[i] : 0;
+    dep[i] = pok[i] ? min(max(a.depth_end[b], 0), T) : 0;
+    for (int d = 0; d < dep[i]; ++d) {
+      const size_t o = ((size_t)d * B + b) * H + u;
+      a.dh_acc[o] = 0.f;
+      a.dc_acc[o] = 0.f;
     }
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
   const bool direct = a.bwd_direct != 0;
-  typedef __attribute__((address_space(3))) void* lds_ptr_t;
   using elem_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
   elem_t* wbuf = reinterpret_cast<elem_t*>(dsm) + (size_t)wave * 16 * QLD;
   if (direct)
@@ -111,49 +119,69 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // Loads are issued a step (or at least a phase) before their values are used. Per pair:
-  //   cur_*  operands of the current step t, fetched during step t+1;
-  //   slot_* gradient of the state produced at step t (dh_acc/dc_acc slot t+1), fetched at the
-  //          start of step t+1 and updated in registers by step t+1's contributions to it;
-  //   tg_*   the slot this step adds into (src+1 for a push, top+1 otherwise), fetched at the
-  //          start of step t and written back with the contribution.
-  auto valid = [&](int t, int op, int& tp, int& sp) {
-    // guard against a producer table that is not the forward's: no access outside [-1, t]
-    if (tp < -1 || tp > t || (op == 1 && tp != t)) tp = -1;
+  // Loads are issued a step before their values are used. Per pair:
+  //   c_*  row info and operands of the current step t;
+  //   n_*  row info of step t-1 (fetched during step t+1) and its operands (during step t);
+  //   nn_* row info of step t-2 (fetched during step t).
+  // The operands are fetched after the step's last wait for dA rows, so no wait of the
+  // step includes them.
+  auto valid_sp = [&](int t, int& sp) {
+    // guard against a producer table that is not the forward's: no access outside [-1, t)
     if (sp < -1 || sp >= t) sp = -1;
   };
-  int c_op[PAIRS], c_tp[PAIRS], c_sp[PAIRS];            // step t row info
-  int n_op[PAIRS], n_sp[PAIRS];                          // step t-1 (top[t-1] = c_sp)
+  int c_op[PAIRS], c_sp[PAIRS];                          // step t row info
+  int n_op[PAIRS], n_sp[PAIRS], nn_op[PAIRS], nn_sp[PAIRS];
   float c_gh[PAIRS], c_gc[PAIRS], c_c[PAIRS], c_cp[PAIRS];
   float4 c_act[PAIRS];
   float n_gh[PAIRS], n_gc[PAIRS], n_c[PAIRS], n_cp[PAIRS];
   float4 n_act[PAIRS];
-  float slot_dh[PAIRS], slot_dc[PAIRS], nx_dh[PAIRS], nx_dc[PAIRS], tg_dh[PAIRS], tg_dc[PAIRS];
+  // gradient of the top state; last spill (value and depth); spill slot prefetched for a push
+  float gh[PAIRS], gc[PAIRS], lh[PAIRS], lc[PAIRS], ph[PAIRS], pc[PAIRS];
+  int ld[PAIRS];
   auto ld_row = [&](int t, int b, int& op, int& sp) {
     op = a.ops[(size_t)t * B + b];
     sp = (t == 0) ? -1 : a.top[(size_t)(t - 1) * B + b];
   };
-  auto ld_ops = [&](int t, int b, float& gh, float& gc, float4& act, float& c) {
+  // the cell operands (gates, c, c_prev) are read for push steps only
+  auto ld_ops = [&](int t, int b, int op, int sp, float& gh_, float& gc_, float4& act, float& c, float& cp) {
     const size_t o = ((size_t)t * B + b) * H + ul;
-    gh = a.dh_top[o];
-    gc = a.dc_top ? a.dc_top[o] : 0.f;
-    act = *(const float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * ul);
-    c = a.ccell[o];
+    gh_ = a.dh_top[o];
+    gc_ = a.dc_top ? a.dc_top[o] : 0.f;
+    if (op == 1) {
+      act = *(const float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * ul);
+      c = a.ccell[o];
+      cp = (sp < 0) ? a.c0[(size_t)b * H + ul] : a.ccell[((size_t)sp * B + b) * H + ul];
+    }
   };
-  auto ld_cp = [&](int sp, int b) -> float {
-    return (sp < 0) ? a.c0[(size_t)b * H + ul] : a.ccell[((size_t)sp * B + b) * H + ul];
+  // operands of step t-1 and row info of step t-2; the spill slot a push at step t-1 reads
+  // (depth dep-1 after this step's update)
+  auto prefetch = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < PAIRS; ++i) {
+      const int b = pok[i] ? row0 + prow[i] : 0;
+      if (t > 0) {
+        ld_ops(t - 1, b, n_op[i], n_sp[i], n_gh[i], n_gc[i], n_act[i], n_c[i], n_cp[i]);
+        const size_t so = ((size_t)max(dep[i] - 1, 0) * B + b) * H + ul;
+        ph[i] = a.dh_acc[so];
+        pc[i] = a.dc_acc[so];
+      }
+      if (t > 1) ld_row(t - 2, b, nn_op[i], nn_sp[i]);   // validated at the rotation
+    }
   };
 #pragma unroll
   for (int i = 0; i < PAIRS; ++i) {
     const int b = pok[i] ? row0 + prow[i] : 0;
-    int op, sp;
-    ld_row(T - 1, b, op, sp);
-    int tp = a.top[(size_t)(T - 1) * B + b];
-    valid(T - 1, op, tp, sp);
-    c_op[i] = op; c_tp[i] = tp; c_sp[i] = sp;
-    ld_ops(T - 1, b, c_gh[i], c_gc[i], c_act[i], c_c[i]);
-    c_cp[i] = ld_cp(sp, b);
-    slot_dh[i] = 0.f; slot_dc[i] = 0.f;                // slot T was zeroed and nothing adds to it later
+    ld_row(T - 1, b, c_op[i], c_sp[i]);
+    valid_sp(T - 1, c_sp[i]);
+    ld_ops(T - 1, b, c_op[i], c_sp[i], c_gh[i], c_gc[i], c_act[i], c_c[i], c_cp[i]);
+    if (T > 1) {
+      ld_row(T - 2, b, n_op[i], n_sp[i]);
+      valid_sp(T - 2, n_sp[i]);
+    }
+    gh[i] = gc[i] = lh[i] = lc[i] = 0.f;
+    ld[i] = -1;
+    // spill slot for a push at step T-1 (the parent sits at depth dep-1): stays-on-stack, 0
+    ph[i] = pc[i] = 0.f;
   }
 
   long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
@@ -164,39 +192,9 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
 #pragma unroll
       for (int i = 0; i < PAIRS; ++i) {
         s_op[prow[i]] = pok[i] ? c_op[i] : 0;
-        s_src[prow[i]] = c_sp[i];
-        s_top[prow[i]] = c_tp[i];
       }
     }
-    // loads, in the order they are needed (vector loads complete in issue order, so the
-    // epilogue's wait for the target slot does not include the HBM prefetch behind it):
-    // this step's target slot, slot t, then row info and operands of step t-1
-#pragma unroll
-    for (int i = 0; i < PAIRS; ++i) {
-      const int b = pok[i] ? row0 + prow[i] : 0;
-      const int tgt = (c_op[i] == 1) ? c_sp[i] : c_tp[i];
-      const size_t to = ((size_t)(tgt + 1) * B + b) * H + ul;
-      tg_dh[i] = a.dh_acc[to];
-      tg_dc[i] = a.dc_acc[to];
-    }
-#pragma unroll
-    for (int i = 0; i < PAIRS; ++i) {
-      const int b = pok[i] ? row0 + prow[i] : 0;
-      if (t > 0) {
-        const size_t no = ((size_t)t * B + b) * H + ul;
-        nx_dh[i] = a.dh_acc[no];
-        nx_dc[i] = a.dc_acc[no];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < PAIRS; ++i) {
-      const int b = pok[i] ? row0 + prow[i] : 0;
-      if (t > 0) {
-        ld_row(t - 1, b, n_op[i], n_sp[i]);
-        ld_ops(t - 1, b, n_gh[i], n_gc[i], n_act[i], n_c[i]);
-      }
-    }
-    __syncthreads();
+    lds_sync();
     if (wave == 0) {
       // list the push rows in row order (wave-wide ballot + prefix count)
       int base = 0;
@@ -217,37 +215,41 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     for (int i = 0; i < PAIRS; ++i) {
       float4 dA4 = float4{0.f, 0.f, 0.f, 0.f};
       const int b = row0 + prow[i];
-      const int tgt = (c_op[i] == 1) ? c_sp[i] : c_tp[i];
-      const bool fwd_slot = (t > 0) && (tgt + 1 == t);   // contribution lands in next step's slot
-      float add_dh = 0.f, add_dc = 0.f;
+      // dh_top[t], dc_top[t] belong to the state at the top after step t
+      gh[i] += c_gh[i];
+      gc[i] += c_gc[i];
       if (c_op[i] == 1) {
+        // the state produced at step t: its whole gradient is (gh, gc)
         const float4 act = c_act[i];
-        const float dh = slot_dh[i] + c_gh[i];
-        const float dcin = slot_dc[i] + c_gc[i];
+        const float dh = gh[i];
         const float tc = tanhf_(c_c[i]);
-        const float dc = dcin + dh * act.w * (1.f - tc * tc);
+        const float dc = gc[i] + dh * act.w * (1.f - tc * tc);
         // never the all-ones fill pattern: a NaN is stored as the canonical quiet NaN
         dA4.x = canon_nan(dc * act.z * act.x * (1.f - act.x));
         dA4.y = canon_nan(dc * c_cp[i] * act.y * (1.f - act.y));
         dA4.z = canon_nan(dc * act.x * (1.f - act.z * act.z));
         dA4.w = canon_nan(dh * tc * act.w * (1.f - act.w));
-        add_dc = dc * act.y;
         if (pok[i]) { dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w; }
-      } else {
-        add_dh = c_gh[i];
-        add_dc = c_gc[i];
+        // the parent (depth dep-1) comes back to the top with its spilled gradient (the last
+        // spill if it was to that depth, else the prefetched slot) plus dc f; dA U^T follows
+        const bool fwd = ld[i] == dep[i] - 1;
+        gh[i] = fwd ? lh[i] : ph[i];
+        gc[i] = (fwd ? lc[i] : pc[i]) + dc * act.y;
+        dep[i] -= 1;
+      } else if (c_op[i] == -1) {
+        // the popped state comes back: the state below is spilled, the popped one starts at 0
+        if (pok[i]) {
+          const size_t o = ((size_t)dep[i] * B + b) * H + u;
+          a.dh_acc[o] = gh[i];
+          a.dc_acc[o] = gc[i];
+        }
+        lh[i] = gh[i];
+        lc[i] = gc[i];
+        ld[i] = dep[i];
+        gh[i] = gc[i] = 0.f;
+        dep[i] += 1;
       }
-      if (fwd_slot) {
-        nx_dh[i] += add_dh;
-        nx_dc[i] += add_dc;
-      } else if (pok[i]) {
-        const size_t to = ((size_t)(tgt + 1) * B + b) * H + u;
-        tg_dh[i] += add_dh;
-        tg_dc[i] += add_dc;
-        if (c_op[i] != 1) a.dh_acc[to] = tg_dh[i];   // a push's dh contribution comes after the GEMM
-        a.dc_acc[to] = tg_dc[i];
-      }
-      if (pok[i]) {
+      if (pok[i] && c_op[i] == 1) {               // only push rows are read (exchange, post-loop GEMMs)
         const size_t ao = ((size_t)t * B + b) * H4 + 4 * u;
         if constexpr (PREC == 0) {
           *(float4*)((float*)a.dA + ao) = dA4;
@@ -261,22 +263,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
 
     if (clk && threadIdx.x == 0) clk[t * 4 + 1] = wall_clock64();
     if (a.poll) {
-      __syncthreads();
+      lds_sync();
     } else if (group_barrier(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_abort)) {
       break;
     }
     if (clk && threadIdx.x == 0) clk[t * 4 + 2] = wall_clock64();
-    // c_prev of step t-1 (its producer index arrived with the prefetch above)
-    if (t > 0) {
-#pragma unroll
-      for (int i = 0; i < PAIRS; ++i) {
-        int op = n_op[i], tp = c_sp[i], sp = n_sp[i];
-        valid(t - 1, op, tp, sp);
-        n_sp[i] = sp;
-        n_cp[i] = ld_cp(sp, pok[i] ? row0 + prow[i] : 0);
-      }
-    }
-
     // Only push rows have non-zero dA. They are listed (in row order) in s_crow and run as
     // compacted 16-row MFMA tiles; each tile's K loop fetches its fragments one group of CG
     // chunks ahead, through the bounds-checked descriptor (a lane past the list or k past H
@@ -286,6 +277,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     constexpr int NG = (KS + CG - 1) / CG;
     const uint32_t kOOB = 0xffffffffu;
     const int nlive = s_nlive;
+    if (!direct || nlive == 0) prefetch(t);
     if (direct) {
       // Each wave copies its own H gate columns of the compacted rows straight into its LDS
       // slice (global_load_lds, 1 KB row segments), waits for its own loads only, and runs
@@ -293,20 +285,16 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       constexpr int SEGQ = KS * KC * ESZ / 1024;          // 1 KB segments per staged row
       for (int jt = 0; jt < NT; ++jt) {
         if (jt * 16 >= nlive) break;
+        // lane r holds the group row of compacted row jt*16 + r (read once, broadcast per row)
+        const int crow = (jt * 16 + (lane & 15) < nlive) ? s_crow[jt * 16 + (lane & 15)] : 0;
+        const int nrows = min(16, nlive - jt * 16);
+        for (int r = 0; r < nrows; ++r) {
+          const int b = row0 + __builtin_amdgcn_readlane(crow, r);
+          const elem_t* rowp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ci = jt * 16 + r;
-          if (ci < nlive) {
-            const int b = row0 + s_crow[ci];
-            const elem_t* rowp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H;
-#pragma unroll
-            for (int sj = 0; sj < SEGQ; ++sj) {
-              const elem_t* gp = rowp + sj * (1024 / ESZ) + lane * (16 / ESZ);
-              lds_ptr_t dst = (lds_ptr_t)(wbuf + r * QLD + sj * (1024 / ESZ));
-              if (a.coh_rows) __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, kSc1);
-              else __builtin_amdgcn_global_load_lds((const void*)gp, dst, 16, 0, 0);
-            }
-          }
+          for (int sj = 0; sj < SEGQ; ++sj)
+            dma16_global(rowp + sj * (1024 / ESZ) + lane * (16 / ESZ), lds_addr(wbuf + r * QLD + sj * (1024 / ESZ)),
+                         a.coh_rows != 0);
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         if (a.poll) {
@@ -332,11 +320,10 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
 #pragma unroll
               for (int sj = 0; sj < SEGQ; ++sj) {
                 if ((bad >> (r * SEGQ + sj)) & 1u) {
-                  const int b = row0 + s_crow[jt * 16 + r];
+                  const int b = row0 + __builtin_amdgcn_readlane(crow, r);
                   const elem_t* gp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H +
                                      sj * (1024 / ESZ) + lane * (16 / ESZ);
-                  __builtin_amdgcn_global_load_lds((const void*)gp, (lds_ptr_t)(wbuf + r * QLD + sj * (1024 / ESZ)),
-                                                   16, 0, kSc1);
+                  dma16_global(gp, lds_addr(wbuf + r * QLD + sj * (1024 / ESZ)), true);
                 }
               }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -349,27 +336,40 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
                   bad &= ~(1u << (r * SEGQ + sj));
           }
         }
+        // the next step's operands, once this step's first wait for dA rows is behind
+        if (jt == 0) prefetch(t);
         f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
+        // fragments read PD chunks ahead (the scheduler is held to that order)
+        constexpr int PD = PREC ? 6 : 3;
         if constexpr (PREC == 0) {
-          float4 bcur = *(const float4*)&wbuf[l16 * QLD + 4 * lq], bnxt = bcur;
+          float4 fr[PD + 1];
+#pragma unroll
+          for (int c = 0; c < PD && c < KS; ++c) fr[c] = *(const float4*)&wbuf[l16 * QLD + c * 16 + 4 * lq];
+          __builtin_amdgcn_sched_group_barrier(0x100, PD < KS ? PD : KS, 0);
 #pragma unroll
           for (int c = 0; c < KS; ++c) {
-            if (c + 1 < KS) bnxt = *(const float4*)&wbuf[l16 * QLD + (c + 1) * 16 + 4 * lq];
+            if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const float4*)&wbuf[l16 * QLD + (c + PD) * 16 + 4 * lq];
             f32x4& acc = (c & 1) ? acc1 : acc0;
+            const float4 bcur = fr[c % (PD + 1)];
             acc = mfma_f32_16x16x4(ureg32[c][0], bcur.x, acc);
             acc = mfma_f32_16x16x4(ureg32[c][1], bcur.y, acc);
             acc = mfma_f32_16x16x4(ureg32[c][2], bcur.z, acc);
             acc = mfma_f32_16x16x4(ureg32[c][3], bcur.w, acc);
-            bcur = bnxt;
+            if (c + PD < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
           }
         } else {
-          bf16x8 bcur = *(const bf16x8*)&wbuf[l16 * QLD + 8 * lq], bnxt = bcur;
+          bf16x8 fr[PD + 1];
+#pragma unroll
+          for (int c = 0; c < PD && c < KS; ++c) fr[c] = *(const bf16x8*)&wbuf[l16 * QLD + c * 32 + 8 * lq];
+          __builtin_amdgcn_sched_group_barrier(0x100, PD < KS ? PD : KS, 0);
 #pragma unroll
           for (int c = 0; c < KS; ++c) {
-            if (c + 1 < KS) bnxt = *(const bf16x8*)&wbuf[l16 * QLD + (c + 1) * 32 + 8 * lq];
+            if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&wbuf[l16 * QLD + (c + PD) * 32 + 8 * lq];
             f32x4& acc = (c & 1) ? acc1 : acc0;
-            acc = mfma_bf16_16x16x32(ureg16[c], bcur, acc);
-            bcur = bnxt;
+            acc = mfma_bf16_16x16x32(ureg16[c], fr[c % (PD + 1)], acc);
+            if (c + PD < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           }
         }
         const int ci = jt * 16 + l16;
@@ -490,47 +490,37 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         for (int j = 0; j < 4; ++j) red[wave][ci][4 * lq + j] = acc0[j] + acc1[j];
       }
     }
-    __syncthreads();
+    lds_sync();
     if (s_abort) break;
+    // dA U^T of the push rows: the parent's dh (the parent is now the top)
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
       if (c_op[i] == 1) {
-        const int r = prow[i], b = row0 + r;
-        const int ci = s_cidx[r];
-        const float sdh = red[0][ci][uu] + red[1][ci][uu] + red[2][ci][uu] + red[3][ci][uu];
-        if (t > 0 && c_sp[i] + 1 == t) {
-          nx_dh[i] += sdh;
-        } else if (pok[i]) {
-          tg_dh[i] += sdh;
-          a.dh_acc[((size_t)(c_sp[i] + 1) * B + b) * H + u] = tg_dh[i];
-        }
+        const int ci = s_cidx[prow[i]];
+        gh[i] += red[0][ci][uu] + red[1][ci][uu] + red[2][ci][uu] + red[3][ci][uu];
       }
     }
     if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
     // rotate: step t-1 becomes current
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
-      slot_dh[i] = nx_dh[i]; slot_dc[i] = nx_dc[i];
-      c_tp[i] = c_sp[i];
       c_op[i] = n_op[i]; c_sp[i] = n_sp[i];
-      {
-        int op = c_op[i], tp = c_tp[i], sp = c_sp[i];
-        valid(t - 1, op, tp, sp);
-        c_tp[i] = tp;
-      }
+      n_op[i] = nn_op[i]; n_sp[i] = nn_sp[i];
+      if (t > 2) valid_sp(t - 2, n_sp[i]);
       c_gh[i] = n_gh[i]; c_gc[i] = n_gc[i]; c_act[i] = n_act[i]; c_c[i] = n_c[i]; c_cp[i] = n_cp[i];
     }
-    __syncthreads();
+    lds_sync();
   }
 
   // ---- outputs of this workgroup: dh0, dc0 for its pairs; per-group bias gradient
+  // after step 0 the initial state is the top: its gradient is dh0, dc0
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
   for (int i = 0; i < PAIRS; ++i) {
     if (!pok[i]) continue;
     int b = row0 + prow[i];
-    a.dh0[(size_t)b * H + u] = a.dh_acc[(size_t)b * H + u];
-    a.dc0[(size_t)b * H + u] = a.dc_acc[(size_t)b * H + u];
+    a.dh0[(size_t)b * H + u] = gh[i];
+    a.dc0[(size_t)b * H + u] = gc[i];
   }
   const int rgrp = threadIdx.x >> 4;                 // 16 row groups share a unit
   for (int j = 0; j < 4; ++j) s_db[rgrp][uu][j] = dbacc[j];

@@ -1,6 +1,6 @@
 // Op validation and stack-pointer scan (paper, section 3: the unified update p <- p + op
 // with op in {+1 push, -1 pop, 0 hold}). ptr[t][b] is the pointer before step t;
-// ptr[T][b] the pointer after the last step. A pop while only the initial state is on
+// ptr[T][b] the pointer after the last step, also kept in depth_end[b] for the backward. A pop while only the initial state is on
 // the stack (p would become -1) is reported as EUNDERFLOW, an op outside {-1, 0, 1} as
 // EOPS; the reported element is the lowest failing batch index, and within it the
 // earliest failing step decides the code.
@@ -13,7 +13,7 @@ __global__ void __launch_bounds__(256) k_init_ctl(uint32_t* ctl) {
 // Block of 256 threads = 16 columns x 16 time segments. Two passes over each segment:
 // segment sums, a scan of the 16 sums per column in LDS, then the pointer values.
 __global__ void __launch_bounds__(256) k_scan(const int8_t* __restrict__ ops, int T, int B, int32_t* __restrict__ ptr,
-                                              uint32_t* ctl) {
+                                              int32_t* __restrict__ depth_end, uint32_t* ctl) {
   __shared__ int s_sum[16][17];
   __shared__ int s_first_bad[16], s_first_uf[16], s_maxd;
   const int c = threadIdx.x & 15, seg = threadIdx.x >> 4;
@@ -45,6 +45,7 @@ __global__ void __launch_bounds__(256) k_scan(const int8_t* __restrict__ ops, in
       ptr[(size_t)(t + 1) * B + b] = p;
       maxd = max(maxd, p);
     }
+    if (t1 == T && t0 < t1) depth_end[b] = p;      // the pointer after the last step
     atomicMin(&s_first_bad[c], first_bad);
     atomicMin(&s_first_uf[c], first_uf);
     atomicMax(&s_maxd, maxd);
