@@ -191,6 +191,32 @@ __device__ __forceinline__ void claim_group_slot(uint32_t* slot_ctrs, int G, int
 // forms address descriptor base + soff (wave-uniform) + voff (the lane's offset, the only
 // part the descriptor's range check covers).
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+// Buffer form: address = descriptor base + soff (wave-uniform) + voff (the lane's offset,
+// the only part the descriptor's range check covers: a lane given kOOB reads no memory and
+// writes zeros to its 16 LDS bytes). sc1 bypasses this CU's L1.
+constexpr uint32_t kOOB = 0xffffffffu;
+__device__ __forceinline__ void bdma16_sc1(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+  lds = __builtin_amdgcn_readfirstlane(lds);   // wave-uniform by contract: kept in SGPRs
+  soff = __builtin_amdgcn_readfirstlane(soff);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
+               ::"s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+__device__ __forceinline__ void bdma16(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+  lds = __builtin_amdgcn_readfirstlane(lds);   // wave-uniform by contract: kept in SGPRs
+  soff = __builtin_amdgcn_readfirstlane(soff);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               ::"s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+// Waits until at most N vector memory operations of this wave are outstanding (they
+// complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N <= 63, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+// Wave-uniform value kept in a scalar register.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ void dma16_global(const void* gp, uint32_t lds, bool sc1) {
   lds = __builtin_amdgcn_readfirstlane(lds);   // wave-uniform by contract; keeps it in an SGPR
   if (sc1)

@@ -275,102 +275,124 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // keep two independent MFMA chains.
     constexpr int CG = 8;
     constexpr int NG = (KS + CG - 1) / CG;
-    const uint32_t kOOB = 0xffffffffu;
     const int nlive = s_nlive;
     if (!direct || nlive == 0) prefetch(t);
-    if (direct) {
+    // whole 1 KB row segments, at most two per staged row (H of at most 512 fp32 / 1024 bf16)
+    constexpr bool kDirectOk = (KS * KC * ESZ) % 1024 == 0 && KS * KC * ESZ / 1024 <= 2;
+    if (kDirectOk && direct) {
+     if constexpr (kDirectOk) {
       // Each wave copies its own H gate columns of the compacted rows straight into its LDS
-      // slice (global_load_lds, 1 KB row segments), waits for its own loads only, and runs
-      // the tile's MFMAs from LDS with the fragments of the next chunk read ahead.
+      // slice (buffer LDS DMA, 1 KB row segments, segment-major: segment s of all 16 rows
+      // before segment s+1; rows past the list get an out-of-range offset, read no memory
+      // and leave zeros, which only reach the MFMA output columns of those rows),
+      // waits for its own loads only, and runs the MFMAs of segment s while the later
+      // segments are still arriving. Fragments of the next chunks are read ahead.
       constexpr int SEGQ = KS * KC * ESZ / 1024;          // 1 KB segments per staged row
+      constexpr int CPS = 1024 / (KC * ESZ);               // K chunks per segment (16)
+      static_assert(SEGQ * CPS == KS && SEGQ <= 2, "whole segments");
       for (int jt = 0; jt < NT; ++jt) {
         if (jt * 16 >= nlive) break;
         // lane r holds the group row of compacted row jt*16 + r (read once, broadcast per row)
         const int crow = (jt * 16 + (lane & 15) < nlive) ? s_crow[jt * 16 + (lane & 15)] : 0;
         const int nrows = min(16, nlive - jt * 16);
-        for (int r = 0; r < nrows; ++r) {
-          const int b = row0 + __builtin_amdgcn_readlane(crow, r);
-          const elem_t* rowp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H;
+        const uint32_t lds0 = lds_addr(wbuf);
+        // every workgroup of the group reads the same rows in the same order (measured faster
+        // than starting each at another row)
 #pragma unroll
-          for (int sj = 0; sj < SEGQ; ++sj)
-            dma16_global(rowp + sj * (1024 / ESZ) + lane * (16 / ESZ), lds_addr(wbuf + r * QLD + sj * (1024 / ESZ)),
-                         a.coh_rows != 0);
-        }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        if (a.poll) {
-          // granules whose producer's store has not arrived yet are fetched again (only the lanes
-          // that hold one take part in the copy), bypassing L1, until complete
-          static_assert(16 * SEGQ <= 32, "segment mask is 32 bits");
+        for (int sj = 0; sj < SEGQ; ++sj)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int b = row0 + __builtin_amdgcn_readlane(crow, r);
+            const uint32_t soff = (uint32_t)uni((int)((((uint32_t)t * B + b) * H4 + wave * H) * ESZ + sj * 1024));
+            bdma16(r_dA, r < nrows ? lane * 16u : kOOB, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
+          }
+        // granules (16 bytes of one lane) whose producer's store had not arrived when they were
+        // copied are fetched again, bypassing L1, until complete
+        auto settle = [&](int sj) {
           uint32_t bad = 0;
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-#pragma unroll
-            for (int sj = 0; sj < SEGQ; ++sj)
-              if (jt * 16 + r < nlive &&
-                  pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
-                bad |= 1u << (r * SEGQ + sj);
+            if (r < nrows && pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
+              bad |= 1u << r;
           int spins = 0;
           while (__builtin_amdgcn_ballot_w64(bad != 0u)) {
             if (spin_out(spins, a.ctl, a.spin_limit)) {
               s_abort = 1;
               break;
             }
+            // a row segment with a pending granule is copied again whole: a lane given an
+            // out-of-range offset would write zeros over its LDS bytes, and the granules that
+            // had arrived read back the same values
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-#pragma unroll
-              for (int sj = 0; sj < SEGQ; ++sj) {
-                if ((bad >> (r * SEGQ + sj)) & 1u) {
-                  const int b = row0 + __builtin_amdgcn_readlane(crow, r);
-                  const elem_t* gp = (const elem_t*)a.dA + ((size_t)t * B + b) * H4 + (size_t)wave * H +
-                                     sj * (1024 / ESZ) + lane * (16 / ESZ);
-                  dma16_global(gp, lds_addr(wbuf + r * QLD + sj * (1024 / ESZ)), true);
-                }
-              }
+            for (int r = 0; r < 16; ++r) {
+              const int b = row0 + __builtin_amdgcn_readlane(crow, r);
+              const uint32_t soff = (uint32_t)uni((int)((((uint32_t)t * B + b) * H4 + wave * H) * ESZ + sj * 1024));
+              if (__builtin_amdgcn_ballot_w64((bad >> r) & 1u))
+                bdma16_sc1(r_dA, lane * 16u, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
+            }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-#pragma unroll
-              for (int sj = 0; sj < SEGQ; ++sj)
-                if (((bad >> (r * SEGQ + sj)) & 1u) &&
-                    !pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
-                  bad &= ~(1u << (r * SEGQ + sj));
+              if (((bad >> r) & 1u) &&
+                  !pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
+                bad &= ~(1u << r);
           }
-        }
-        // the next step's operands, once this step's first wait for dA rows is behind
-        if (jt == 0) prefetch(t);
+        };
+        // segment sj is in LDS once at most 16 * (SEGQ - 1 - sj) DMAs are outstanding; the
+        // next step's operands are fetched after the tile's last wait (tile 0 only)
+        auto seg_ready = [&](int sj) {
+          if (sj == SEGQ - 1) wait_vm<0>();
+          else wait_vm<16 * (SEGQ > 1 ? SEGQ - 1 : 1)>();   // SEGQ <= 2
+          if (a.poll) settle(sj);
+          if (sj == SEGQ - 1 && jt == 0) prefetch(t);
+        };
         f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
-        // fragments read PD chunks ahead (the scheduler is held to that order)
+        // fragments read PD chunks ahead (the scheduler is held to that order); the wait for
+        // a segment comes before the first read ahead into it
         constexpr int PD = PREC ? 6 : 3;
-        if constexpr (PREC == 0) {
-          float4 fr[PD + 1];
+        // MFMAs over chunks [C0, C1): its own read-ahead ring, so no read crosses a segment
+        // boundary ahead of that segment's wait
+        auto run = [&](auto c0_, auto c1_) {
+          constexpr int C0 = decltype(c0_)::value, C1 = decltype(c1_)::value, N = C1 - C0;
+          if constexpr (PREC == 0) {
+            float4 fr[PD + 1];
 #pragma unroll
-          for (int c = 0; c < PD && c < KS; ++c) fr[c] = *(const float4*)&wbuf[l16 * QLD + c * 16 + 4 * lq];
-          __builtin_amdgcn_sched_group_barrier(0x100, PD < KS ? PD : KS, 0);
+            for (int c = 0; c < PD && c < N; ++c) fr[c] = *(const float4*)&wbuf[l16 * QLD + (C0 + c) * 16 + 4 * lq];
+            __builtin_amdgcn_sched_group_barrier(0x100, PD < N ? PD : N, 0);
 #pragma unroll
-          for (int c = 0; c < KS; ++c) {
-            if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const float4*)&wbuf[l16 * QLD + (c + PD) * 16 + 4 * lq];
-            f32x4& acc = (c & 1) ? acc1 : acc0;
-            const float4 bcur = fr[c % (PD + 1)];
-            acc = mfma_f32_16x16x4(ureg32[c][0], bcur.x, acc);
-            acc = mfma_f32_16x16x4(ureg32[c][1], bcur.y, acc);
-            acc = mfma_f32_16x16x4(ureg32[c][2], bcur.z, acc);
-            acc = mfma_f32_16x16x4(ureg32[c][3], bcur.w, acc);
-            if (c + PD < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+            for (int c = 0; c < N; ++c) {
+              if (c + PD < N) fr[(c + PD) % (PD + 1)] = *(const float4*)&wbuf[l16 * QLD + (C0 + c + PD) * 16 + 4 * lq];
+              f32x4& acc = (c & 1) ? acc1 : acc0;
+              const float4 bcur = fr[c % (PD + 1)];
+              acc = mfma_f32_16x16x4(ureg32[C0 + c][0], bcur.x, acc);
+              acc = mfma_f32_16x16x4(ureg32[C0 + c][1], bcur.y, acc);
+              acc = mfma_f32_16x16x4(ureg32[C0 + c][2], bcur.z, acc);
+              acc = mfma_f32_16x16x4(ureg32[C0 + c][3], bcur.w, acc);
+              if (c + PD < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+            }
+          } else {
+            bf16x8 fr[PD + 1];
+#pragma unroll
+            for (int c = 0; c < PD && c < N; ++c) fr[c] = *(const bf16x8*)&wbuf[l16 * QLD + (C0 + c) * 32 + 8 * lq];
+            __builtin_amdgcn_sched_group_barrier(0x100, PD < N ? PD : N, 0);
+#pragma unroll
+            for (int c = 0; c < N; ++c) {
+              if (c + PD < N) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&wbuf[l16 * QLD + (C0 + c + PD) * 32 + 8 * lq];
+              f32x4& acc = (c & 1) ? acc1 : acc0;
+              acc = mfma_bf16_16x16x32(ureg16[C0 + c], fr[c % (PD + 1)], acc);
+              if (c + PD < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            }
           }
+        };
+        seg_ready(0);
+        if constexpr (SEGQ == 1) {
+          run(std::integral_constant<int, 0>{}, std::integral_constant<int, KS>{});
         } else {
-          bf16x8 fr[PD + 1];
-#pragma unroll
-          for (int c = 0; c < PD && c < KS; ++c) fr[c] = *(const bf16x8*)&wbuf[l16 * QLD + c * 32 + 8 * lq];
-          __builtin_amdgcn_sched_group_barrier(0x100, PD < KS ? PD : KS, 0);
-#pragma unroll
-          for (int c = 0; c < KS; ++c) {
-            if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&wbuf[l16 * QLD + (c + PD) * 32 + 8 * lq];
-            f32x4& acc = (c & 1) ? acc1 : acc0;
-            acc = mfma_bf16_16x16x32(ureg16[c], fr[c % (PD + 1)], acc);
-            if (c + PD < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          }
+          run(std::integral_constant<int, 0>{}, std::integral_constant<int, CPS>{});
+          seg_ready(1);
+          run(std::integral_constant<int, CPS>{}, std::integral_constant<int, KS>{});
         }
         const int ci = jt * 16 + l16;
         if (ci < nlive) {
@@ -378,6 +400,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
           for (int j = 0; j < 4; ++j) red[wave][ci][4 * lq + j] = acc0[j] + acc1[j];
         }
       }
+     }
     } else
     for (int jt = 0; jt < NT; ++jt) {
       if (jt * 16 >= nlive) break;

@@ -44,40 +44,17 @@ typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
 namespace {
 
-// Waits until at most N vector memory operations of this wave are outstanding.
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N <= 63, "vmcnt is 6 bits");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-  asm volatile("" ::: "memory");
-}
 __device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 // Workgroup barrier for LDS data only: it does not wait for global loads or stores.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 __device__ __forceinline__ void order() { asm volatile("" ::: "memory"); }
 
 __device__ __forceinline__ uint32_t f2u(float f) { return __float_as_uint(f); }
-// LDS DMA written as inline assembly: the compiler then does not order every later LDS
-// read behind it with a vmcnt(0) wait (this kernel counts its own waits). M0 holds the
-// wave's LDS destination (lane i writes at M0 + i * size); writing M0 needs one wait state
-// before the DMA. Buffer form: address = descriptor base + soff (wave-uniform) + voff (the
-// lane's offset, the only part the descriptor's range check covers).
-__device__ __forceinline__ void bdma16_sc1(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
-               ::"s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
-}
-__device__ __forceinline__ void bdma16(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               ::"s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
-}
 __device__ __forceinline__ void dma4(const void* gp, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(gp) : "memory", "m0");
 }
-// Wave-uniform value kept in a scalar register.
-__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ uint32_t umax3(uint32_t a, uint32_t b, uint32_t c) { return max(max(a, b), c); }
 
-constexpr uint32_t kOOB = 0xffffffffu;   // buffer offset past every record: the access is dropped
 
 }  // namespace
 
