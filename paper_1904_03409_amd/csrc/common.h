@@ -193,7 +193,8 @@ __device__ __forceinline__ void claim_group_slot(uint32_t* slot_ctrs, int G, int
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 // Buffer form: address = descriptor base + soff (wave-uniform) + voff (the lane's offset,
 // the only part the descriptor's range check covers: a lane given kOOB reads no memory and
-// writes zeros to its 16 LDS bytes). sc1 bypasses this CU's L1.
+// writes zeros to its 16 LDS bytes). sc1 bypasses this CU's L1. An instruction immediate
+// offset would move the LDS address as well (M0 + immediate + 16 * lane); these forms use none.
 constexpr uint32_t kOOB = 0xffffffffu;
 __device__ __forceinline__ void bdma16_sc1(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
   lds = __builtin_amdgcn_readfirstlane(lds);   // wave-uniform by contract: kept in SGPRs
@@ -214,6 +215,18 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N <= 63, "vmcnt is 6 bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
   asm volatile("" ::: "memory");
+}
+// The same for a wave-uniform count n in [0, 16] (n outside it waits for all).
+__device__ __forceinline__ void wait_vm_upto16(int n) {
+  switch (n) {
+#define SLSTM_WAIT_CASE(k) case k: wait_vm<k>(); break;
+    SLSTM_WAIT_CASE(1) SLSTM_WAIT_CASE(2) SLSTM_WAIT_CASE(3) SLSTM_WAIT_CASE(4) SLSTM_WAIT_CASE(5)
+    SLSTM_WAIT_CASE(6) SLSTM_WAIT_CASE(7) SLSTM_WAIT_CASE(8) SLSTM_WAIT_CASE(9) SLSTM_WAIT_CASE(10)
+    SLSTM_WAIT_CASE(11) SLSTM_WAIT_CASE(12) SLSTM_WAIT_CASE(13) SLSTM_WAIT_CASE(14) SLSTM_WAIT_CASE(15)
+    SLSTM_WAIT_CASE(16)
+#undef SLSTM_WAIT_CASE
+    default: wait_vm<0>(); break;
+  }
 }
 // Wave-uniform value kept in a scalar register.
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }

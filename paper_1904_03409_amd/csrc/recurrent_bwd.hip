@@ -282,11 +282,12 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     if (kDirectOk && direct) {
      if constexpr (kDirectOk) {
       // Each wave copies its own H gate columns of the compacted rows straight into its LDS
-      // slice (buffer LDS DMA, 1 KB row segments, segment-major: segment s of all 16 rows
-      // before segment s+1; rows past the list get an out-of-range offset, read no memory
-      // and leave zeros, which only reach the MFMA output columns of those rows),
-      // waits for its own loads only, and runs the MFMAs of segment s while the later
-      // segments are still arriving. Fragments of the next chunks are read ahead.
+      // slice (buffer LDS DMA, 1 KB row segments, segment-major: segment s of the tile's rows
+      // before segment s+1), waits for its own loads only, and runs the MFMAs of segment s
+      // while the later segments are still arriving. Only listed rows are copied: an LDS DMA
+      // costs about the same whether its lanes are in range or not. Slots of the rows past
+      // the list keep an earlier tile's values, which only reach the MFMA output columns of
+      // those rows (discarded). Fragments of the next chunks are read ahead.
       constexpr int SEGQ = KS * KC * ESZ / 1024;          // 1 KB segments per staged row
       constexpr int CPS = 1024 / (KC * ESZ);               // K chunks per segment (16)
       static_assert(SEGQ * CPS == KS && SEGQ <= 2, "whole segments");
@@ -302,9 +303,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         for (int sj = 0; sj < SEGQ; ++sj)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int b = row0 + __builtin_amdgcn_readlane(crow, r);
-            const uint32_t soff = (uint32_t)uni((int)((((uint32_t)t * B + b) * H4 + wave * H) * ESZ + sj * 1024));
-            bdma16(r_dA, r < nrows ? lane * 16u : kOOB, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
+            if (r < nrows) {
+              const int b = row0 + __builtin_amdgcn_readlane(crow, r);
+              const uint32_t soff = (uint32_t)uni((int)((((uint32_t)t * B + b) * H4 + wave * H) * ESZ + sj * 1024));
+              bdma16(r_dA, lane * 16u, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
+            }
           }
         // granules (16 bytes of one lane) whose producer's store had not arrived when they were
         // copied are fetched again, bypassing L1, until complete
@@ -338,11 +341,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
                 bad &= ~(1u << r);
           }
         };
-        // segment sj is in LDS once at most 16 * (SEGQ - 1 - sj) DMAs are outstanding; the
+        // segment sj is in LDS once at most nrows * (SEGQ - 1 - sj) DMAs are outstanding; the
         // next step's operands are fetched after the tile's last wait (tile 0 only)
         auto seg_ready = [&](int sj) {
           if (sj == SEGQ - 1) wait_vm<0>();
-          else wait_vm<16 * (SEGQ > 1 ? SEGQ - 1 : 1)>();   // SEGQ <= 2
+          else wait_vm_upto16(nrows);   // SEGQ == 2: the second segment's nrows DMAs may be in flight
           if (a.poll) settle(sj);
           if (sj == SEGQ - 1 && jt == 0) prefetch(t);
         };
