@@ -135,12 +135,18 @@ __device__ __forceinline__ bool spin_out(int& spins, uint32_t* ctl, int spin_lim
 // Data written by other workgroups before the barrier must then be read with the
 // ld_coh_* loads above. Returns true when the spin limit ran out (or another group's
 // did): the caller must then leave its loop so that every wave of the grid exits.
-__device__ __forceinline__ bool group_barrier(uint32_t* ctr, uint32_t target, uint32_t* ctl, int spin_limit,
-                                              int* s_flag) {
+// Arrival half: stores acknowledged, workgroup met, the group counter incremented.
+__device__ __forceinline__ void group_arrive(uint32_t* ctr) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waiting half: one lane polls the counter up to target; returns true when the spin limit
+// ran out or another workgroup gave up. Work that needs no other workgroup's data can run
+// between the two halves.
+__device__ __forceinline__ bool group_wait(uint32_t* ctr, uint32_t target, uint32_t* ctl, int spin_limit,
+                                           int* s_flag) {
   if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     int spins = 0, bad = 0;
     while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       ++spins;
@@ -159,6 +165,11 @@ __device__ __forceinline__ bool group_barrier(uint32_t* ctr, uint32_t target, ui
   }
   __syncthreads();
   return *s_flag != 0;
+}
+__device__ __forceinline__ bool group_barrier(uint32_t* ctr, uint32_t target, uint32_t* ctl, int spin_limit,
+                                              int* s_flag) {
+  group_arrive(ctr);
+  return group_wait(ctr, target, ctl, spin_limit, s_flag);
 }
 
 // Claims this workgroup's (group, member) slot from the XCC it runs on, so that every

@@ -262,10 +262,21 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     }
 
     if (clk && threadIdx.x == 0) clk[t * 4 + 1] = wall_clock64();
+    // byte offset (this wave's gate columns) of the dA row of compacted row r of tile 0, in
+    // lane r: computed while the group barrier is in flight
+    uint32_t soff0 = 0;
+    auto row_offsets0 = [&]() {
+      const int cr = lane & 15;
+      const int crow0 = cr < s_nlive ? s_crow[cr] : 0;
+      soff0 = (((uint32_t)t * B + row0 + crow0) * H4 + wave * H) * ESZ;
+    };
     if (a.poll) {
       lds_sync();
-    } else if (group_barrier(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_abort)) {
-      break;
+      if (direct) row_offsets0();
+    } else {
+      group_arrive(&a.ctl[CTL_BAR_B + g * 16]);
+      if (direct) row_offsets0();
+      if (group_wait(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_abort)) break;
     }
     if (clk && threadIdx.x == 0) clk[t * 4 + 2] = wall_clock64();
     // Only push rows have non-zero dA. They are listed (in row order) in s_crow and run as
@@ -293,8 +304,12 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       static_assert(SEGQ * CPS == KS && SEGQ <= 2, "whole segments");
       for (int jt = 0; jt < NT; ++jt) {
         if (jt * 16 >= nlive) break;
-        // lane r holds the group row of compacted row jt*16 + r (read once, broadcast per row)
-        const int crow = (jt * 16 + (lane & 15) < nlive) ? s_crow[jt * 16 + (lane & 15)] : 0;
+        // lane r holds the byte offset of the dA row of compacted row jt*16 + r (broadcast per row)
+        uint32_t soffv = soff0;
+        if (jt > 0) {
+          const int crow = (jt * 16 + (lane & 15) < nlive) ? s_crow[jt * 16 + (lane & 15)] : 0;
+          soffv = (((uint32_t)t * B + row0 + crow) * H4 + wave * H) * ESZ;
+        }
         const int nrows = min(16, nlive - jt * 16);
         const uint32_t lds0 = lds_addr(wbuf);
         // every workgroup of the group reads the same rows in the same order (measured faster
@@ -304,8 +319,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             if (r < nrows) {
-              const int b = row0 + __builtin_amdgcn_readlane(crow, r);
-              const uint32_t soff = (uint32_t)uni((int)((((uint32_t)t * B + b) * H4 + wave * H) * ESZ + sj * 1024));
+              const uint32_t soff = (uint32_t)__builtin_amdgcn_readlane((int)soffv, r) + sj * 1024;
               bdma16(r_dA, lane * 16u, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
             }
           }
@@ -328,8 +342,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
             // had arrived read back the same values
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-              const int b = row0 + __builtin_amdgcn_readlane(crow, r);
-              const uint32_t soff = (uint32_t)uni((int)((((uint32_t)t * B + b) * H4 + wave * H) * ESZ + sj * 1024));
+              const uint32_t soff = (uint32_t)__builtin_amdgcn_readlane((int)soffv, r) + sj * 1024;
               if (__builtin_amdgcn_ballot_w64((bad >> r) & 1u))
                 bdma16_sc1(r_dA, lane * 16u, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
             }
