@@ -6,6 +6,8 @@
 #include <algorithm>
 #include <mutex>
 
+#include <rocblas/rocblas.h>
+
 #include "../../include/stacklstm.h"
 #include "common.h"
 #include "gemm.h"
@@ -23,6 +25,8 @@ __global__ void k_zero_u32(uint32_t* p, int n);
 __global__ void k_fill_pattern(unsigned char* p, size_t bytes, uint32_t v);
 __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
+__global__ void k_augment_x(const float* x, size_t rows, int I, int KA, int nones, float* out32, bf16_t* out16);
+__global__ void k_bias_rows(const float* b, int H, int nparts, int nrows, float* out32, bf16_t* out16);
 __global__ void k_push_rows(const int8_t* ops, int n, int32_t* rows, uint32_t* count);
 __global__ void k_zero_nonpush_rows(const int8_t* ops, float* out, size_t n, int cols);
 __global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const int32_t* prow,
@@ -168,6 +172,27 @@ int make_plan(const slstm_dims* d, Plan* p) {
   return SLSTM_OK;
 }
 
+// The input projection XW = x Wp + b is one plain GEMM on the vendor BLAS: x gets columns of
+// ones (one in fp32 mode; three in bf16 mode, where b is carried as the sum of three bf16
+// parts, so the bias keeps fp32 precision) and Wp gets the matching bias rows; K is padded
+// to a multiple of 8 with zeros.
+int xw_ones(const slstm_dims* d) { return d->precision == SLSTM_BF16_GEMM ? 3 : 1; }
+size_t xw_k(const slstm_dims* d) { return ((size_t)d->I + xw_ones(d) + 7) / 8 * 8; }
+
+// One rocBLAS handle per device, created on first use; calls that share it are serialised
+// (the handle's stream is set per call).
+std::mutex& blas_mutex() {
+  static std::mutex mu;
+  return mu;
+}
+rocblas_handle blas_handle() {
+  static rocblas_handle h[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!h[dev] && rocblas_create_handle(&h[dev]) != rocblas_status_success) h[dev] = nullptr;
+  return h[dev];
+}
+
 // Work-space layout; splits are bounded by 64 so the layout does not depend on the device.
 Layout layout(const slstm_dims* d) {
   const size_t T = d->T, B = d->B, I = d->I, H = d->H;
@@ -177,11 +202,12 @@ Layout layout(const slstm_dims* d) {
   size_t o = 0;
   L.ctl = o; o += align256(CTL_WORDS * 4);
   L.stack = o; o += align256(B * (T + 1) * 4);
-  L.wp = o; o += align256(I * 4 * H * 4);
+  const size_t KA = xw_k(d);
+  L.wp = o; o += align256(KA * 4 * H * 4);                              // Wp and its bias rows
   L.r1 = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));   // XW (forward), dA (backward)
   L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
   L.hx = o; o += bf ? align256((T + 1) * B * H * 2) : 0;
-  L.xb = o; o += bf ? align256(T * B * I * 2) : 0;                    // x in bf16 (bf16 mode)
+  L.xb = o; o += align256(T * B * KA * (bf ? 2 : 4));                 // [x | ones | 0] for the XW GEMM
   // post-loop operands over the push rows (at most T*B of them; KP with the K-tile padding)
   L.xbt = o; o += bf ? align256(KP * I * 2) : 0;                      // x^T in bf16 (bf16 mode)
   L.hp = o; o += align256(std::max<size_t>(bf ? KP * H * 2 : T * B * H * 4, 16));   // Hprev (bf16 mode: Hprev^T)
@@ -334,27 +360,36 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   mark(d, 1, st);
   if (T == 0) return SLSTM_OK;
 
-  // a2: XW = x Wp + b for all steps (Wp = W with gate-interleaved columns)
+  // a2: XW = [x | 1] [Wp ; b] for all steps (Wp = W with gate-interleaved columns), on rocBLAS
   const bool bf = p.prec == SLSTM_BF16_GEMM;
   void* wp = ws + L.wp;
+  const int KA = (int)xw_k(d), NO = xw_ones(d);
   hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W,
                      bf ? nullptr : (float*)wp, bf ? (bf16_t*)wp : nullptr, I, H);
+  hipLaunchKernelGGL(k_bias_rows, dim3(grid1d((size_t)(KA - I) * 4 * H)), dim3(256), 0, st, b, H, NO, KA - I,
+                     bf ? nullptr : (float*)wp + (size_t)I * 4 * H, bf ? (bf16_t*)wp + (size_t)I * 4 * H : nullptr);
   float* xw = (float*)(ws + L.r1);
-  const void* xa = x;
-  if (bf) {
-    hipLaunchKernelGGL(k_to_bf16, dim3(grid1d((size_t)T * B * I)), dim3(256), 0, st, x, (bf16_t*)(ws + L.xb),
-                       (size_t)T * B * I);
-    xa = ws + L.xb;
+  void* xa = ws + L.xb;
+  hipLaunchKernelGGL(k_augment_x, dim3(grid1d((size_t)T * B * KA)), dim3(256), 0, st, x, (size_t)T * B, I, KA, NO,
+                     bf ? nullptr : (float*)xa, bf ? (bf16_t*)xa : nullptr);
+  if ((rc = hip_status(hipGetLastError()))) return rc;
+  {
+    // column-major view: XW^T [4H x TB] = Wp_aug^T [4H x KA] . x_aug^T [KA x TB]
+    std::lock_guard<std::mutex> lk(blas_mutex());
+    rocblas_handle h = blas_handle();
+    if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+    const float one = 1.f, zero = 0.f;
+    rocblas_status bs;
+    if (!bf)
+      bs = rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_none, 4 * H, T * B, KA, &one, (const float*)wp,
+                         4 * H, (const float*)xa, KA, &zero, xw, 4 * H);
+    else
+      bs = rocblas_gemm_ex(h, rocblas_operation_none, rocblas_operation_none, 4 * H, T * B, KA, &one, wp,
+                           rocblas_datatype_bf16_r, 4 * H, xa, rocblas_datatype_bf16_r, KA, &zero, xw,
+                           rocblas_datatype_f32_r, 4 * H, xw, rocblas_datatype_f32_r, 4 * H, rocblas_datatype_f32_r,
+                           rocblas_gemm_algo_standard, 0, 0);
+    if (bs != rocblas_status_success) return SLSTM_EDEVICE;
   }
-  GemmArgs g;
-  memset(&g, 0, sizeof(g));
-  g.M = T * B; g.N = 4 * H; g.K = I;
-  const int VE = bf ? 8 : 4;
-  g.A = xa; g.lda = I; g.a_vec = (I % VE == 0);
-  g.Bm = wp; g.ldb = 4 * H; g.b_vec = ((4 * H) % VE == 0);
-  g.C = xw; g.ldc = 4 * H; g.bias = b; g.bias_H = H;
-  g.k_chunk = k_chunk_for(I, 1); g.split_stride = 0;
-  if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_KN, g, 1, st))) return rc;
 
   // a3-a6: persistent recurrent kernel
   RecArgs a = rec_args(d, p, ws, L, false);

@@ -168,6 +168,47 @@ __global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ in, b
     out[i] = f32_to_bf16_bits(in[i]);
 }
 
+// Operand of the input-projection GEMM: out [rows][KA] = [x | nones columns of 1 | 0], in
+// fp32 (out32) or bf16 (out16, x rounded as k_to_bf16 does).
+__global__ void __launch_bounds__(256) k_augment_x(const float* __restrict__ x, size_t rows, int I, int KA, int nones,
+                                                   float* __restrict__ out32, bf16_t* __restrict__ out16) {
+  const size_t n = rows * (size_t)KA;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t r = i / (size_t)KA;
+    const int c = (int)(i - r * (size_t)KA);
+    const float v = c < I ? x[r * (size_t)I + c] : (c < I + nones ? 1.f : 0.f);
+    if (out32) out32[i] = v;
+    else out16[i] = f32_to_bf16_bits(v);
+  }
+}
+
+// Bias rows under the gate-interleaved Wp: row j < nparts holds the j-th part of b (fp32: b
+// itself; bf16: b = p0 + p1 + p2 with p0 = bf16(b), p1 = bf16(b - p0), p2 = bf16(b - p0 - p1),
+// each difference exact in fp32), the other rows up to nrows are 0.
+__global__ void __launch_bounds__(256) k_bias_rows(const float* __restrict__ b, int H, int nparts, int nrows,
+                                                   float* __restrict__ out32, bf16_t* __restrict__ out16) {
+  const int H4 = 4 * H;
+  const size_t n = (size_t)nrows * H4;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int j = (int)(i / (size_t)H4);
+    const int col = (int)(i - (size_t)j * H4);
+    float rem = b ? b[perm_to_orig(col, H)] : 0.f;
+    float part = 0.f;
+    if (out32) {
+      part = j == 0 ? rem : 0.f;
+      out32[i] = part;
+    } else {
+      bf16_t bits = 0;
+      for (int q = 0; q <= j && q < nparts; ++q) {
+        bits = f32_to_bf16_bits(rem);
+        const float pv = __uint_as_float((uint32_t)bits << 16);
+        if (q < j) rem -= pv;
+      }
+      out16[i] = j < nparts ? bits : (bf16_t)0;
+    }
+  }
+}
+
 // Push-row list: rows[k] = t*B + b of the k-th push (op = +1) in increasing row order, and
 // *count = the number of pushes. Only push steps have a non-zero gate gradient dA (the
 // states other steps write are never read, section 3, Observation 2), so the post-loop
