@@ -185,6 +185,23 @@ std::mutex& blas_mutex() {
   static std::mutex mu;
   return mu;
 }
+// Side stream and fork/join events per device (default priority, kept for the process's
+// lifetime): the producer trace runs there, beside the input projection on the caller's
+// stream. Enqueued under blas_mutex(), so a join always follows the trace of the same call.
+struct SideStream { hipStream_t s; hipEvent_t fork, join; bool ok; };
+SideStream* side_stream() {
+  static SideStream ss[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  SideStream& x = ss[dev];
+  if (!x.ok) {
+    if (hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&x.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess) return nullptr;
+    x.ok = true;
+  }
+  return &x;
+}
 rocblas_handle blas_handle() {
   static rocblas_handle h[64] = {};
   int dev = 0;
@@ -348,15 +365,15 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if (hipMemcpyAsync(hs, ctl + CTL_STATUS, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
   if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
   if (hs[0] != 0x7fffffffu) return (int)(hs[0] & 7u);
-  if (T > 0 && p.wide) {
-    // producer trace from the ops (the wide forward keeps no integer stack): one thread per
-    // element, its stack in LDS (odd slot count: no bank conflicts between neighbours)
-    const int cap = (int)std::min<uint32_t>(hs[1] + 2u, (uint32_t)T + 1u) | 1;
-    int R = 64;
-    while (R > 1 && (size_t)R * cap * 4 > 48 * 1024) R /= 2;
-    if ((size_t)R * cap * 4 > 48 * 1024) return SLSTM_EINVAL;   // stack deeper than 12 K slots
-    hipLaunchKernelGGL(k_trace, dim3((B + R - 1) / R), dim3(R), (size_t)R * cap * 4, st, ops, T, B, cap, top);
-  }
+  // the wide and the pipelined forward read a finished producer trace (they keep no integer
+  // stack of their own); the plain forward traces in-kernel
+  const bool pretrace = p.wide || p.pipe;
+  // producer trace from the ops: one thread per element, its stack in LDS (odd slot count:
+  // no bank conflicts between neighbours); launched beside the input projection below
+  const int trace_cap = (int)std::min<uint32_t>(hs[1] + 2u, (uint32_t)T + 1u) | 1;
+  int trace_R = 64;
+  while (trace_R > 1 && (size_t)trace_R * trace_cap * 4 > 48 * 1024) trace_R /= 2;
+  if (T > 0 && pretrace && (size_t)trace_R * trace_cap * 4 > 48 * 1024) return SLSTM_EINVAL;   // deeper than 12 K slots
   mark(d, 1, st);
   if (T == 0) return SLSTM_OK;
 
@@ -376,6 +393,15 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   {
     // column-major view: XW^T [4H x TB] = Wp_aug^T [4H x KA] . x_aug^T [KA x TB]
     std::lock_guard<std::mutex> lk(blas_mutex());
+    SideStream* side = pretrace ? side_stream() : nullptr;
+    if (pretrace && !side) return SLSTM_EDEVICE;
+    if (pretrace) {
+      if (hipEventRecord(side->fork, st) != hipSuccess || hipStreamWaitEvent(side->s, side->fork, 0) != hipSuccess)
+        return SLSTM_EDEVICE;
+      hipLaunchKernelGGL(k_trace, dim3((B + trace_R - 1) / trace_R), dim3(trace_R), (size_t)trace_R * trace_cap * 4,
+                         side->s, ops, T, B, trace_cap, top);
+      if (hipEventRecord(side->join, side->s) != hipSuccess) return SLSTM_EDEVICE;
+    }
     rocblas_handle h = blas_handle();
     if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
     const float one = 1.f, zero = 0.f;
@@ -389,6 +415,7 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                            rocblas_datatype_f32_r, 4 * H, xw, rocblas_datatype_f32_r, 4 * H, rocblas_datatype_f32_r,
                            rocblas_gemm_algo_standard, 0, 0);
     if (bs != rocblas_status_success) return SLSTM_EDEVICE;
+    if (pretrace && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return SLSTM_EDEVICE;
   }
 
   // a3-a6: persistent recurrent kernel
@@ -401,10 +428,11 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     const size_t ex_bytes = (size_t)T * B * H * (bf ? 2 : 4);
     unsigned char* ex = bf ? (unsigned char*)(a.hx + (size_t)B * H) : (unsigned char*)h_cell;
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(ex_bytes / 16 + 1)), dim3(256), 0, st, ex, ex_bytes, 0xffffffffu);
-    if (!p.wide)                                   // the wide forward reads the finished trace
+    if (!pretrace)
       hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st,
                          (unsigned char*)top, (size_t)T * B * 4, kTopPending);
   }
+  a.traced = pretrace ? 1 : 0;
   a.htop = p.wide ? h_top : nullptr;
   a.ctop = p.wide ? c_top : nullptr;
   if (p.wide) a.NW = p.NWw;

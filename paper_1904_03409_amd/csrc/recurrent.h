@@ -12,6 +12,7 @@ struct RecArgs {
   int coh_rows, coh_top;
   int bwd_direct;        // backward stages dA rows with global_load_lds (host checks the LDS fits)
   int poll;              // 1: workgroups exchange rows by polling fill-marked data; 0: group barrier per step
+  int traced;            // 1: top[] holds the finished producer trace before the forward kernel starts
   const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)

@@ -127,8 +127,10 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   bf16x8 ureg16[PREC ? KS : 1];
   fwd_load_u<PREC, KS>(a, unit_base, l16, lq, ureg32, ureg16);
 
-  // integer stack of the group's rows, kept by workgroup 0 one step ahead of the floats
-  const bool tracer = (w == 0) && ((int)threadIdx.x < BG) && (row0 + (int)threadIdx.x < B);
+  // integer stack of the group's rows, kept by workgroup 0 one step ahead of the floats,
+  // unless the producer trace was computed before the kernel (then top[] is final and the
+  // polls below return at their first load)
+  const bool tracer = !a.traced && (w == 0) && ((int)threadIdx.x < BG) && (row0 + (int)threadIdx.x < B);
   const int my_row = row0 + (int)threadIdx.x;
   const size_t stk_base = (size_t)my_row * (T + 1);
   int my_p = 0, my_top = -1, op_next = 0;
