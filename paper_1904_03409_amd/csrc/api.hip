@@ -19,6 +19,8 @@ __global__ void k_scan(const int8_t* ops, int T, int B, int32_t* ptr, int32_t* d
 __global__ void k_gather_top(const int32_t* top, const float* cellv, const float* init, float* out, int T, int B,
                              int H, int skip_push);
 __global__ void k_trace(const int8_t* ops, int T, int B, int cap, int32_t* top);
+__global__ void k_gather_top4(const int32_t* top, const float* hcell, const float* h0, float* htop, const float* ccell,
+                              const float* c0, float* ctop, int T, int B, int H, int skip_h);
 __global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
@@ -445,10 +447,18 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
 
   // a7: Algorithm 1's return values (the wide forward writes c_top and the h_top of push steps)
   size_t n = (size_t)T * B * H;
-  if (h_top)
-    hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H, p.wide);
-  if (c_top && !p.wide)
-    hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, c_top, T, B, H, 0);
+  float* ctop_g = p.wide ? nullptr : c_top;          // the wide forward writes c_top itself
+  const auto al16 = [](const void* q) { return ((uintptr_t)q & 15u) == 0; };
+  if (H % 4 == 0 && al16(h_cell) && al16(h0) && al16(h_top) && al16(c_cell) && al16(c0) && al16(c_top)) {
+    if (h_top || ctop_g)
+      hipLaunchKernelGGL(k_gather_top4, dim3(grid1d(n / 4)), dim3(256), 0, st, top, h_cell, h0, h_top, c_cell, c0, ctop_g,
+                         T, B, H, p.wide);
+  } else {
+    if (h_top)
+      hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H, p.wide);
+    if (ctop_g)
+      hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, ctop_g, T, B, H, 0);
+  }
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 4, st);
   if (d->spin_limit > 0) return check_timeout(ctl, st);

@@ -117,6 +117,33 @@ __global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ 
   }
 }
 
+// The same for h_top and c_top in one pass (either may be null; skip_h as skip_push for
+// h_top), four units per thread: H must be a multiple of 4 and the arrays 16-byte aligned.
+__global__ void __launch_bounds__(256) k_gather_top4(const int32_t* __restrict__ top, const float* __restrict__ hcell,
+                                                     const float* __restrict__ h0, float* __restrict__ htop,
+                                                     const float* __restrict__ ccell, const float* __restrict__ c0,
+                                                     float* __restrict__ ctop, int T, int B, int H, int skip_h) {
+  const int H4 = H / 4;
+  const size_t n = (size_t)T * B * H4;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t tb = i / H4;
+    const int u4 = (int)(i - tb * H4);
+    const int b = (int)(tb % B), t = (int)(tb / B);
+    const int s = top[tb];
+    const bool bad = s < -1 || s > t;             // not a valid producer
+    const float nan = __builtin_nanf("");
+    const size_t src = (s < 0 || bad) ? (size_t)b * H4 + u4 : ((size_t)s * B + b) * H4 + u4;
+    if (htop && !(skip_h && s == t)) {
+      const float4 v = bad ? float4{nan, nan, nan, nan} : (s < 0 ? ((const float4*)h0)[src] : ((const float4*)hcell)[src]);
+      ((float4*)htop)[i] = v;
+    }
+    if (ctop) {
+      const float4 v = bad ? float4{nan, nan, nan, nan} : (s < 0 ? ((const float4*)c0)[src] : ((const float4*)ccell)[src]);
+      ((float4*)ctop)[i] = v;
+    }
+  }
+}
+
 // W [I][4H] (gate-major columns) -> Wp [I][4H] gate-interleaved, as fp32 or bf16.
 __global__ void __launch_bounds__(256) k_permute_w(const float* __restrict__ W, float* __restrict__ Wp32,
                                                    bf16_t* __restrict__ Wp16, int I, int H) {
