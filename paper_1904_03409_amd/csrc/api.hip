@@ -5,6 +5,7 @@
 #include <string.h>
 #include <algorithm>
 #include <mutex>
+#include <unordered_map>
 
 #include <rocblas/rocblas.h>
 
@@ -31,6 +32,8 @@ __global__ void k_augment_x(const float* x, size_t rows, int I, int KA, int none
 __global__ void k_bias_rows(const float* b, int H, int nparts, int nrows, float* out32, bf16_t* out16);
 __global__ void k_push_rows(const int8_t* ops, int n, int32_t* rows, uint32_t* count);
 __global__ void k_zero_nonpush_rows(const int8_t* ops, float* out, size_t n, int cols);
+__global__ void k_gather_rows(const float* src, const int32_t* prow, const uint32_t* count, size_t max_rows, int cols,
+                              int scatter, float* dst);
 __global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const int32_t* prow,
                                const uint32_t* count, float* out, int T, int B, int H);
 __global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int cols, const int32_t* prow,
@@ -75,7 +78,7 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, prow, dep, total;
+  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, prow, dep, dac, xc, total;
 };
 
 // Push-row count padded to the K tile: leading dimension of the transposed bf16 operands
@@ -212,6 +215,19 @@ rocblas_handle blas_handle() {
   return h[dev];
 }
 
+// Number of push rows per work space, read back with the forward's status: the backward's
+// vendor-BLAS gradient GEMMs need it on the host. A backward without a recorded count (or
+// with other T, B) runs the device-count kernels instead.
+struct PushCount { int T, B; uint32_t n; };
+std::mutex& push_mutex() {
+  static std::mutex mu;
+  return mu;
+}
+std::unordered_map<const void*, PushCount>& push_counts() {
+  static std::unordered_map<const void*, PushCount> m;
+  return m;
+}
+
 // Work-space layout; splits are bounded by 64 so the layout does not depend on the device.
 Layout layout(const slstm_dims* d) {
   const size_t T = d->T, B = d->B, I = d->I, H = d->H;
@@ -237,6 +253,9 @@ Layout layout(const slstm_dims* d) {
   L.part = o; o += align256((size_t)64 * std::max(I, H) * 4 * H * 4);
   L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
   L.dep = o; o += align256(B * 4);                                     // pointer after the last step
+  // fp32 post-loop operands on the vendor BLAS: dA and x rows of the push steps, compacted
+  L.dac = o; o += bf ? 0 : align256(std::max<size_t>(T * B * 4 * H * 4, 16));
+  L.xc = o; o += bf ? 0 : align256(std::max<size_t>(T * B * std::max(I, (size_t)1) * 4, 16));
   L.total = o;
   return L;
 }
@@ -363,10 +382,15 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   mark(d, 0, st);
   hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl);
   hipLaunchKernelGGL(k_scan, dim3((B + 15) / 16), dim3(256), 0, st, ops, T, B, ptr, (int32_t*)(ws + L.dep), ctl);
-  uint32_t hs[2] = {0, 0};
-  if (hipMemcpyAsync(hs, ctl + CTL_STATUS, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
+  uint32_t hs[CTL_NPUSHF + 1] = {};
+  if (hipMemcpyAsync(hs, ctl + CTL_STATUS, sizeof(hs), hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
   if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
   if (hs[0] != 0x7fffffffu) return (int)(hs[0] & 7u);
+  {
+    std::lock_guard<std::mutex> lk(push_mutex());
+    if (push_counts().size() > 4096) push_counts().clear();   // bounded: work spaces are reused in practice
+    push_counts()[workspace] = PushCount{T, B, hs[CTL_NPUSHF]};
+  }
   // the wide and the pipelined forward read a finished producer trace (they keep no integer
   // stack of their own); the plain forward traces in-kernel
   const bool pretrace = p.wide || p.pipe;
@@ -549,6 +573,67 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   } else {
     hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0, prow, npush,
                        (float*)hp, T, B, H);
+  }
+  // fp32 with the push count known on the host (recorded by the forward on this work space):
+  // the three gradient GEMMs on rocBLAS over compacted push rows
+  uint32_t np_host = 0;
+  {
+    std::lock_guard<std::mutex> lk(push_mutex());
+    auto it = push_counts().find(workspace);
+    if (it != push_counts().end() && it->second.T == T && it->second.B == B && it->second.n <= (uint32_t)K)
+      np_host = it->second.n;
+  }
+  if (!bf && np_host > 0) {
+    float* dac = (float*)(ws + L.dac);
+    float* xc = (float*)(ws + L.xc);
+    const int np = (int)np_host;
+    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * H4 / 4)), dim3(256), 0, st, (const float*)a.dA, prow,
+                       npush, (size_t)K, H4, 0, dac);
+    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * I / 4 + 1)), dim3(256), 0, st, x, prow, npush,
+                       (size_t)K, I, 0, xc);
+    if ((rc = hip_status(hipGetLastError()))) return rc;
+    const float one = 1.f, zero = 0.f;
+    {
+      std::lock_guard<std::mutex> lk(blas_mutex());
+      rocblas_handle h = blas_handle();
+      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      // column-major views: dWp^T [4H x I] = dA_c^T [4H x np] . x_c [np x I]
+      if (rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, H4, I, np, &one, dac, H4, xc, I, &zero,
+                        part, H4) != rocblas_status_success)
+        return SLSTM_EDEVICE;
+    }
+    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, 1, (size_t)I * H4, I, H4,
+                       H, dW);
+    mark(d, 7, st);
+    {
+      std::lock_guard<std::mutex> lk(blas_mutex());
+      rocblas_handle h = blas_handle();
+      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      // dUp^T [4H x H] = dA_c^T [4H x np] . Hprev_c [np x H]
+      if (rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, H4, H, np, &one, dac, H4,
+                        (const float*)hp, H, &zero, part, H4) != rocblas_status_success)
+        return SLSTM_EDEVICE;
+    }
+    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, 1, (size_t)H * H4, H, H4,
+                       H, dU);
+    mark(d, 8, st);
+    {
+      std::lock_guard<std::mutex> lk(blas_mutex());
+      rocblas_handle h = blas_handle();
+      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      // dx_c^T [I x np] = Wp [I x 4H] . dA_c^T [4H x np]   (Wp rows are the first I of [Wp ; b])
+      if (rocblas_sgemm(h, rocblas_operation_transpose, rocblas_operation_none, I, np, H4, &one, (const float*)(ws + L.wp),
+                        H4, dac, H4, &zero, xc, I) != rocblas_status_success)
+        return SLSTM_EDEVICE;
+    }
+    hipLaunchKernelGGL(k_zero_nonpush_rows, dim3(grid1d((size_t)K * I / 4 + 1)), dim3(256), 0, st, ops, dx, (size_t)K,
+                       I);
+    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * I / 4 + 1)), dim3(256), 0, st, (const float*)xc, prow,
+                       npush, (size_t)K, I, 1, dx);
+    if ((rc = hip_status(hipGetLastError()))) return rc;
+    mark(d, 9, st);
+    if (d->spin_limit > 0) return check_timeout(ctl, st);
+    return SLSTM_OK;
   }
   gemm_base();
   g.M = I; g.N = H4; g.dyn_axis = 1;

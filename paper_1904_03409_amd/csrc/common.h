@@ -21,6 +21,7 @@ enum {
   CTL_ABORT = 2,         // set when a group barrier ran out of spins
   CTL_TIMEOUT = 3,
   CTL_NPUSH = 4,         // number of push rows (written by k_push_rows in the backward)
+  CTL_NPUSHF = 5,        // number of push rows (counted by k_scan in the forward, read back by the host)
   CTL_XCC_SLOT = 16,     // 16 per-XCC slot counters (forward kernel)
   CTL_XCC_SLOT_B = 32,   // 16 per-XCC slot counters (backward kernel)
   CTL_BAR_F = 64,        // forward group barrier counters, one 64-byte line per group

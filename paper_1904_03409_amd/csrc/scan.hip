@@ -36,16 +36,18 @@ __global__ void __launch_bounds__(256) k_scan(const int8_t* __restrict__ ops, in
   int first_bad = 0x7fffffff, first_uf = 0x7fffffff, maxd = 0;
   if (b < B) {
     if (seg == 0) ptr[b] = 0;
-    int p = off;
+    int p = off, npush = 0;
     for (int t = t0; t < t1; ++t) {
       int op = ops[(size_t)t * B + b];
       if (op < -1 || op > 1) { if (first_bad == 0x7fffffff) first_bad = t; op = 0; }
+      npush += op == 1;
       p += op;
       if (p < 0 && first_uf == 0x7fffffff) first_uf = t;
       ptr[(size_t)(t + 1) * B + b] = p;
       maxd = max(maxd, p);
     }
     if (t1 == T && t0 < t1) depth_end[b] = p;      // the pointer after the last step
+    if (npush) atomicAdd(&ctl[CTL_NPUSHF], (uint32_t)npush);
     atomicMin(&s_first_bad[c], first_bad);
     atomicMin(&s_first_uf[c], first_uf);
     atomicMax(&s_maxd, maxd);
@@ -317,6 +319,34 @@ __global__ void __launch_bounds__(256) k_gather_hprev(const int32_t* __restrict_
     int s = (t == 0) ? -1 : top[tb - B];
     if (s < -1 || s >= t) s = -1;                 // only a valid producer is ever indexed
     out[i] = (s < 0) ? h0[(size_t)b * H + u] : hcell[((size_t)s * B + b) * H + u];
+  }
+}
+
+// Row gather / scatter over the push rows (k < *count): dst[k] = src[prow[k]] and
+// dst[prow[k]] = src[k], rows of `cols` floats (four at a time when cols % 4 == 0).
+__global__ void __launch_bounds__(256) k_gather_rows(const float* __restrict__ src, const int32_t* __restrict__ prow,
+                                                     const uint32_t* __restrict__ count, size_t max_rows, int cols,
+                                                     int scatter, float* __restrict__ dst) {
+  const size_t rows = min((size_t)*count, max_rows);
+  if (cols % 4 == 0) {
+    const int c4 = cols / 4;
+    const size_t n = rows * c4;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+      const size_t k = i / c4;
+      const int c = (int)(i - k * c4);
+      const size_t r = (size_t)prow[k];
+      if (scatter) ((float4*)dst)[r * c4 + c] = ((const float4*)src)[i];
+      else ((float4*)dst)[i] = ((const float4*)src)[r * c4 + c];
+    }
+  } else {
+    const size_t n = rows * cols;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+      const size_t k = i / cols;
+      const int c = (int)(i - k * cols);
+      const size_t r = (size_t)prow[k];
+      if (scatter) dst[r * cols + c] = src[i];
+      else dst[i] = src[r * cols + c];
+    }
   }
 }
 

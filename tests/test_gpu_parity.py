@@ -148,3 +148,33 @@ def test_wide_forward_streams(oracle_mod, kind):
     T, B = 48, 24
     wl = wk.custom(T=T, B=B, I=16, H=640, seed=4, ops=_streams(kind, T, B, rng), wscale=0.2, random_state=True)
     _check(oracle_mod, wl, 1)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", ["parser", "large"])
+def test_bwd_without_recorded_push_count(name):
+    """The fp32 backward runs its gradient GEMMs on the vendor BLAS when the forward recorded
+    the push count for the work space, and on the library's own device-count kernels
+    otherwise. A backward on a copy of the work space (no recorded count) must give the same
+    gradients as the backward on the original, to fp32 rounding of the two contraction orders."""
+    need_gpu()
+    import torch
+    from paper_1904_03409_amd.stacklstm import DeviceRun, stacklstm_bwd
+    wl = wk.make(name)
+    r = DeviceRun.from_workload(wl, precision=0)
+    r.forward()
+    ws_copy = r.workspace.clone()
+    r.backward()
+    torch.cuda.synchronize()
+    ref = {k: getattr(r, k).clone() for k in ("dx", "dW", "dU", "db", "dh0", "dc0")}
+    for k in ref:
+        getattr(r, k).zero_()
+    stacklstm_bwd(r.dims, r.x, r.ops, r.W, r.U, r.h0, r.c0, r.h_cell, r.c_cell, r.top, ws_copy, r.dh_top, r.dc_top,
+                  r.dx, r.dW, r.dU, r.db, r.dh0, r.dc0)
+    torch.cuda.synchronize()
+    for k, v in ref.items():
+        got = getattr(r, k)
+        scale = float(v.abs().max()) or 1.0
+        err = float((got - v).abs().max()) / scale
+        assert err < 1e-4, (k, err)
+    assert torch.equal(r.db, ref["db"]) and torch.equal(r.dh0, ref["dh0"]) and torch.equal(r.dc0, ref["dc0"])
