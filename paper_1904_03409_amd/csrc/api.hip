@@ -255,7 +255,7 @@ Layout layout(const slstm_dims* d) {
   L.dep = o; o += align256(B * 4);                                     // pointer after the last step
   // fp32 post-loop operands on the vendor BLAS: dA and x rows of the push steps, compacted
   L.dac = o; o += bf ? 0 : align256(std::max<size_t>(T * B * 4 * H * 4, 16));
-  L.xc = o; o += bf ? 0 : align256(std::max<size_t>(T * B * std::max(I, (size_t)1) * 4, 16));
+  L.xc = o; o += align256(std::max<size_t>(T * B * std::max(I, (size_t)1) * 4, 16));   // also dx rows in bf16 mode
   L.total = o;
   return L;
 }
@@ -582,6 +582,51 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     auto it = push_counts().find(workspace);
     if (it != push_counts().end() && it->second.T == T && it->second.B == B && it->second.n <= (uint32_t)K)
       np_host = it->second.n;
+  }
+  if (bf && np_host > 0) {
+    // bf16 operands are already compacted and transposed: xbt [I][KP], dat [4H][KP] (push index
+    // contiguous, zero past the count); dx on rocBLAS, dW and dU on the library's kernel (faster
+    // than the vendor BLAS on these transposed operands, measured at large)
+    const int np = (int)np_host;
+    float* xc = (float*)(ws + L.xc);
+    const float one = 1.f, zero = 0.f;
+    gemm_base();
+    g.M = I; g.N = H4; g.dyn_axis = 1;
+    g.K = KP; g.A = ws + L.xbt; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1;
+    g.C = part; g.ldc = H4;
+    g.split_stride = (size_t)I * H4;
+    if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, p.splits_w, st))) return rc;
+    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, p.splits_w,
+                       g.split_stride, I, H4, H, dW);
+    mark(d, 7, st);
+    gemm_base();
+    g.M = H; g.N = H4; g.dyn_axis = 1;
+    g.K = KP; g.A = hp; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1;
+    g.C = part; g.ldc = H4;
+    g.split_stride = (size_t)H * H4;
+    if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, p.splits_u, st))) return rc;
+    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, p.splits_u,
+                       g.split_stride, H, H4, H, dU);
+    mark(d, 8, st);
+    {
+      std::lock_guard<std::mutex> lk(blas_mutex());
+      rocblas_handle h = blas_handle();
+      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      // dx_c^T [I x np] = Wp [I x 4H] . dat [4H x np]   (Wp rows are the first I of [Wp ; b])
+      if (rocblas_gemm_ex(h, rocblas_operation_transpose, rocblas_operation_transpose, I, np, H4, &one, ws + L.wp,
+                          rocblas_datatype_bf16_r, H4, ws + L.dat, rocblas_datatype_bf16_r, KP, &zero, xc,
+                          rocblas_datatype_f32_r, I, xc, rocblas_datatype_f32_r, I, rocblas_datatype_f32_r,
+                          rocblas_gemm_algo_standard, 0, 0) != rocblas_status_success)
+        return SLSTM_EDEVICE;
+    }
+    hipLaunchKernelGGL(k_zero_nonpush_rows, dim3(grid1d((size_t)K * I / 4 + 1)), dim3(256), 0, st, ops, dx, (size_t)K,
+                       I);
+    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * I / 4 + 1)), dim3(256), 0, st, (const float*)xc, prow,
+                       npush, (size_t)K, I, 1, dx);
+    if ((rc = hip_status(hipGetLastError()))) return rc;
+    mark(d, 9, st);
+    if (d->spin_limit > 0) return check_timeout(ctl, st);
+    return SLSTM_OK;
   }
   if (!bf && np_host > 0) {
     float* dac = (float*)(ws + L.dac);

@@ -151,17 +151,18 @@ def test_wide_forward_streams(oracle_mod, kind):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("name", ["parser", "large"])
-def test_bwd_without_recorded_push_count(name):
-    """The fp32 backward runs its gradient GEMMs on the vendor BLAS when the forward recorded
-    the push count for the work space, and on the library's own device-count kernels
-    otherwise. A backward on a copy of the work space (no recorded count) must give the same
-    gradients as the backward on the original, to fp32 rounding of the two contraction orders."""
+@pytest.mark.parametrize("name,precision", [("parser", 0), ("large", 0), ("parser", 1), ("large", 1)])
+def test_bwd_without_recorded_push_count(name, precision):
+    """The backward runs its gradient GEMMs on the vendor BLAS when the forward recorded the
+    push count for the work space, and on the library's own device-count kernels otherwise.
+    A backward on a copy of the work space (no recorded count) must give the same gradients
+    as the backward on the original, to rounding of the two contraction orders (fp32
+    accumulation in both modes; in bf16 mode the split-K partial sums differ in order)."""
     need_gpu()
     import torch
     from paper_1904_03409_amd.stacklstm import DeviceRun, stacklstm_bwd
     wl = wk.make(name)
-    r = DeviceRun.from_workload(wl, precision=0)
+    r = DeviceRun.from_workload(wl, precision=precision)
     r.forward()
     ws_copy = r.workspace.clone()
     r.backward()
@@ -176,5 +177,5 @@ def test_bwd_without_recorded_push_count(name):
         got = getattr(r, k)
         scale = float(v.abs().max()) or 1.0
         err = float((got - v).abs().max()) / scale
-        assert err < 1e-4, (k, err)
+        assert err < (1e-4 if precision == 0 else 2e-3), (k, err)
     assert torch.equal(r.db, ref["db"]) and torch.equal(r.dh0, ref["dh0"]) and torch.equal(r.dc0, ref["dc0"])
