@@ -91,10 +91,18 @@ typedef struct {
 
 /* Bytes of device work space that stacklstm_fwd / stacklstm_bwd need for `d`
  * (0 for invalid dims). The work space carries the forward's gate activations and
- * stack to the backward; pass the same buffer, untouched, to both calls. */
+ * stack to the backward; pass the same buffer, untouched, to both calls. The forward
+ * also records, in the library (host side, keyed by the work space's address), the
+ * number of push steps it validated; a backward on that work space uses it to run its
+ * gradient contractions on rocBLAS over the compacted push rows, and a backward on a
+ * work space without such a record runs the same contractions on the library's own
+ * kernels (same results up to fp32 rounding of the summation order). */
 size_t stacklstm_workspace_bytes(const slstm_dims* d);
 
-/* Forward over T steps (Algorithm 1 for every element and step).
+/* Forward over T steps (Algorithm 1 for every element and step). The input projection
+ * x_t W + b of all steps runs as one rocBLAS GEMM; everything else runs in the
+ * library's kernels. */
+/* Forward over T steps, arguments:
  *  x      [T, B, I]   inputs x_t                                 (read)
  *  ops    [T, B]      int8 ops, +1 push / -1 pop / 0 hold         (read)
  *  W [I, 4H], U [H, 4H], b [4H], h0 [B, H], c0 [B, H]             (read)
