@@ -101,8 +101,7 @@ size_t stacklstm_workspace_bytes(const slstm_dims* d);
 
 /* Forward over T steps (Algorithm 1 for every element and step). The input projection
  * x_t W + b of all steps runs as one rocBLAS GEMM; everything else runs in the
- * library's kernels. */
-/* Forward over T steps, arguments:
+ * library's kernels.
  *  x      [T, B, I]   inputs x_t                                 (read)
  *  ops    [T, B]      int8 ops, +1 push / -1 pop / 0 hold         (read)
  *  W [I, 4H], U [H, 4H], b [4H], h0 [B, H], c0 [B, H]             (read)
