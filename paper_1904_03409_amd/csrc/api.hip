@@ -25,6 +25,7 @@ __global__ void k_gather_top4(const int32_t* top, const float* hcell, const floa
 __global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
+__global__ void k_zero_ctl_bwd(uint32_t* ctl);
 __global__ void k_fill_pattern(unsigned char* p, size_t bytes, uint32_t v);
 __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
@@ -518,9 +519,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   }
 
   // a8: persistent reverse loop
-  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_XCC_SLOT_B, 16);
-  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_BAR_B, 16 * MAX_GROUPS);
-  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, ctl + CTL_ABORT, 2);
+  hipLaunchKernelGGL(k_zero_ctl_bwd, dim3(1), dim3(256), 0, st, ctl);
   RecArgs a = rec_args(d, p, ws, L, true);
   a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0;
   a.hcell = const_cast<float*>(h_cell); a.ccell = const_cast<float*>(c_cell); a.top = const_cast<int32_t*>(top);

@@ -197,10 +197,44 @@ __global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ in, b
     out[i] = f32_to_bf16_bits(in[i]);
 }
 
+// Clears the backward's control words: slot counters, group barrier counters, abort flags.
+__global__ void __launch_bounds__(256) k_zero_ctl_bwd(uint32_t* __restrict__ ctl) {
+  for (int i = threadIdx.x; i < 16; i += blockDim.x) ctl[CTL_XCC_SLOT_B + i] = 0u;
+  for (int i = threadIdx.x; i < 16 * MAX_GROUPS; i += blockDim.x) ctl[CTL_BAR_B + i] = 0u;
+  if (threadIdx.x < 2) ctl[CTL_ABORT + threadIdx.x] = 0u;
+}
+
 // Operand of the input-projection GEMM: out [rows][KA] = [x | nones columns of 1 | 0], in
 // fp32 (out32) or bf16 (out16, x rounded as k_to_bf16 does).
 __global__ void __launch_bounds__(256) k_augment_x(const float* __restrict__ x, size_t rows, int I, int KA, int nones,
                                                    float* __restrict__ out32, bf16_t* __restrict__ out16) {
+  // eight output columns per thread when I and KA are multiples of 8 and x is 16-byte aligned
+  if (I % 8 == 0 && KA % 8 == 0 && ((uintptr_t)x & 15u) == 0) {
+    const int K8 = KA / 8;
+    const size_t n8 = rows * (size_t)K8;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (size_t)gridDim.x * blockDim.x) {
+      const size_t r = i / (size_t)K8;
+      const int c = (int)(i - r * (size_t)K8) * 8;
+      float v[8];
+      if (c < I) {
+        const float4 a = *(const float4*)(x + r * (size_t)I + c), b = *(const float4*)(x + r * (size_t)I + c + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (c + j < I + nones) ? 1.f : 0.f;
+      }
+      if (out32) {
+        *(float4*)(out32 + r * (size_t)KA + c) = float4{v[0], v[1], v[2], v[3]};
+        *(float4*)(out32 + r * (size_t)KA + c + 4) = float4{v[4], v[5], v[6], v[7]};
+      } else {
+        bf16_t q[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) q[j] = f32_to_bf16_bits(v[j]);
+        *(uint4*)(out16 + r * (size_t)KA + c) = *(const uint4*)q;
+      }
+    }
+    return;
+  }
   const size_t n = rows * (size_t)KA;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     const size_t r = i / (size_t)KA;
@@ -253,9 +287,19 @@ __global__ void __launch_bounds__(1024) k_push_rows(const int8_t* __restrict__ o
   int base = 0;
   for (int t0 = 0; t0 < n; t0 += TILE) {
     const int len = min(TILE, n - t0);
-    for (int i = tid; i < TILE; i += 1024) s_ops[i] = i < len ? ops[(size_t)t0 + i] : (int8_t)0;
-    __syncthreads();
-    const uint4 q0 = *(const uint4*)&s_ops[tid * PER], q1 = *(const uint4*)&s_ops[tid * PER + 16];
+    // each thread reads its own 32 ops: two 16-byte loads when they are all in range and the
+    // array is 16-byte aligned, else bytes through LDS
+    uint4 q0, q1;
+    const bool vec = ((uintptr_t)ops & 15u) == 0 && tid * PER + PER <= len;
+    if (!vec)
+      for (int i = 0; i < PER; ++i) s_ops[tid * PER + i] = tid * PER + i < len ? ops[(size_t)t0 + tid * PER + i] : (int8_t)0;
+    if (vec) {
+      q0 = *(const uint4*)(ops + (size_t)t0 + tid * PER);
+      q1 = *(const uint4*)(ops + (size_t)t0 + tid * PER + 16);
+    } else {
+      q0 = *(const uint4*)&s_ops[tid * PER];
+      q1 = *(const uint4*)&s_ops[tid * PER + 16];
+    }
     const uint32_t w[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
     uint32_t mask = 0;                               // bit j: op j of this thread is a push
 #pragma unroll
