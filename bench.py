@@ -293,7 +293,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the StackLSTM step is measured on one MI355X "
-              "(batch sharding across GPUs is described in DESIGN.md, not launched)", file=sys.stderr)
+              "(the batch would shard across GPUs with one all-reduce of dW, dU, db after the backward; that path is not launched)", file=sys.stderr)
         sys.exit(2)
 
     import torch
