@@ -307,12 +307,15 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   a.stash = (float*)(ws + L.stash);
   a.hx = d->precision == SLSTM_BF16_GEMM ? (uint16_t*)(ws + L.hx) : nullptr;
   a.clk = (long long*)d->step_clock;
-  // Exchange protocol (measured on the large parser workload): in bf16 mode a step is short
-  // and a group barrier's fixed cost (store acknowledgement, then an atomic and a poll round
-  // trip) dominates it, so the workgroups poll the fill-marked rows instead; in fp32 mode the
-  // rows are twice as long, checking a staged tile for the fill pattern costs more than the
-  // barrier, and the backward's fill of dA is a large write, so fp32 keeps the barrier.
-  a.poll = d->precision == SLSTM_BF16_GEMM ? 1 : 0;
+  // Exchange protocol (measured on the large parser workload): the bf16 forward's step is
+  // short and a group barrier's fixed cost (store acknowledgement, then an atomic and a poll
+  // round trip) dominates it, so its workgroups poll the fill-marked rows instead; the fp32
+  // forward's rows are twice as long and checking a staged tile for the fill pattern costs
+  // more than the barrier. The backward uses the barrier in both precisions: it stores and
+  // exchanges only push rows, its barrier's arrival overlaps the row-offset set-up, and a
+  // fill of dA before it would be a large write (bf16 large: 1.24 ms with the barrier,
+  // 1.32 ms polling).
+  a.poll = (d->precision == SLSTM_BF16_GEMM && !bwd) ? 1 : 0;
   // the pipelined forward has no barrier: it always polls
   if (!bwd && p.pipe) a.poll = 1;
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
