@@ -181,9 +181,10 @@ int make_plan(const slstm_dims* d, Plan* p) {
 // The input projection XW = x Wp + b is one plain GEMM on the vendor BLAS: x gets columns of
 // ones (one in fp32 mode; three in bf16 mode, where b is carried as the sum of three bf16
 // parts, so the bias keeps fp32 precision) and Wp gets the matching bias rows; K is padded
-// to a multiple of 8 with zeros.
+// to a multiple of 32 with zeros (the vendor GEMM picks faster tiles for such K: measured
+// 0.12 ms against 0.15 ms in bf16 at T*B = 61440, 4H = 2048, I = 256).
 int xw_ones(const slstm_dims* d) { return d->precision == SLSTM_BF16_GEMM ? 3 : 1; }
-size_t xw_k(const slstm_dims* d) { return ((size_t)d->I + xw_ones(d) + 7) / 8 * 8; }
+size_t xw_k(const slstm_dims* d) { return ((size_t)d->I + xw_ones(d) + 31) / 32 * 32; }
 
 // One rocBLAS handle per device, created on first use; calls that share it are serialised
 // (the handle's stream is set per call).
