@@ -186,8 +186,10 @@ int make_plan(const slstm_dims* d, Plan* p) {
 int xw_ones(const slstm_dims* d) { return d->precision == SLSTM_BF16_GEMM ? 3 : 1; }
 size_t xw_k(const slstm_dims* d) { return ((size_t)d->I + xw_ones(d) + 31) / 32 * 32; }
 
-// One rocBLAS handle per device, created on first use; calls that share it are serialised
-// (the handle's stream is set per call).
+// rocBLAS handles, one per (device, stream), created on first use with atomic
+// (order-dependent) kernels disabled, so a GEMM's result does not depend on what runs beside
+// it. A handle owns a device work space that its split-K GEMMs write, so GEMMs that run at
+// once on two streams need two handles. Calls are serialised under blas_mutex().
 std::mutex& blas_mutex() {
   static std::mutex mu;
   return mu;
@@ -209,12 +211,32 @@ SideStream* side_stream() {
   }
   return &x;
 }
-rocblas_handle blas_handle() {
-  static rocblas_handle h[64] = {};
+// At most kBlasHandles handles per device: past that the device is drained and its handles
+// are released before a new one is made (the streams of earlier calls may be gone).
+constexpr int kBlasHandles = 32;
+rocblas_handle blas_handle(hipStream_t st) {
+  struct Entry { hipStream_t st; rocblas_handle h; };
+  static Entry tab[64][kBlasHandles] = {};
+  static int used[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  if (!h[dev] && rocblas_create_handle(&h[dev]) != rocblas_status_success) h[dev] = nullptr;
-  return h[dev];
+  Entry* e = tab[dev];
+  for (int i = 0; i < used[dev]; ++i)
+    if (e[i].st == st) return e[i].h;
+  if (used[dev] == kBlasHandles) {
+    if (hipDeviceSynchronize() != hipSuccess) return nullptr;
+    for (int i = 0; i < used[dev]; ++i) rocblas_destroy_handle(e[i].h);
+    used[dev] = 0;
+  }
+  rocblas_handle h = nullptr;
+  if (rocblas_create_handle(&h) != rocblas_status_success) return nullptr;
+  if (rocblas_set_atomics_mode(h, rocblas_atomics_not_allowed) != rocblas_status_success ||
+      rocblas_set_stream(h, st) != rocblas_status_success) {
+    rocblas_destroy_handle(h);
+    return nullptr;
+  }
+  e[used[dev]++] = Entry{st, h};
+  return h;
 }
 
 // Number of push rows per work space, read back with the forward's status: the backward's
@@ -433,8 +455,8 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                          side->s, ops, T, B, trace_cap, top);
       if (hipEventRecord(side->join, side->s) != hipSuccess) return SLSTM_EDEVICE;
     }
-    rocblas_handle h = blas_handle();
-    if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+    rocblas_handle h = blas_handle(st);
+    if (!h) return SLSTM_EDEVICE;
     const float one = 1.f, zero = 0.f;
     rocblas_status bs;
     if (!bf)
@@ -613,8 +635,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     mark(d, 8, st);
     {
       std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle();
-      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      rocblas_handle h = blas_handle(st);
+      if (!h) return SLSTM_EDEVICE;
       // dx_c^T [I x np] = Wp [I x 4H] . dat [4H x np]   (Wp rows are the first I of [Wp ; b])
       if (rocblas_gemm_ex(h, rocblas_operation_transpose, rocblas_operation_transpose, I, np, H4, &one, ws + L.wp,
                           rocblas_datatype_bf16_r, H4, ws + L.dat, rocblas_datatype_bf16_r, KP, &zero, xc,
@@ -643,8 +665,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     const float one = 1.f, zero = 0.f;
     {
       std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle();
-      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      rocblas_handle h = blas_handle(st);
+      if (!h) return SLSTM_EDEVICE;
       // column-major views: dWp^T [4H x I] = dA_c^T [4H x np] . x_c [np x I]
       if (rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, H4, I, np, &one, dac, H4, xc, I, &zero,
                         part, H4) != rocblas_status_success)
@@ -655,8 +677,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     mark(d, 7, st);
     {
       std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle();
-      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      rocblas_handle h = blas_handle(st);
+      if (!h) return SLSTM_EDEVICE;
       // dUp^T [4H x H] = dA_c^T [4H x np] . Hprev_c [np x H]
       if (rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, H4, H, np, &one, dac, H4,
                         (const float*)hp, H, &zero, part, H4) != rocblas_status_success)
@@ -667,8 +689,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     mark(d, 8, st);
     {
       std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle();
-      if (!h || rocblas_set_stream(h, st) != rocblas_status_success) return SLSTM_EDEVICE;
+      rocblas_handle h = blas_handle(st);
+      if (!h) return SLSTM_EDEVICE;
       // dx_c^T [I x np] = Wp [I x 4H] . dA_c^T [4H x np]   (Wp rows are the first I of [Wp ; b])
       if (rocblas_sgemm(h, rocblas_operation_transpose, rocblas_operation_none, I, np, H4, &one, (const float*)(ws + L.wp),
                         H4, dac, H4, &zero, xc, I) != rocblas_status_success)

@@ -179,3 +179,51 @@ def test_bwd_without_recorded_push_count(name, precision):
         err = float((got - v).abs().max()) / scale
         assert err < (1e-4 if precision == 0 else 2e-3), (k, err)
     assert torch.equal(r.db, ref["db"]) and torch.equal(r.dh0, ref["dh0"]) and torch.equal(r.dc0, ref["dc0"])
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("threaded", [False, True])
+def test_concurrent_calls_on_two_streams(threaded):
+    """Two independent problems run fwd + bwd on two HIP streams at once (interleaved from one
+    host thread, or from two host threads): the producer trace's side stream, the shared BLAS
+    handle and the per-work-space push counts must keep the calls apart, so every output is
+    bit-identical to the same problem run alone."""
+    need_gpu()
+    import threading
+    import torch
+    from paper_1904_03409_amd.stacklstm import DeviceRun
+    wls = [wk.make("large"), wk.make("large", seed=7)]
+    alone = []
+    for wl in wls:
+        r = DeviceRun.from_workload(wl, precision=0, want_top=True)
+        r.forward()
+        r.backward()
+        torch.cuda.synchronize()
+        alone.append(r.results())
+    runs = [DeviceRun.from_workload(wl, precision=0, want_top=True) for wl in wls]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    if threaded:
+        def work(i):
+            with torch.cuda.stream(streams[i]):
+                for _ in range(2):
+                    runs[i].forward(stream=streams[i])
+                    runs[i].backward(stream=streams[i])
+        th = [threading.Thread(target=work, args=(i,)) for i in range(2)]
+        for x in th:
+            x.start()
+        for x in th:
+            x.join()
+    else:
+        for _ in range(2):
+            for i in range(2):
+                with torch.cuda.stream(streams[i]):
+                    runs[i].forward(stream=streams[i])
+            for i in range(2):
+                with torch.cuda.stream(streams[i]):
+                    runs[i].backward(stream=streams[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        got = runs[i].results()
+        for k, v in alone[i].items():
+            assert np.array_equal(got[k], v), (i, k)
