@@ -41,6 +41,12 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;
   constexpr int BG = NT * 16;
   constexpr int PAIRS = BG * 16 / 256;            // (row, unit) pairs per thread
+  // Two workgroups per CU (bf16, H = 1024) leave 256 registers per lane, half of them for
+  // the U slice: the lean variant keeps only the current step's row info per pair and
+  // loads each step's operands at the step (in batches of LB pairs) instead of a step ahead.
+  constexpr bool LEAN = OCC == 2;
+  constexpr int LB = PAIRS < 4 ? PAIRS : 4;
+  static_assert(PAIRS % LB == 0, "whole load batches");
   // staged dA rows (direct path): per wave 16 compacted rows of its H gate columns
   constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
   extern __shared__ __align__(16) unsigned char dsm[];
@@ -156,6 +162,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // operands of step t-1 and row info of step t-2; the spill slot a push at step t-1 reads
   // (depth dep-1 after this step's update)
   auto prefetch = [&](int t) {
+    if constexpr (LEAN) return;
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
       const int b = pok[i] ? row0 + prow[i] : 0;
@@ -173,10 +180,12 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     const int b = pok[i] ? row0 + prow[i] : 0;
     ld_row(T - 1, b, c_op[i], c_sp[i]);
     valid_sp(T - 1, c_sp[i]);
-    ld_ops(T - 1, b, c_op[i], c_sp[i], c_gh[i], c_gc[i], c_act[i], c_c[i], c_cp[i]);
-    if (T > 1) {
-      ld_row(T - 2, b, n_op[i], n_sp[i]);
-      valid_sp(T - 2, n_sp[i]);
+    if constexpr (!LEAN) {
+      ld_ops(T - 1, b, c_op[i], c_sp[i], c_gh[i], c_gc[i], c_act[i], c_c[i], c_cp[i]);
+      if (T > 1) {
+        ld_row(T - 2, b, n_op[i], n_sp[i]);
+        valid_sp(T - 2, n_sp[i]);
+      }
     }
     gh[i] = gc[i] = lh[i] = lc[i] = 0.f;
     ld[i] = -1;
@@ -211,30 +220,53 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     }
 
     // ---- cell backward for this workgroup's (row, unit) pairs
+    // lean variant: the operands of LB pairs (and the spill slot a push reads) are loaded
+    // together, then used
+    float e_gh[LEAN ? LB : 1], e_gc[LEAN ? LB : 1], e_c[LEAN ? LB : 1], e_cp[LEAN ? LB : 1];
+    float e_ph[LEAN ? LB : 1], e_pc[LEAN ? LB : 1];
+    float4 e_act[LEAN ? LB : 1];
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
+      if constexpr (LEAN) {
+        if (i % LB == 0) {
+#pragma unroll
+          for (int j = 0; j < LB; ++j) {
+            const int ii = i + j;
+            const int bl = pok[ii] ? row0 + prow[ii] : 0;
+            ld_ops(t, bl, c_op[ii], c_sp[ii], e_gh[j], e_gc[j], e_act[j], e_c[j], e_cp[j]);
+            const size_t so = ((size_t)max(dep[ii] - 1, 0) * B + bl) * H + ul;
+            e_ph[j] = a.dh_acc[so];
+            e_pc[j] = a.dc_acc[so];
+          }
+        }
+      }
+      const int j = LEAN ? i % LB : 0;
+      const float o_gh = LEAN ? e_gh[j] : c_gh[i], o_gc = LEAN ? e_gc[j] : c_gc[i];
+      const float o_c = LEAN ? e_c[j] : c_c[i], o_cp = LEAN ? e_cp[j] : c_cp[i];
+      const float4 o_act = LEAN ? e_act[j] : c_act[i];
       float4 dA4 = float4{0.f, 0.f, 0.f, 0.f};
       const int b = row0 + prow[i];
       // dh_top[t], dc_top[t] belong to the state at the top after step t
-      gh[i] += c_gh[i];
-      gc[i] += c_gc[i];
+      gh[i] += o_gh;
+      gc[i] += o_gc;
       if (c_op[i] == 1) {
         // the state produced at step t: its whole gradient is (gh, gc)
-        const float4 act = c_act[i];
+        const float4 act = o_act;
         const float dh = gh[i];
-        const float tc = tanhf_(c_c[i]);
+        const float tc = tanhf_(o_c);
         const float dc = gc[i] + dh * act.w * (1.f - tc * tc);
         // never the all-ones fill pattern: a NaN is stored as the canonical quiet NaN
         dA4.x = canon_nan(dc * act.z * act.x * (1.f - act.x));
-        dA4.y = canon_nan(dc * c_cp[i] * act.y * (1.f - act.y));
+        dA4.y = canon_nan(dc * o_cp * act.y * (1.f - act.y));
         dA4.z = canon_nan(dc * act.x * (1.f - act.z * act.z));
         dA4.w = canon_nan(dh * tc * act.w * (1.f - act.w));
         if (pok[i]) { dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w; }
         // the parent (depth dep-1) comes back to the top with its spilled gradient (the last
         // spill if it was to that depth, else the prefetched slot) plus dc f; dA U^T follows
         const bool fwd = ld[i] == dep[i] - 1;
-        gh[i] = fwd ? lh[i] : ph[i];
-        gc[i] = (fwd ? lc[i] : pc[i]) + dc * act.y;
+        const float sh = LEAN ? e_ph[j] : ph[i], sc = LEAN ? e_pc[j] : pc[i];
+        gh[i] = fwd ? lh[i] : sh;
+        gc[i] = (fwd ? lc[i] : sc) + dc * act.y;
         dep[i] -= 1;
       } else if (c_op[i] == -1) {
         // the popped state comes back: the state below is spilled, the popped one starts at 0
@@ -284,12 +316,14 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // chunks ahead, through the bounds-checked descriptor (a lane past the list or k past H
     // gets an out-of-range offset: value 0, no memory access). Two accumulators per tile
     // keep two independent MFMA chains.
-    constexpr int CG = 8;
+    constexpr int CG = LEAN ? 4 : 8;
     constexpr int NG = (KS + CG - 1) / CG;
     const int nlive = s_nlive;
     if (!direct || nlive == 0) prefetch(t);
-    // whole 1 KB row segments, at most two per staged row (H of at most 512 fp32 / 1024 bf16)
-    constexpr bool kDirectOk = (KS * KC * ESZ) % 1024 == 0 && KS * KC * ESZ / 1024 <= 2;
+    // whole 1 KB row segments, at most two per staged row (H of at most 512 fp32 / 1024 bf16);
+    // not at two workgroups per CU, where the staged rows do not fit beside the other
+    // workgroup's LDS (the host then never asks for it)
+    constexpr bool kDirectOk = (KS * KC * ESZ) % 1024 == 0 && KS * KC * ESZ / 1024 <= 2 && !LEAN;
     if (kDirectOk && direct) {
      if constexpr (kDirectOk) {
       // Each wave copies its own H gate columns of the compacted rows straight into its LDS
@@ -543,6 +577,13 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // rotate: step t-1 becomes current
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
+      if constexpr (LEAN) {
+        if (t > 0) {
+          ld_row(t - 1, pok[i] ? row0 + prow[i] : 0, c_op[i], c_sp[i]);
+          valid_sp(t - 1, c_sp[i]);
+        }
+        continue;
+      }
       c_op[i] = n_op[i]; c_sp[i] = n_sp[i];
       n_op[i] = nn_op[i]; n_sp[i] = nn_sp[i];
       if (t > 2) valid_sp(t - 2, n_sp[i]);
