@@ -45,7 +45,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // the U slice: the lean variant keeps only the current step's row info per pair and
   // loads each step's operands at the step (in batches of LB pairs) instead of a step ahead.
   constexpr bool LEAN = OCC == 2;
-  constexpr int LB = PAIRS < 4 ? PAIRS : 4;
+  constexpr int LB = PAIRS < 8 ? PAIRS : 8;
   static_assert(PAIRS % LB == 0, "whole load batches");
   // staged dA rows (direct path): per wave 16 compacted rows of its H gate columns
   constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
@@ -316,7 +316,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // chunks ahead, through the bounds-checked descriptor (a lane past the list or k past H
     // gets an out-of-range offset: value 0, no memory access). Two accumulators per tile
     // keep two independent MFMA chains.
-    constexpr int CG = LEAN ? 4 : 8;
+    constexpr int CG = LEAN ? 2 : 8;                // lean: measured fastest (fewer spills)
     constexpr int NG = (KS + CG - 1) / CG;
     const int nlive = s_nlive;
     if (!direct || nlive == 0) prefetch(t);
