@@ -227,3 +227,28 @@ def test_concurrent_calls_on_two_streams(threaded):
         got = runs[i].results()
         for k, v in alone[i].items():
             assert np.array_equal(got[k], v), (i, k)
+
+
+@pytest.mark.gpu
+def test_many_streams_blas_handles():
+    """Calls on more streams than the library keeps BLAS handles for (32 per device): past
+    that it drains the device and starts again, and every call still gives the same outputs
+    as the first, bit for bit."""
+    need_gpu()
+    import torch
+    from paper_1904_03409_amd.stacklstm import DeviceRun
+    wl = wk.make("parser")
+    r = DeviceRun.from_workload(wl, precision=0, want_top=True)
+    r.forward()
+    r.backward()
+    torch.cuda.synchronize()
+    ref = r.results()
+    streams = [torch.cuda.Stream() for _ in range(40)]
+    for i, s in enumerate(streams):
+        with torch.cuda.stream(s):
+            r.forward(stream=s)
+            r.backward(stream=s)
+        s.synchronize()
+        got = r.results()
+        for k, v in ref.items():
+            assert np.array_equal(got[k], v), (i, k)
