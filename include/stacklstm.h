@@ -26,8 +26,12 @@
  *    calls synchronise at the end to report SLSTM_ETIMEOUT.
  *  - Gradient outputs are overwritten, not accumulated.
  *  - On an error status nothing further is launched; output contents are unspecified.
- *  - No exception crosses the ABI. The functions keep no mutable global state apart
- *    from cached device properties; calls on different work spaces may overlap.
+ *  - No exception crosses the ABI. Global state, kept for the process's lifetime and
+ *    guarded by mutexes: cached device properties, one side stream per device (for the
+ *    producer trace), rocBLAS handles per (device, stream) (at most 32 per device; past
+ *    that the device is synchronised and the handles are released), and the push count
+ *    per work space. Calls on different work spaces may overlap, on any streams and from
+ *    any host threads; their results do not depend on what runs beside them.
  *  - Supported sizes: T >= 0, B >= 1, I >= 1, 1 <= H <= 512 (SLSTM_FP32) or
  *    H <= 1024 (SLSTM_BF16_GEMM); B up to 8 groups of 128 rows per XCC pass
  *    (SLSTM_ENORESIDENT beyond what one launch can hold).

@@ -185,8 +185,8 @@ def test_bwd_without_recorded_push_count(name, precision):
 @pytest.mark.parametrize("threaded", [False, True])
 def test_concurrent_calls_on_two_streams(threaded):
     """Two independent problems run fwd + bwd on two HIP streams at once (interleaved from one
-    host thread, or from two host threads): the producer trace's side stream, the shared BLAS
-    handle and the per-work-space push counts must keep the calls apart, so every output is
+    host thread, or from two host threads): the producer trace's side stream, the per-stream BLAS
+    handles and the per-work-space push counts must keep the calls apart, so every output is
     bit-identical to the same problem run alone."""
     need_gpu()
     import threading
