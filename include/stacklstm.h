@@ -20,18 +20,20 @@
  * Conventions for every entry point:
  *  - All array arguments are DEVICE pointers, owned by the caller; the library keeps
  *    none of them after the call returns. Shapes are row-major, time-major.
- *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream), except
- *    that stacklstm_fwd reads back one status word after validating the ops (the only
- *    host synchronisation), and that a positive dims->spin_limit (debug) makes both
- *    calls synchronise at the end to report SLSTM_ETIMEOUT.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream) up to
+ *    one status read-back at the end of each call (the only host synchronisation): it
+ *    reports invalid ops, a wait that gave up (SLSTM_ETIMEOUT) and an index out of range
+ *    (SLSTM_EINDEX) for the kernels of that call.
  *  - Gradient outputs are overwritten, not accumulated.
- *  - On an error status nothing further is launched; output contents are unspecified.
- *  - No exception crosses the ABI. Global state, kept for the process's lifetime and
- *    guarded by mutexes: cached device properties, one side stream per device (for the
- *    producer trace), rocBLAS handles per (device, stream) (at most 32 per device; past
- *    that the device is synchronised and the handles are released), and the push count
- *    per work space. Calls on different work spaces may overlap, on any streams and from
- *    any host threads; their results do not depend on what runs beside them.
+ *  - An error found by the argument checks (EINVAL, EWORKSPACE, ENORESIDENT) launches
+ *    nothing. On an error found by the read-back the call's kernels have run; output
+ *    contents are then unspecified (an invalid op is walked as a hold so that every
+ *    index stays in range).
+ *  - No exception crosses the ABI. The only global state is the cached device
+ *    properties (multiprocessor count per device) and the kernels' launch attributes.
+ *    Calls on different work spaces may overlap, on any streams and from any host
+ *    threads; calls that share a work space must not overlap. Results do not depend on
+ *    what runs beside them.
  *  - Supported sizes: T >= 0, B >= 1, I >= 1, 1 <= H <= 512 (SLSTM_FP32) or
  *    H <= 1024 (SLSTM_BF16_GEMM); B up to 8 groups of 128 rows per XCC pass
  *    (SLSTM_ENORESIDENT beyond what one launch can hold).
@@ -54,8 +56,11 @@ typedef enum {
   SLSTM_EWORKSPACE = 4,    /* ws_bytes < stacklstm_workspace_bytes(dims) */
   SLSTM_ENORESIDENT = 5,   /* the persistent kernels cannot be made co-resident */
   SLSTM_EDEVICE = 6,       /* a HIP runtime error */
-  SLSTM_ETIMEOUT = 7       /* a wait for another workgroup's data exceeded dims->spin_limit
-                              failed polls */
+  SLSTM_ETIMEOUT = 7,      /* a wait for another workgroup's data exceeded its spin limit
+                              (dims->spin_limit failed polls, or the default limit) */
+  SLSTM_EINDEX = 8         /* a kernel read a producer index or reached a stack depth outside
+                              its valid range: the top or ops passed to stacklstm_bwd are not
+                              the forward's (or a read returned stale data) */
 } slstm_status;
 
 typedef enum {
@@ -71,11 +76,11 @@ typedef struct {
   int32_t I;               /* input size */
   int32_t H;               /* hidden size */
   int32_t precision;       /* slstm_precision */
-  int32_t spin_limit;      /* 0 = default limit of failed polls per wait; > 0 = debug limit +
-                              final sync */
+  int32_t spin_limit;      /* failed polls per wait before the kernels give up and report
+                              SLSTM_ETIMEOUT: 0 = the default (4M), > 0 = this limit */
   void* phase_events;      /* NULL, or an array of SLSTM_PHASE_EVENTS hipEvent_t created by the
                               caller; the calls record them on `stream` between their phases:
-                              fwd [0] start, [1] after the op scan and its status read-back,
+                              fwd [0] start, [1] after the op scan and trace,
                               [2] after the input projection and the preparation of the exchange
                               buffers, [3] after the persistent forward kernel, [4] after the
                               h_top/c_top gathers; bwd [5] after the backward's preparation
@@ -95,17 +100,13 @@ typedef struct {
 
 /* Bytes of device work space that stacklstm_fwd / stacklstm_bwd need for `d`
  * (0 for invalid dims). The work space carries the forward's gate activations and
- * stack to the backward; pass the same buffer, untouched, to both calls. The forward
- * also records, in the library (host side, keyed by the work space's address), the
- * number of push steps it validated; a backward on that work space uses it to run its
- * gradient contractions on rocBLAS over the compacted push rows, and a backward on a
- * work space without such a record runs the same contractions on the library's own
- * kernels (same results up to fp32 rounding of the summation order). */
+ * stack depths to the backward; pass the same buffer, untouched, to both calls. */
 size_t stacklstm_workspace_bytes(const slstm_dims* d);
 
-/* Forward over T steps (Algorithm 1 for every element and step). The input projection
- * x_t W + b of all steps runs as one rocBLAS GEMM; everything else runs in the
- * library's kernels.
+/* Forward over T steps (Algorithm 1 for every element and step). Op scan and producer
+ * trace (section 3's p <- p + op on an integer stack), the input projection x_t W + b of
+ * all steps as one MFMA GEMM, the persistent recurrent kernel and the gathers of the
+ * returned states all run in the library's kernels.
  *  x      [T, B, I]   inputs x_t                                 (read)
  *  ops    [T, B]      int8 ops, +1 push / -1 pop / 0 hold         (read)
  *  W [I, 4H], U [H, 4H], b [4H], h0 [B, H], c0 [B, H]             (read)
@@ -116,13 +117,18 @@ size_t stacklstm_workspace_bytes(const slstm_dims* d);
  *  ptr    [T + 1, B]  int32 pointer before step t (ptr[T] = after the last step)
  *  top    [T, B]      int32 step that produced the returned state of step t, -1 for the
  *                     initial state (h0, c0)                      (written)
- * Returns SLSTM_EOPS / SLSTM_EUNDERFLOW after validating ops (before any other work). */
+ * Returns SLSTM_EOPS / SLSTM_EUNDERFLOW for invalid ops (lowest failing element, earliest
+ * failing step), SLSTM_ETIMEOUT / SLSTM_EINDEX as above. */
 int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
                   const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
                   float* c_top, int32_t* ptr, int32_t* top, void* workspace, size_t ws_bytes, void* stream);
 
 /* Backward of L given dL/dh_top and dL/dc_top (section 5), after stacklstm_fwd on the
- * same inputs and work space.
+ * same inputs and work space. The reverse loop scatters each step's gradient into the step
+ * that produced the state it read (the producer table `top`); dW, dU, db, dx are contracted
+ * over the push steps only (on the other steps the gate gradient is exactly 0) on the
+ * library's MFMA GEMM. A `top` or `ops` that is not the forward's gives SLSTM_EINDEX when
+ * a kernel meets an index or stack depth outside its range.
  *  x, ops, W, U, h0, c0       as given to stacklstm_fwd          (read)
  *  h_cell, c_cell, top        as written by stacklstm_fwd        (read)
  *  dh_top [T, B, H]           gradient w.r.t. h_top              (read)
@@ -134,9 +140,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                   void* workspace, size_t ws_bytes, const float* dh_top, const float* dc_top, float* dx, float* dW,
                   float* dU, float* db, float* dh0, float* dc0, void* stream);
 
-/* Synchronises `stream` and reports SLSTM_ETIMEOUT if a persistent kernel of the last
- * call on `workspace` gave up waiting for data of another workgroup (spin limit),
- * SLSTM_OK otherwise. */
+/* Synchronises `stream` and reports again the status of the last call on `workspace`
+ * (what that call returned from its read-back, for calls whose return value was lost). */
 int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream);
 
 /* Static text for a status code. */

@@ -5,9 +5,6 @@
 #include <string.h>
 #include <algorithm>
 #include <mutex>
-#include <unordered_map>
-
-#include <rocblas/rocblas.h>
 
 #include "../../include/stacklstm.h"
 #include "common.h"
@@ -16,29 +13,26 @@
 #include "recurrent.h"
 
 __global__ void k_init_ctl(uint32_t* ctl);
-__global__ void k_scan(const int8_t* ops, int T, int B, int32_t* ptr, int32_t* depth_end, uint32_t* ctl);
+template <bool LDS>
+__global__ void k_scan(const int8_t* ops, int T, int B, int cap, int32_t* ptr, int32_t* top, int32_t* depth_end,
+                       int32_t* gstack, uint32_t* ctl);
 __global__ void k_gather_top(const int32_t* top, const float* cellv, const float* init, float* out, int T, int B,
-                             int H, int skip_push);
-__global__ void k_trace(const int8_t* ops, int T, int B, int cap, int32_t* top);
+                             int H, int skip_push, uint32_t* ctl);
 __global__ void k_gather_top4(const int32_t* top, const float* hcell, const float* h0, float* htop, const float* ccell,
-                              const float* c0, float* ctop, int T, int B, int H, int skip_h);
-__global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, int I, int H);
+                              const float* c0, float* ctop, int T, int B, int H, int skip_h, uint32_t* ctl);
+__global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, bf16_t* WpT16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
 __global__ void k_zero_ctl_bwd(uint32_t* ctl);
 __global__ void k_fill_pattern(unsigned char* p, size_t bytes, uint32_t v);
 __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16(const float* in, bf16_t* out, size_t n);
-__global__ void k_augment_x(const float* x, size_t rows, int I, int KA, int nones, float* out32, bf16_t* out16);
-__global__ void k_bias_rows(const float* b, int H, int nparts, int nrows, float* out32, bf16_t* out16);
 __global__ void k_push_rows(const int8_t* ops, int n, int32_t* rows, uint32_t* count);
 __global__ void k_zero_nonpush_rows(const int8_t* ops, float* out, size_t n, int cols);
-__global__ void k_gather_rows(const float* src, const int32_t* prow, const uint32_t* count, size_t max_rows, int cols,
-                              int scatter, float* dst);
 __global__ void k_gather_hprev(const int32_t* top, const float* hcell, const float* h0, const int32_t* prow,
-                               const uint32_t* count, float* out, int T, int B, int H);
+                               const uint32_t* count, float* out, int T, int B, int H, uint32_t* ctl);
 __global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int cols, const int32_t* prow,
-                                 const uint32_t* count, int ldo, const int32_t* gtop, int B, bf16_t* out);
+                                 const uint32_t* count, int ldo, const int32_t* gtop, int B, bf16_t* out, uint32_t* ctl);
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
@@ -66,6 +60,7 @@ int device_cus() {
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+bool al16(const void* q) { return ((uintptr_t)q & 15u) == 0; }
 
 // Rows per group are chosen per kernel (forward and backward differ in register use and so
 // in how many workgroups share a CU): NT/G/per_xcc for the forward, NTb/Gb/per_xcc_b for
@@ -79,7 +74,7 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, xb, xbt, hp, dat, dh, dc, dbp, part, prow, dep, dac, xc, total;
+  size_t ctl, stack, wp, r1, stash, hx, xbt, hp, dat, dh, dc, dbp, part, prow, dep, total;
 };
 
 // Push-row count padded to the K tile: leading dimension of the transposed bf16 operands
@@ -178,80 +173,6 @@ int make_plan(const slstm_dims* d, Plan* p) {
   return SLSTM_OK;
 }
 
-// The input projection XW = x Wp + b is one plain GEMM on the vendor BLAS: x gets columns of
-// ones (one in fp32 mode; three in bf16 mode, where b is carried as the sum of three bf16
-// parts, so the bias keeps fp32 precision) and Wp gets the matching bias rows; K is padded
-// to a multiple of 32 with zeros (the vendor GEMM picks faster tiles for such K: measured
-// 0.12 ms against 0.15 ms in bf16 at T*B = 61440, 4H = 2048, I = 256).
-int xw_ones(const slstm_dims* d) { return d->precision == SLSTM_BF16_GEMM ? 3 : 1; }
-size_t xw_k(const slstm_dims* d) { return ((size_t)d->I + xw_ones(d) + 31) / 32 * 32; }
-
-// rocBLAS handles, one per (device, stream), created on first use with atomic
-// (order-dependent) kernels disabled, so a GEMM's result does not depend on what runs beside
-// it. A handle owns a device work space that its split-K GEMMs write, so GEMMs that run at
-// once on two streams need two handles. Calls are serialised under blas_mutex().
-std::mutex& blas_mutex() {
-  static std::mutex mu;
-  return mu;
-}
-// Side stream and fork/join events per device (default priority, kept for the process's
-// lifetime): the producer trace runs there, beside the input projection on the caller's
-// stream. Enqueued under blas_mutex(), so a join always follows the trace of the same call.
-struct SideStream { hipStream_t s; hipEvent_t fork, join; bool ok; };
-SideStream* side_stream() {
-  static SideStream ss[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  SideStream& x = ss[dev];
-  if (!x.ok) {
-    if (hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&x.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess) return nullptr;
-    x.ok = true;
-  }
-  return &x;
-}
-// At most kBlasHandles handles per device: past that the device is drained and its handles
-// are released before a new one is made (the streams of earlier calls may be gone).
-constexpr int kBlasHandles = 32;
-rocblas_handle blas_handle(hipStream_t st) {
-  struct Entry { hipStream_t st; rocblas_handle h; };
-  static Entry tab[64][kBlasHandles] = {};
-  static int used[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  Entry* e = tab[dev];
-  for (int i = 0; i < used[dev]; ++i)
-    if (e[i].st == st) return e[i].h;
-  if (used[dev] == kBlasHandles) {
-    if (hipDeviceSynchronize() != hipSuccess) return nullptr;
-    for (int i = 0; i < used[dev]; ++i) rocblas_destroy_handle(e[i].h);
-    used[dev] = 0;
-  }
-  rocblas_handle h = nullptr;
-  if (rocblas_create_handle(&h) != rocblas_status_success) return nullptr;
-  if (rocblas_set_atomics_mode(h, rocblas_atomics_not_allowed) != rocblas_status_success ||
-      rocblas_set_stream(h, st) != rocblas_status_success) {
-    rocblas_destroy_handle(h);
-    return nullptr;
-  }
-  e[used[dev]++] = Entry{st, h};
-  return h;
-}
-
-// Number of push rows per work space, read back with the forward's status: the backward's
-// vendor-BLAS gradient GEMMs need it on the host. A backward without a recorded count (or
-// with other T, B) runs the device-count kernels instead.
-struct PushCount { int T, B; uint32_t n; };
-std::mutex& push_mutex() {
-  static std::mutex mu;
-  return mu;
-}
-std::unordered_map<const void*, PushCount>& push_counts() {
-  static std::unordered_map<const void*, PushCount> m;
-  return m;
-}
-
 // Work-space layout; splits are bounded by 64 so the layout does not depend on the device.
 Layout layout(const slstm_dims* d) {
   const size_t T = d->T, B = d->B, I = d->I, H = d->H;
@@ -260,13 +181,11 @@ Layout layout(const slstm_dims* d) {
   Layout L;
   size_t o = 0;
   L.ctl = o; o += align256(CTL_WORDS * 4);
-  L.stack = o; o += align256(B * (T + 1) * 4);
-  const size_t KA = xw_k(d);
-  L.wp = o; o += align256(KA * 4 * H * 4);                              // Wp and its bias rows
+  L.stack = o; o += align256(B * (T + 1) * 4);                        // op scan: stacks that do not fit in LDS
+  L.wp = o; o += align256(I * 4 * H * 4);                             // Wp fp32, or Wp and Wp^T in bf16
   L.r1 = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));   // XW (forward), dA (backward)
   L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
   L.hx = o; o += bf ? align256((T + 1) * B * H * 2) : 0;
-  L.xb = o; o += align256(T * B * KA * (bf ? 2 : 4));                 // [x | ones | 0] for the XW GEMM
   // post-loop operands over the push rows (at most T*B of them; KP with the K-tile padding)
   L.xbt = o; o += bf ? align256(KP * I * 2) : 0;                      // x^T in bf16 (bf16 mode)
   L.hp = o; o += align256(std::max<size_t>(bf ? KP * H * 2 : T * B * H * 4, 16));   // Hprev (bf16 mode: Hprev^T)
@@ -277,9 +196,6 @@ Layout layout(const slstm_dims* d) {
   L.part = o; o += align256((size_t)64 * std::max(I, H) * 4 * H * 4);
   L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
   L.dep = o; o += align256(B * 4);                                     // pointer after the last step
-  // fp32 post-loop operands on the vendor BLAS: dA and x rows of the push steps, compacted
-  L.dac = o; o += bf ? 0 : align256(std::max<size_t>(T * B * 4 * H * 4, 16));
-  L.xc = o; o += align256(std::max<size_t>(T * B * std::max(I, (size_t)1) * 4, 16));   // also dx rows in bf16 mode
   L.total = o;
   return L;
 }
@@ -304,7 +220,7 @@ int launch_gemm(int prec, int AL, int BL, const GemmArgs& g, int splits, hipStre
     return hip_status(hipGetLastError());                                     \
   }
   GCASE(0, GEMM_MK, GEMM_KN) GCASE(0, GEMM_MK, GEMM_NK) GCASE(0, GEMM_KM, GEMM_KN)
-  GCASE(1, GEMM_MK, GEMM_KN) GCASE(1, GEMM_MK, GEMM_NK) GCASE(1, GEMM_KM, GEMM_KN)
+  GCASE(1, GEMM_MK, GEMM_NK) GCASE(1, GEMM_MK_F32, GEMM_NK)
 #undef GCASE
   return SLSTM_EINVAL;
 }
@@ -312,11 +228,16 @@ int launch_gemm(int prec, int AL, int BL, const GemmArgs& g, int splits, hipStre
 // K slice per split, a multiple of the GEMM's K tile (64 covers both precisions)
 int k_chunk_for(int K, int splits) { return ((K + splits - 1) / splits + 63) / 64 * 64; }
 
-int check_timeout(const uint32_t* ctl, hipStream_t st) {
-  uint32_t v = 0;
-  if (hipMemcpyAsync(&v, ctl + CTL_TIMEOUT, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
+// The call's one host synchronisation: reads the control words its kernels set and maps them
+// to a status (op errors first, then a wait that gave up, then a producer index out of range).
+int read_status(const uint32_t* ctl, hipStream_t st) {
+  uint32_t v[CTL_BADIDX + 1] = {};
+  if (hipMemcpyAsync(v, ctl, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
   if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
-  return v ? SLSTM_ETIMEOUT : SLSTM_OK;
+  if (v[CTL_STATUS] != kStatusOk) return (int)(v[CTL_STATUS] & 7u);
+  if (v[CTL_TIMEOUT]) return SLSTM_ETIMEOUT;
+  if (v[CTL_BADIDX]) return SLSTM_EINDEX;
+  return SLSTM_OK;
 }
 
 RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, bool bwd) {
@@ -326,7 +247,6 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   a.G = bwd ? p.Gb : p.G; a.NW = p.NW; a.ks_eff = p.ks_eff;
   a.spin_limit = d->spin_limit > 0 ? d->spin_limit : kDefaultSpin;
   a.ctl = (uint32_t*)(ws + L.ctl);
-  a.stack = (int32_t*)(ws + L.stack);
   a.stash = (float*)(ws + L.stash);
   a.hx = d->precision == SLSTM_BF16_GEMM ? (uint16_t*)(ws + L.hx) : nullptr;
   a.clk = (long long*)d->step_clock;
@@ -343,7 +263,6 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   if (!bwd && p.pipe) a.poll = 1;
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
   a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
-  a.coh_top = ((size_t)d->B * 4) % 128 != 0;
   // backward direct staging: whole 1 KB row segments, K range equal to the register capacity,
   // and the LDS slice plus static LDS within one CU (one workgroup per CU)
   const int KC = rec_kc(d->precision);
@@ -372,6 +291,7 @@ const char* stacklstm_status_string(int s) {
     case SLSTM_ENORESIDENT: return "persistent kernels cannot be co-resident";
     case SLSTM_EDEVICE: return "HIP runtime error";
     case SLSTM_ETIMEOUT: return "a wait for another workgroup's data exceeded the spin limit";
+    case SLSTM_EINDEX: return "a producer index or stack depth outside its valid range (top or ops not the forward's)";
     default: return "unknown status";
   }
 }
@@ -404,71 +324,47 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   char* ws = (char*)workspace;
   uint32_t* ctl = (uint32_t*)(ws + L.ctl);
   const int T = d->T, B = d->B, I = d->I, H = d->H;
+  const bool bf = p.prec == SLSTM_BF16_GEMM;
 
-  // a1: validate ops and scan the pointer (the call's one host synchronisation)
+  // a1: op validation, pointer scan and producer trace. One thread per element; its stack of
+  // T + 1 step indices in LDS when a few elements' stacks fit in 64 KB, else in the work space
   mark(d, 0, st);
   hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl);
-  hipLaunchKernelGGL(k_scan, dim3((B + 15) / 16), dim3(256), 0, st, ops, T, B, ptr, (int32_t*)(ws + L.dep), ctl);
-  uint32_t hs[CTL_NPUSHF + 1] = {};
-  if (hipMemcpyAsync(hs, ctl + CTL_STATUS, sizeof(hs), hipMemcpyDeviceToHost, st) != hipSuccess) return SLSTM_EDEVICE;
-  if (hipStreamSynchronize(st) != hipSuccess) return SLSTM_EDEVICE;
-  if (hs[0] != 0x7fffffffu) return (int)(hs[0] & 7u);
   {
-    std::lock_guard<std::mutex> lk(push_mutex());
-    if (push_counts().size() > 4096) push_counts().clear();   // bounded: work spaces are reused in practice
-    push_counts()[workspace] = PushCount{T, B, hs[CTL_NPUSHF]};
-  }
-  // the wide and the pipelined forward read a finished producer trace (they keep no integer
-  // stack of their own); the plain forward traces in-kernel
-  const bool pretrace = p.wide || p.pipe;
-  // producer trace from the ops: one thread per element, its stack in LDS (odd slot count:
-  // no bank conflicts between neighbours); launched beside the input projection below
-  const int trace_cap = (int)std::min<uint32_t>(hs[1] + 2u, (uint32_t)T + 1u) | 1;
-  int trace_R = 64;
-  while (trace_R > 1 && (size_t)trace_R * trace_cap * 4 > 48 * 1024) trace_R /= 2;
-  if (T > 0 && pretrace && (size_t)trace_R * trace_cap * 4 > 48 * 1024) return SLSTM_EINVAL;   // deeper than 12 K slots
-  mark(d, 1, st);
-  if (T == 0) return SLSTM_OK;
-
-  // a2: XW = [x | 1] [Wp ; b] for all steps (Wp = W with gate-interleaved columns), on rocBLAS
-  const bool bf = p.prec == SLSTM_BF16_GEMM;
-  void* wp = ws + L.wp;
-  const int KA = (int)xw_k(d), NO = xw_ones(d);
-  hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W,
-                     bf ? nullptr : (float*)wp, bf ? (bf16_t*)wp : nullptr, I, H);
-  hipLaunchKernelGGL(k_bias_rows, dim3(grid1d((size_t)(KA - I) * 4 * H)), dim3(256), 0, st, b, H, NO, KA - I,
-                     bf ? nullptr : (float*)wp + (size_t)I * 4 * H, bf ? (bf16_t*)wp + (size_t)I * 4 * H : nullptr);
-  float* xw = (float*)(ws + L.r1);
-  void* xa = ws + L.xb;
-  hipLaunchKernelGGL(k_augment_x, dim3(grid1d((size_t)T * B * KA)), dim3(256), 0, st, x, (size_t)T * B, I, KA, NO,
-                     bf ? nullptr : (float*)xa, bf ? (bf16_t*)xa : nullptr);
-  if ((rc = hip_status(hipGetLastError()))) return rc;
-  {
-    // column-major view: XW^T [4H x TB] = Wp_aug^T [4H x KA] . x_aug^T [KA x TB]
-    std::lock_guard<std::mutex> lk(blas_mutex());
-    SideStream* side = pretrace ? side_stream() : nullptr;
-    if (pretrace && !side) return SLSTM_EDEVICE;
-    if (pretrace) {
-      if (hipEventRecord(side->fork, st) != hipSuccess || hipStreamWaitEvent(side->s, side->fork, 0) != hipSuccess)
-        return SLSTM_EDEVICE;
-      hipLaunchKernelGGL(k_trace, dim3((B + trace_R - 1) / trace_R), dim3(trace_R), (size_t)trace_R * trace_cap * 4,
-                         side->s, ops, T, B, trace_cap, top);
-      if (hipEventRecord(side->join, side->s) != hipSuccess) return SLSTM_EDEVICE;
-    }
-    rocblas_handle h = blas_handle(st);
-    if (!h) return SLSTM_EDEVICE;
-    const float one = 1.f, zero = 0.f;
-    rocblas_status bs;
-    if (!bf)
-      bs = rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_none, 4 * H, T * B, KA, &one, (const float*)wp,
-                         4 * H, (const float*)xa, KA, &zero, xw, 4 * H);
+    const int cap = (T + 1) | 1;                  // odd: neighbouring stacks start in other banks
+    int R = (int)std::min<size_t>(64, 65536 / ((size_t)cap * 4));
+    const int lds = R >= 1 ? 1 : 0;
+    if (!lds) R = 64;
+    if (lds)
+      hipLaunchKernelGGL(k_scan<true>, dim3((B + R - 1) / R), dim3(R), (size_t)R * cap * 4, st, ops, T, B, cap, ptr, top,
+                         (int32_t*)(ws + L.dep), (int32_t*)(ws + L.stack), ctl);
     else
-      bs = rocblas_gemm_ex(h, rocblas_operation_none, rocblas_operation_none, 4 * H, T * B, KA, &one, wp,
-                           rocblas_datatype_bf16_r, 4 * H, xa, rocblas_datatype_bf16_r, KA, &zero, xw,
-                           rocblas_datatype_f32_r, 4 * H, xw, rocblas_datatype_f32_r, 4 * H, rocblas_datatype_f32_r,
-                           rocblas_gemm_algo_standard, 0, 0);
-    if (bs != rocblas_status_success) return SLSTM_EDEVICE;
-    if (pretrace && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return SLSTM_EDEVICE;
+      hipLaunchKernelGGL(k_scan<false>, dim3((B + R - 1) / R), dim3(R), 0, st, ops, T, B, cap, ptr, top,
+                         (int32_t*)(ws + L.dep), (int32_t*)(ws + L.stack), ctl);
+  }
+  if ((rc = hip_status(hipGetLastError()))) return rc;
+  mark(d, 1, st);
+  if (T == 0) return read_status(ctl, st);
+
+  // a2: XW = x W + b for all steps on the library's MFMA GEMM, columns gate-interleaved
+  // (Wp = W with permuted columns; bf16 mode: Wp and its transpose in bf16), bias added in
+  // the GEMM's epilogue in fp32
+  void* wp = ws + L.wp;
+  bf16_t* wpt = bf ? (bf16_t*)wp + (size_t)I * 4 * H : nullptr;
+  hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W, bf ? nullptr : (float*)wp,
+                     bf ? (bf16_t*)wp : nullptr, wpt, I, H);
+  float* xw = (float*)(ws + L.r1);
+  {
+    GemmArgs g;
+    memset(&g, 0, sizeof(g));
+    g.M = T * B; g.N = 4 * H; g.K = I;
+    g.A = x; g.lda = I; g.a_vec = (I % 4 == 0) && al16(x);
+    if (bf) { g.Bm = wpt; g.ldb = I; g.b_vec = (I % 8 == 0); }
+    else    { g.Bm = wp; g.ldb = 4 * H; g.b_vec = 1; }
+    g.C = xw; g.ldc = 4 * H;
+    g.bias = b; g.bias_H = H;
+    g.k_chunk = k_chunk_for(I, 1);
+    if ((rc = launch_gemm(p.prec, bf ? GEMM_MK_F32 : GEMM_MK, bf ? GEMM_NK : GEMM_KN, g, 1, st))) return rc;
   }
 
   // a3-a6: persistent recurrent kernel
@@ -476,16 +372,12 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if (bf) hipLaunchKernelGGL(k_h0_bf16, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, h0, (bf16_t*)a.hx, (size_t)B * H);
   a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
   // exchange buffers start as "not yet produced": all-one bits in the state rows the
-  // workgroups read from each other, kTopPending in the producer-index table
+  // workgroups read from each other
   if (a.poll || p.wide) {
     const size_t ex_bytes = (size_t)T * B * H * (bf ? 2 : 4);
     unsigned char* ex = bf ? (unsigned char*)(a.hx + (size_t)B * H) : (unsigned char*)h_cell;
     hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(ex_bytes / 16 + 1)), dim3(256), 0, st, ex, ex_bytes, 0xffffffffu);
-    if (!pretrace)
-      hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d((size_t)T * B / 4 + 1)), dim3(256), 0, st,
-                         (unsigned char*)top, (size_t)T * B * 4, kTopPending);
   }
-  a.traced = pretrace ? 1 : 0;
   a.htop = p.wide ? h_top : nullptr;
   a.ctop = p.wide ? c_top : nullptr;
   if (p.wide) a.NW = p.NWw;
@@ -499,21 +391,19 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   // a7: Algorithm 1's return values (the wide forward writes c_top and the h_top of push steps)
   size_t n = (size_t)T * B * H;
   float* ctop_g = p.wide ? nullptr : c_top;          // the wide forward writes c_top itself
-  const auto al16 = [](const void* q) { return ((uintptr_t)q & 15u) == 0; };
   if (H % 4 == 0 && al16(h_cell) && al16(h0) && al16(h_top) && al16(c_cell) && al16(c0) && al16(c_top)) {
     if (h_top || ctop_g)
       hipLaunchKernelGGL(k_gather_top4, dim3(grid1d(n / 4)), dim3(256), 0, st, top, h_cell, h0, h_top, c_cell, c0, ctop_g,
-                         T, B, H, p.wide);
+                         T, B, H, p.wide, ctl);
   } else {
     if (h_top)
-      hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H, p.wide);
+      hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, h_cell, h0, h_top, T, B, H, p.wide, ctl);
     if (ctop_g)
-      hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, ctop_g, T, B, H, 0);
+      hipLaunchKernelGGL(k_gather_top, dim3(grid1d(n)), dim3(256), 0, st, top, c_cell, c0, ctop_g, T, B, H, 0, ctl);
   }
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 4, st);
-  if (d->spin_limit > 0) return check_timeout(ctl, st);
-  return SLSTM_OK;
+  return read_status(ctl, st);
 }
 
 int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
@@ -535,17 +425,19 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   uint32_t* ctl = (uint32_t*)(ws + L.ctl);
   const int T = d->T, B = d->B, I = d->I, H = d->H;
   const bool bf = p.prec == SLSTM_BF16_GEMM;
+  // the backward's control words (slot and barrier counters, wait and index flags) start at 0
+  hipLaunchKernelGGL(k_zero_ctl_bwd, dim3(1), dim3(256), 0, st, ctl);
   if (T == 0) {
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, dW, (size_t)I * 4 * H, 0.f);
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)H * 4 * H)), dim3(256), 0, st, dU, (size_t)H * 4 * H, 0.f);
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)4 * H)), dim3(256), 0, st, db, (size_t)4 * H, 0.f);
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, dh0, (size_t)B * H, 0.f);
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, dc0, (size_t)B * H, 0.f);
-    return hip_status(hipGetLastError());
+    if ((rc = hip_status(hipGetLastError()))) return rc;
+    return read_status(ctl, st);
   }
 
   // a8: persistent reverse loop
-  hipLaunchKernelGGL(k_zero_ctl_bwd, dim3(1), dim3(256), 0, st, ctl);
   RecArgs a = rec_args(d, p, ws, L, true);
   a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0;
   a.hcell = const_cast<float*>(h_cell); a.ccell = const_cast<float*>(c_cell); a.top = const_cast<int32_t*>(top);
@@ -556,7 +448,8 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   a.depth_end = (const int32_t*)(ws + L.dep);
   a.dh0 = dh0; a.dc0 = dc0;
   if (a.clk) a.clk += (size_t)512 * T * 4;
-  // rows of the push steps, for the post-loop gradients (dA is exactly zero on other rows)
+  // rows of the push steps, for the post-loop gradients (dA is exactly zero on other rows);
+  // their number stays on the device: the GEMMs below take it as their K or M extent
   int32_t* prow = (int32_t*)(ws + L.prow);
   const uint32_t* npush = ctl + CTL_NPUSH;
   hipLaunchKernelGGL(k_push_rows, dim3(1), dim3(1024), 0, st, ops, T * B, prow, ctl + CTL_NPUSH);
@@ -570,7 +463,10 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if ((rc = hip_status(launch_bwd(a, p.prec, p.NTb, p.KS, dim3(8 * p.per_xcc_b), st, nullptr)))) return rc;
   mark(d, 6, st);
 
-  // a9: post-loop gradients, contracted over the push rows only (rows prow[0 .. *npush))
+  // a9: post-loop gradients on the library's MFMA GEMM, contracted over the push rows only
+  // (rows prow[0 .. *npush)). fp32: the GEMMs gather x and dA rows through prow, Hprev is
+  // gathered first; bf16: x, dA and Hprev are written transposed and compacted (k = push
+  // index contiguous, zero up to the next multiple of 64) for dW and dU.
   const int H4 = 4 * H;
   float* part = (float*)(ws + L.part);
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H4)), dim3(256), 0, st, a.db_part, p.Gb, (size_t)H4, 1, H4,
@@ -584,131 +480,23 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     g.dyn = npush;
     g.dyn_round = bf ? 64 : 1;
   };
-  // dW = x^T dA and dU = Hprev^T dA over the push rows. fp32: the GEMM gathers x and dA rows
-  // through prow, Hprev is gathered first; bf16: the three operands are written transposed
-  // and compacted (k = push index contiguous, zero up to the next multiple of 64).
   if (bf) {
     const dim3 tg4((H4 + 63) / 64, KP / 64), tgI((I + 63) / 64, KP / 64), tgH((H + 63) / 64, KP / 64);
     hipLaunchKernelGGL(k_transpose_bf16, tg4, dim3(256), 0, st, a.dA, 0, H4, H4, prow, npush, KP,
-                       (const int32_t*)nullptr, B, (bf16_t*)(ws + L.dat));
+                       (const int32_t*)nullptr, B, (bf16_t*)(ws + L.dat), ctl);
     hipLaunchKernelGGL(k_transpose_bf16, tgI, dim3(256), 0, st, x, 1, I, I, prow, npush, KP, (const int32_t*)nullptr,
-                       B, (bf16_t*)(ws + L.xbt));
+                       B, (bf16_t*)(ws + L.xbt), ctl);
     hipLaunchKernelGGL(k_transpose_bf16, tgH, dim3(256), 0, st, ws + L.hx, 0, H, H, prow, npush, KP, top, B,
-                       (bf16_t*)hp);
+                       (bf16_t*)hp, ctl);
   } else {
     hipLaunchKernelGGL(k_gather_hprev, dim3(grid1d((size_t)K * H)), dim3(256), 0, st, top, h_cell, h0, prow, npush,
-                       (float*)hp, T, B, H);
+                       (float*)hp, T, B, H, ctl);
   }
-  // fp32 with the push count known on the host (recorded by the forward on this work space):
-  // the three gradient GEMMs on rocBLAS over compacted push rows
-  uint32_t np_host = 0;
-  {
-    std::lock_guard<std::mutex> lk(push_mutex());
-    auto it = push_counts().find(workspace);
-    if (it != push_counts().end() && it->second.T == T && it->second.B == B && it->second.n <= (uint32_t)K)
-      np_host = it->second.n;
-  }
-  if (bf && np_host > 0) {
-    // bf16 operands are already compacted and transposed: xbt [I][KP], dat [4H][KP] (push index
-    // contiguous, zero past the count); dx on rocBLAS, dW and dU on the library's kernel (faster
-    // than the vendor BLAS on these transposed operands, measured at large)
-    const int np = (int)np_host;
-    float* xc = (float*)(ws + L.xc);
-    const float one = 1.f, zero = 0.f;
-    gemm_base();
-    g.M = I; g.N = H4; g.dyn_axis = 1;
-    g.K = KP; g.A = ws + L.xbt; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1;
-    g.C = part; g.ldc = H4;
-    g.split_stride = (size_t)I * H4;
-    if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, p.splits_w, st))) return rc;
-    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, p.splits_w,
-                       g.split_stride, I, H4, H, dW);
-    mark(d, 7, st);
-    gemm_base();
-    g.M = H; g.N = H4; g.dyn_axis = 1;
-    g.K = KP; g.A = hp; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1;
-    g.C = part; g.ldc = H4;
-    g.split_stride = (size_t)H * H4;
-    if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, p.splits_u, st))) return rc;
-    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, p.splits_u,
-                       g.split_stride, H, H4, H, dU);
-    mark(d, 8, st);
-    {
-      std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle(st);
-      if (!h) return SLSTM_EDEVICE;
-      // dx_c^T [I x np] = Wp [I x 4H] . dat [4H x np]   (Wp rows are the first I of [Wp ; b])
-      if (rocblas_gemm_ex(h, rocblas_operation_transpose, rocblas_operation_transpose, I, np, H4, &one, ws + L.wp,
-                          rocblas_datatype_bf16_r, H4, ws + L.dat, rocblas_datatype_bf16_r, KP, &zero, xc,
-                          rocblas_datatype_f32_r, I, xc, rocblas_datatype_f32_r, I, rocblas_datatype_f32_r,
-                          rocblas_gemm_algo_standard, 0, 0) != rocblas_status_success)
-        return SLSTM_EDEVICE;
-    }
-    hipLaunchKernelGGL(k_zero_nonpush_rows, dim3(grid1d((size_t)K * I / 4 + 1)), dim3(256), 0, st, ops, dx, (size_t)K,
-                       I);
-    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * I / 4 + 1)), dim3(256), 0, st, (const float*)xc, prow,
-                       npush, (size_t)K, I, 1, dx);
-    if ((rc = hip_status(hipGetLastError()))) return rc;
-    mark(d, 9, st);
-    if (d->spin_limit > 0) return check_timeout(ctl, st);
-    return SLSTM_OK;
-  }
-  if (!bf && np_host > 0) {
-    float* dac = (float*)(ws + L.dac);
-    float* xc = (float*)(ws + L.xc);
-    const int np = (int)np_host;
-    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * H4 / 4)), dim3(256), 0, st, (const float*)a.dA, prow,
-                       npush, (size_t)K, H4, 0, dac);
-    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * I / 4 + 1)), dim3(256), 0, st, x, prow, npush,
-                       (size_t)K, I, 0, xc);
-    if ((rc = hip_status(hipGetLastError()))) return rc;
-    const float one = 1.f, zero = 0.f;
-    {
-      std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle(st);
-      if (!h) return SLSTM_EDEVICE;
-      // column-major views: dWp^T [4H x I] = dA_c^T [4H x np] . x_c [np x I]
-      if (rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, H4, I, np, &one, dac, H4, xc, I, &zero,
-                        part, H4) != rocblas_status_success)
-        return SLSTM_EDEVICE;
-    }
-    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, 1, (size_t)I * H4, I, H4,
-                       H, dW);
-    mark(d, 7, st);
-    {
-      std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle(st);
-      if (!h) return SLSTM_EDEVICE;
-      // dUp^T [4H x H] = dA_c^T [4H x np] . Hprev_c [np x H]
-      if (rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, H4, H, np, &one, dac, H4,
-                        (const float*)hp, H, &zero, part, H4) != rocblas_status_success)
-        return SLSTM_EDEVICE;
-    }
-    hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, 1, (size_t)H * H4, H, H4,
-                       H, dU);
-    mark(d, 8, st);
-    {
-      std::lock_guard<std::mutex> lk(blas_mutex());
-      rocblas_handle h = blas_handle(st);
-      if (!h) return SLSTM_EDEVICE;
-      // dx_c^T [I x np] = Wp [I x 4H] . dA_c^T [4H x np]   (Wp rows are the first I of [Wp ; b])
-      if (rocblas_sgemm(h, rocblas_operation_transpose, rocblas_operation_none, I, np, H4, &one, (const float*)(ws + L.wp),
-                        H4, dac, H4, &zero, xc, I) != rocblas_status_success)
-        return SLSTM_EDEVICE;
-    }
-    hipLaunchKernelGGL(k_zero_nonpush_rows, dim3(grid1d((size_t)K * I / 4 + 1)), dim3(256), 0, st, ops, dx, (size_t)K,
-                       I);
-    hipLaunchKernelGGL(k_gather_rows, dim3(grid1d((size_t)np * I / 4 + 1)), dim3(256), 0, st, (const float*)xc, prow,
-                       npush, (size_t)K, I, 1, dx);
-    if ((rc = hip_status(hipGetLastError()))) return rc;
-    mark(d, 9, st);
-    if (d->spin_limit > 0) return check_timeout(ctl, st);
-    return SLSTM_OK;
-  }
+  // dW = x^T dA
   gemm_base();
   g.M = I; g.N = H4; g.dyn_axis = 1;
   if (bf) { g.K = KP; g.A = ws + L.xbt; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1; }
-  else    { g.K = K; g.A = x; g.lda = I; g.a_vec = (I % 4 == 0); g.a_rows = prow;
+  else    { g.K = K; g.A = x; g.lda = I; g.a_vec = (I % 4 == 0) && al16(x); g.a_rows = prow;
             g.Bm = a.dA; g.ldb = H4; g.b_vec = 1; g.b_rows = prow; }
   g.C = part; g.ldc = H4;
   g.split_stride = (size_t)I * H4;
@@ -716,6 +504,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, p.splits_w,
                      g.split_stride, I, H4, H, dW);
   mark(d, 7, st);
+  // dU = Hprev^T dA
   gemm_base();
   g.M = H; g.N = H4; g.dyn_axis = 1;
   if (bf) { g.K = KP; g.A = hp; g.lda = KP; g.a_vec = 1; g.Bm = ws + L.dat; g.ldb = KP; g.b_vec = 1; }
@@ -741,13 +530,12 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                      I);
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 9, st);
-  if (d->spin_limit > 0) return check_timeout(ctl, st);
-  return SLSTM_OK;
+  return read_status(ctl, st);
 }
 
 int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream) {
   if (!workspace || ws_bytes < align256(CTL_WORDS * 4)) return SLSTM_EINVAL;
-  return check_timeout((const uint32_t*)workspace, (hipStream_t)stream);
+  return read_status((const uint32_t*)workspace, (hipStream_t)stream);
 }
 
 }  // extern "C"

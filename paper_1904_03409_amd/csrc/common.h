@@ -11,17 +11,21 @@ typedef uint16_t bf16_t;  // raw bfloat16 bits in memory
 // Status codes shared with the C-ABI (values fixed by include/stacklstm.h).
 enum {
   ST_OK = 0, ST_EINVAL = 1, ST_EOPS = 2, ST_EUNDERFLOW = 3, ST_EWORKSPACE = 4,
-  ST_ENORESIDENT = 5, ST_EDEVICE = 6, ST_ETIMEOUT = 7
+  ST_ENORESIDENT = 5, ST_EDEVICE = 6, ST_ETIMEOUT = 7, ST_EINDEX = 8
 };
+
+// CTL_STATUS while every op is valid.
+constexpr uint32_t kStatusOk = 0x7fffffffu;
 
 // Work-space word offsets (uint32 units) of the control block at the start of the work space.
 enum {
   CTL_STATUS = 0,        // lowest (element * 8 + code) of a failing element, or 0x7fffffff
   CTL_MAXDEPTH = 1,
-  CTL_ABORT = 2,         // set when a group barrier ran out of spins
-  CTL_TIMEOUT = 3,
+  CTL_ABORT = 2,         // set when a wait ran out of spins: every workgroup leaves its loop
+  CTL_TIMEOUT = 3,       // set when a wait ran out of spins (reported as SLSTM_ETIMEOUT)
   CTL_NPUSH = 4,         // number of push rows (written by k_push_rows in the backward)
-  CTL_NPUSHF = 5,        // number of push rows (counted by k_scan in the forward, read back by the host)
+  CTL_NPUSHF = 5,        // number of push rows (counted by k_scan in the forward)
+  CTL_BADIDX = 6,        // set when a kernel read a producer index outside its valid range
   CTL_XCC_SLOT = 16,     // 16 per-XCC slot counters (forward kernel)
   CTL_XCC_SLOT_B = 32,   // 16 per-XCC slot counters (backward kernel)
   CTL_BAR_F = 64,        // forward group barrier counters, one 64-byte line per group
@@ -90,11 +94,10 @@ __device__ __forceinline__ uint16_t ld_coh_b16(rsrc_t r, uint32_t off) {
 
 // Barrier-free exchange of states between the workgroups of one XCC. Before the kernel
 // the exchanged rows are filled with all-one bits (a NaN no producer ever stores: produced
-// NaNs are stored as the canonical quiet NaN) and the producer-index table with
-// kTopPending; a consumer reads a row, and re-reads every 16-byte granule that still holds
-// the fill, with agent-scope atomic loads (never hoisted or merged by the compiler, and
-// they miss in this CU's L1), until the producer's store has reached the XCC's L2.
-constexpr uint32_t kTopPending = 0x80000000u;
+// NaNs are stored as the canonical quiet NaN); a consumer reads a row, and re-reads every
+// 16-byte granule that still holds the fill, with agent-scope atomic loads (never hoisted
+// or merged by the compiler, and they miss in this CU's L1), until the producer's store has
+// reached the XCC's L2.
 __device__ __forceinline__ bool pending_f32x4(uint4 v) {
   return v.x == 0xffffffffu || v.y == 0xffffffffu || v.z == 0xffffffffu || v.w == 0xffffffffu;
 }
@@ -116,6 +119,22 @@ __device__ __forceinline__ uint4 ld_poll_b128(const void* p) {
   return uint4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
 }
 __device__ __forceinline__ float canon_nan(float h) { return h == h ? h : __builtin_nanf(""); }
+
+// A producer index s read at step t must lie in [-1, t) (the state read at step t) or
+// [-1, t] (the state at the top after step t). An index outside its range means that the
+// producer table passed in was not the forward's, or that a read returned stale data: the
+// kernel raises CTL_BADIDX (the call then reports SLSTM_EINDEX), and uses -1 so that every
+// access stays inside the arrays.
+__device__ __forceinline__ void raise_badidx(uint32_t* ctl) {
+  __hip_atomic_store(&ctl[CTL_BADIDX], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int checked_src(int s, int hi, uint32_t* ctl) {
+  if (s < -1 || s > hi) {
+    raise_badidx(ctl);
+    return -1;
+  }
+  return s;
+}
 
 // Bounded wait: counts failed polls of one wait; gives up (returns true) when the count
 // reaches the limit, raising the abort and time-out flags, or when another workgroup has

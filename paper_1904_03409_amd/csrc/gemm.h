@@ -3,7 +3,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
-enum { GEMM_MK = 0, GEMM_KM = 1 };   // A layouts: A(m,k) = A[m*lda+k] or A[k*lda+m]
+// A layouts: A(m,k) = A[m*lda+k] (MK) or A[k*lda+m] (KM); MK_F32: MK with fp32 elements,
+// rounded to bf16 on load (bf16 kernels)
+enum { GEMM_MK = 0, GEMM_KM = 1, GEMM_MK_F32 = 2 };
 enum { GEMM_KN = 0, GEMM_NK = 1 };   // B layouts: B(k,n) = B[k*ldb+n] or B[n*ldb+k]
 
 struct GemmArgs {

@@ -4,7 +4,8 @@
 //   dx = dA Wp^T      dW = x^T dA      dU = Hprev^T dA   (Hprev = the state each step read)
 // C[M][N] = sum_k A(m, k) B(k, n); A stored MK (A[m*lda+k]) or KM (A[k*lda+m]); B stored KN
 // (B[k*ldb+n]) or NK (B[n*ldb+k]). Both operands share one element type: fp32
-// (v_mfma_f32_16x16x4f32) or bf16 (v_mfma_f32_16x16x32_bf16), fp32 accumulation.
+// (v_mfma_f32_16x16x4f32) or bf16 (v_mfma_f32_16x16x32_bf16), fp32 accumulation; a bf16
+// kernel can also read an fp32 A (MK) and round it to bf16 as it loads it.
 // 128x128 block tile, four 64x64 wave tiles, K slices of BK; the next slice is fetched
 // into registers while the current one is multiplied (two LDS buffers, one barrier per
 // slice). Split K writes partials that k_reduce_splits adds in a fixed order.
@@ -35,8 +36,10 @@ template <int P, bool KMAJOR> struct Geo {
   static constexpr int ELEMS = ROWS * LD;
 };
 
-// Register staging of one operand tile: NV vectors of VE elements per thread.
-template <int P, bool KMAJOR> struct Stage {
+// Register staging of one operand tile: NV vectors of VE elements per thread. With F32SRC
+// (bf16 kernels only) the array holds fp32 values, rounded to bf16 (nearest even) as they are
+// loaded.
+template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
   using T = typename Cfg<P>::T;
   static constexpr int BK = Cfg<P>::BK, VE = Cfg<P>::VE;
   static constexpr int NV = 128 * BK / VE / 256;
@@ -61,8 +64,42 @@ template <int P, bool KMAJOR> struct Stage {
   // bounds-checked buffer descriptor: an element past the row or column limit is given an
   // offset beyond the buffer, which reads 0 without a branch or a memory access. It needs
   // the row stride and both limits to be multiples of VE (checked by the host).
-  __device__ __forceinline__ void load(const T* __restrict__ base, size_t bytes, int ld, int r0, int rlim, int c0,
+  __device__ __forceinline__ void load(const void* __restrict__ vbase, size_t bytes, int ld, int r0, int rlim, int c0,
                                        int clim, bool vec, const int32_t* __restrict__ rows) {
+    if constexpr (F32SRC) {
+      static_assert(P == 1 && !KMAJOR, "fp32 source: bf16 kernels, k-contiguous rows");
+      // two 16-byte loads of four floats per vector; the vector path needs the row stride and
+      // both limits to be multiples of 4 (each half lies wholly inside or outside the row)
+      const float* fb = (const float*)vbase;
+      const rsrc_t rs = make_rsrc(fb, bytes);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int e = threadIdx.x + 256 * i;
+        const int r = e / (BK / VE), c = (e % (BK / VE)) * VE;
+        const int gr = r0 + r, gc = c0 + c;
+        const int pr = prow[i];
+        bf16_t q[VE];
+        if (vec) {
+          float f[8];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const bool ok = gr < rlim && gc + 4 * hh < clim;
+            const uint32_t off = ok ? (uint32_t)(((size_t)pr * ld + gc + 4 * hh) * 4) : 0xffffffffu;
+            const float4 v4 = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+            f[4 * hh] = v4.x; f[4 * hh + 1] = v4.y; f[4 * hh + 2] = v4.z; f[4 * hh + 3] = v4.w;
+          }
+#pragma unroll
+          for (int j = 0; j < VE; ++j) q[j] = f32_to_bf16_bits(f[j]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < VE; ++j)
+            q[j] = (gr < rlim && gc + j < clim) ? f32_to_bf16_bits(fb[(size_t)pr * ld + gc + j]) : (bf16_t)0;
+        }
+        v[i] = *(const uint4*)q;
+      }
+      return;
+    }
+    const T* base = (const T*)vbase;
     if (vec) {
       const rsrc_t rs = make_rsrc(base, bytes);
 #pragma unroll
@@ -127,6 +164,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
   using T = typename Cfg<P>::T;
   constexpr int BK = Cfg<P>::BK;
   constexpr bool AKM = (AL == GEMM_KM), BKN = (BL == GEMM_KN);
+  constexpr bool AF32 = (AL == GEMM_MK_F32);       // bf16 kernel, fp32 A rounded on load
   using GA = Geo<P, AKM>;
   using GB = Geo<P, BKN>;
   __shared__ __align__(16) T As[2][GA::ELEMS];
@@ -148,13 +186,13 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int l16 = lane & 15, lq = lane >> 4;
-  const T* A = (const T*)g.A;
+  const void* A = g.A;
   const T* Bp = (const T*)g.Bm;
 
-  Stage<P, AKM> sa;
+  Stage<P, AKM, AF32> sa;
   Stage<P, BKN> sb;
   // buffer extents: the arrays' static sizes (gathered rows index within them)
-  const size_t abytes = (AKM ? (size_t)g.K * g.lda : (size_t)g.M * g.lda) * sizeof(T);
+  const size_t abytes = (AKM ? (size_t)g.K * g.lda : (size_t)g.M * g.lda) * (AF32 ? 4 : sizeof(T));
   const size_t bbytes = (BKN ? (size_t)g.K * g.ldb : (size_t)g.N * g.ldb) * sizeof(T);
   if (!AKM) sa.set_rows(g.a_rows, m0, M);
   if (!BKN) sb.set_rows(g.b_rows, n0, g.N);
@@ -266,6 +304,5 @@ __global__ void __launch_bounds__(256) k_reduce_splits(const float* __restrict__
 INST(0, GEMM_MK, GEMM_KN)
 INST(0, GEMM_MK, GEMM_NK)
 INST(0, GEMM_KM, GEMM_KN)
-INST(1, GEMM_MK, GEMM_KN)
 INST(1, GEMM_MK, GEMM_NK)
-INST(1, GEMM_KM, GEMM_KN)
+INST(1, GEMM_MK_F32, GEMM_NK)

@@ -43,11 +43,12 @@ __device__ __forceinline__ void fwd_load_u(const RecArgs& a, int unit_base, int 
 }
 
 // Fused LSTM cell of one (step t, row b, unit u) pair from the MFMA output (gates i, f, g,
-// o of the pair in acc) and the input projection: writes h, c, the bf16 copy of h and the
+// o of the pair in acc) and the input projection: writes h, c, the bf16 copy of h and, when
+// `keep` (a push step: the backward reads the gate activations of push steps only), the
 // gate activations; returns c. h is never stored as the all-ones fill pattern.
 template <int PREC>
 __device__ __forceinline__ float fwd_cell(const RecArgs& a, const f32x4& acc, const float4& xw, float cp, int t,
-                                          int b, int u) {
+                                          int b, int u, bool keep) {
   const float gi = sigmoidf_(acc[0] + xw.x);
   const float gf = sigmoidf_(acc[1] + xw.y);
   const float gg = tanhf_(acc[2] + xw.z);
@@ -58,6 +59,6 @@ __device__ __forceinline__ float fwd_cell(const RecArgs& a, const f32x4& acc, co
   a.hcell[o] = h;
   a.ccell[o] = c;
   if constexpr (PREC == 1) a.hx[o + (size_t)a.B * a.H] = f32_to_bf16_bits(h);
-  *(float4*)(a.stash + ((size_t)t * a.B + b) * (4 * a.H) + 4 * u) = float4{gi, gf, gg, go};
+  if (keep) *(float4*)(a.stash + ((size_t)t * a.B + b) * (4 * a.H) + 4 * u) = float4{gi, gf, gg, go};
   return c;
 }

@@ -9,10 +9,9 @@ struct RecArgs {
   // 1 when a cache line of the exchanged arrays can hold entries of two different steps
   // (rows not 128-byte multiples): then every exchanged value is read with L1-bypassing
   // loads; with aligned rows a line is never read before its only write, plain loads suffice
-  int coh_rows, coh_top;
+  int coh_rows;
   int bwd_direct;        // backward stages dA rows with global_load_lds (host checks the LDS fits)
   int poll;              // 1: workgroups exchange rows by polling fill-marked data; 0: group barrier per step
-  int traced;            // 1: top[] holds the finished producer trace before the forward kernel starts
   const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)
@@ -22,8 +21,8 @@ struct RecArgs {
   float* ccell;          // [T][B][H]
   uint16_t* hx;          // [T+1][B][H] bf16 copies: slot 0 = h0, slot t+1 = hcell[t] (bf16-GEMM mode)
   float* stash;          // [T][B][4H] gate activations i, f, g, o, gate-interleaved
-  int32_t* top;          // [T][B]     producer step of the state returned at step t (-1 = initial)
-  int32_t* stack;        // [B][T+1]   step index written to each stack slot
+  int32_t* top;          // [T][B]     producer step of the state returned at step t (-1 = initial),
+                         //            complete before the forward kernel starts (op scan)
   float* htop;           // [T][B][H] or null: state at the top after step t (wide forward writes it)
   float* ctop;           // [T][B][H] (with htop)
   uint32_t* ctl;         // control block (status, barrier counters)

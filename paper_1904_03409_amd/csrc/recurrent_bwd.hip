@@ -132,8 +132,8 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // The operands are fetched after the step's last wait for dA rows, so no wait of the
   // step includes them.
   auto valid_sp = [&](int t, int& sp) {
-    // guard against a producer table that is not the forward's: no access outside [-1, t)
-    if (sp < -1 || sp >= t) sp = -1;
+    // a producer table that is not the forward's is reported (no access outside [-1, t))
+    sp = checked_src(sp, t - 1, a.ctl);
   };
   int c_op[PAIRS], c_sp[PAIRS];                          // step t row info
   int n_op[PAIRS], n_sp[PAIRS], nn_op[PAIRS], nn_sp[PAIRS];
@@ -269,7 +269,14 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         gc[i] = (fwd ? lc[i] : sc) + dc * act.y;
         dep[i] -= 1;
       } else if (c_op[i] == -1) {
-        // the popped state comes back: the state below is spilled, the popped one starts at 0
+        // the popped state comes back: the state below is spilled, the popped one starts at 0.
+        // The depth stays in [0, T] for the forward's ops; ops that are not the forward's are
+        // reported, with no store outside the spill slots. (Pairs outside the batch or the
+        // units follow row 0's ops from depth 0 and store nothing.)
+        if (pok[i] && (dep[i] < 0 || dep[i] > T)) {
+          raise_badidx(a.ctl);
+          dep[i] = 0;
+        }
         if (pok[i]) {
           const size_t o = ((size_t)dep[i] * B + b) * H + u;
           a.dh_acc[o] = gh[i];

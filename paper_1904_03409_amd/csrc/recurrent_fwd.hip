@@ -10,8 +10,10 @@
 // the group's h_prev rows into LDS, runs h_prev U on MFMA (gates^T = U^T h_prev^T so
 // one lane holds the four gates of one (unit, row) pair), applies the gate
 // nonlinearities and the cell update in registers, writes h, c, the bf16 copy of h
-// and the gate activations, and meets the group at a barrier. Workgroup 0 of the
-// group also keeps the integer stack: stack[b][p+1] <- t, p <- p + op, top <- stack[b][p].
+// and (for push steps, the only ones the backward reads) the gate activations, and meets
+// the group at a barrier. The producer of every state read comes from top[], which the op
+// scan filled before the kernel (the integer stack stack[p+1] <- t, p <- p + op,
+// top <- stack[p] depends on the ops alone).
 //
 // Latency schedule of one step: the h_prev rows go straight from L2 into LDS
 // (global_load_lds, whole 1 KB row segments per wave instruction) when the row length
@@ -38,7 +40,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   elem_t* hs = reinterpret_cast<elem_t*>(smem);
   __shared__ int s_src[BG];
   __shared__ int s_g, s_w;
-  __shared__ int s_abort[2];   // [0]: a staging wait gave up, [1]: a producer-index wait gave up
+  __shared__ int s_abort[2];   // [0]: a staging wait gave up, [1]: a group barrier gave up
 
   claim_group_slot(a.ctl + CTL_XCC_SLOT, a.G, a.NW, &s_g, &s_w);
   const int g = s_g, w = s_w;
@@ -52,7 +54,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   const int u = unit_base + lq;                    // epilogue unit of this lane
   const int ks_eff = a.ks_eff;
   const size_t TBH = (size_t)T * B * H;
-  const rsrc_t r_top = make_rsrc(a.top, (size_t)T * B * 4);
   // staged rows: fp32 mode reads h_cell (src >= 0) or h0; bf16 mode reads the bf16 copy
   // whose slot 0 holds h0 and slot s+1 the state of step s
   const rsrc_t r_h = PREC ? make_rsrc(a.hx, TBH * 2 + (size_t)B * H * 2) : make_rsrc(a.hcell, TBH * 4);
@@ -62,9 +63,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   bf16x8 ureg16[PREC ? KS : 1];
   fwd_load_u<PREC, KS>(a, unit_base, l16, lq, ureg32, ureg16);
 
-  const bool tracer = (w == 0) && ((int)threadIdx.x < BG) && (row0 + (int)threadIdx.x < B);
-  const int my_row = row0 + (int)threadIdx.x;
-  const size_t stk_base = (size_t)my_row * (T + 1);
   const int kmax = ks_eff * KC;                    // staged K (>= H)
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
   const bool direct = vec_ok && kmax == KP && (KP * ESZ) % 1024 == 0;
@@ -83,20 +81,8 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   };
   auto top_at = [&](int t, int ti) -> int {
     const int b = lrow[ti] < B ? lrow[ti] : 0;
-    return (int)ld_coh_b32(r_top, (uint32_t)(((size_t)t * B + b) * 4));
+    return a.top[(size_t)t * B + b];
   };
-
-  // Integer stack of the group's rows, kept by workgroup 0 one step ahead of the floats.
-  int my_p = 0, my_top = -1, op_next = 0;
-  if (tracer) {
-    int op0 = a.ops[my_row];
-    op_next = (T > 1) ? a.ops[(size_t)B + my_row] : 0;
-    a.stack[stk_base] = -1;                       // slot 0: the initial state
-    a.stack[stk_base + 1] = 0;
-    my_p = max(0, op0);
-    my_top = (op0 == 1) ? 0 : -1;                 // a pop at step 0 is rejected by the scan
-    a.top[my_row] = my_top;
-  }
   if ((int)threadIdx.x < BG) s_src[threadIdx.x] = -1;
   if (threadIdx.x < 2) s_abort[threadIdx.x] = 0;
   constexpr int NV = (BG + 63) / 64;
@@ -132,7 +118,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     float4 xw_nxt[NT];
     int src_nxt[NT];
     float cp_nxt[NT];
-    int tp_next = 0;
 
     if constexpr (PREC == 1) {
       // bf16 steps are short: the next step's input projection (HBM) and producer indices are
@@ -323,15 +308,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
       }
 
-      // trace for step t+1 (stack[p+1] <- t+1, p <- p + op, top <- stack[p]), published at the end of the step
-      if (nb == 0 && tracer && more) {
-        int op = op_next;
-        op_next = (t + 2 < T) ? a.ops[(size_t)(t + 2) * B + my_row] : 0;
-        a.stack[stk_base + my_p + 1] = t + 1;
-        my_p = max(0, my_p + op);
-        tp_next = (op == 1) ? t + 1 : (op == 0 ? my_top : a.stack[stk_base + my_p]);
-      }
-
       // ---- gates^T (16 cols x 16 rows per tile) = U^T h_prev^T; B fragments read one chunk ahead
       f32x4 acc[NTB];
 #pragma unroll
@@ -379,34 +355,17 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       for (int nt = 0; nt < NTB; ++nt) {
         const int ti = nb * NTB + nt;
         if (!lok[ti]) continue;
-        cp_cur[ti] = fwd_cell<PREC>(a, acc[nt], xw_cur[ti], cp_cur[ti], t, lrow[ti], u);   // the state this step produced
+        // the state this step produced; gate activations kept for a push (top[t] = t)
+        cp_cur[ti] = fwd_cell<PREC>(a, acc[nt], xw_cur[ti], cp_cur[ti], t, lrow[ti], u, src_nxt[ti] == t);
       }
       if (NPASS > 1) __syncthreads();
     }
     if (stop) break;
 
-    // producers of step t+1: published by the tracer at the end of step t-1
-    if (more) {
-#pragma unroll
-      for (int ti = 0; ti < NT; ++ti) {
-        int s = src_nxt[ti];
-        int spins = 0;
-        while (s == (int)kTopPending) {
-          if (spin_out(spins, a.ctl, a.spin_limit)) {
-            s_abort[1] = 1;
-            break;
-          }
-          const int b = lrow[ti] < B ? lrow[ti] : 0;
-          s = (int)__hip_atomic_load((uint32_t*)a.top + (size_t)t * B + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        src_nxt[ti] = s;
-      }
-    }
     // c_prev of step t+1: the state produced now (push at t) or an older one of this workgroup
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) {
-      int s = src_nxt[ti];
-      if (!more || s < -1 || s > t) s = -1;
+      const int s = more ? checked_src(src_nxt[ti], t, a.ctl) : -1;
       src_nxt[ti] = s;
       cp_nxt[ti] = cp_cur[ti];
       if (lok[ti] && s != t) {
@@ -415,10 +374,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       }
     }
     if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
-    if (tracer && more) {
-      a.top[(size_t)(t + 1) * B + my_row] = tp_next;
-      my_top = tp_next;
-    }
     if (wave == 0 && lq == 0) {
 #pragma unroll
       for (int ti = 0; ti < NT; ++ti) s_src[ti * 16 + l16] = src_nxt[ti];
@@ -426,7 +381,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) { xw_cur[ti] = xw_nxt[ti]; cp_cur[ti] = cp_nxt[ti]; }
     if (!a.poll) {
-      // barrier mode: the tracer's index and every state of step t are complete past this point
+      // barrier mode: every state of step t is complete past this point
       if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_abort[1]))
         break;
     } else {

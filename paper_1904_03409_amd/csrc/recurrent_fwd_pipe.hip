@@ -12,8 +12,9 @@
 // long finished tile 0 of step t.
 //
 // There is no group barrier: the states a workgroup reads from the others are filled with
-// all-one bits before the kernel, a copied granule that still holds them is copied again,
-// and the producer-index table is polled the same way (see common.h).
+// all-one bits before the kernel, and a copied granule that still holds them is copied again
+// (see common.h). The producer of every state read comes from top[], which the op scan
+// filled before the kernel.
 #include "common.h"
 #include "recurrent.h"
 #include "rec_config.h"
@@ -107,9 +108,9 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   elem_t* hs = reinterpret_cast<elem_t*>(smem);  // two tile buffers; tile p of a step uses buffer p % 2
   __shared__ int s_g, s_w;
-  // wait failures: [0]/[1] copies of even/odd tiles, [2] producer indices. Each flag is read
-  // right after the barrier that follows its writes, and written again only after a later one.
-  __shared__ int s_abort[3];
+  // wait failures of the copies of even/odd tiles. Each flag is read right after the barrier
+  // that follows its writes, and written again only after a later one.
+  __shared__ int s_abort[2];
 
   claim_group_slot(a.ctl + CTL_XCC_SLOT, a.G, a.NW, &s_g, &s_w);
   const int g = s_g, w = s_w;
@@ -121,28 +122,10 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   const int row0 = g * BG;
   const int unit_base = w * 16 + wave * 4;
   const int u = unit_base + lq;                    // epilogue unit of this lane
-  const rsrc_t r_top = make_rsrc(a.top, (size_t)T * B * 4);
 
   float ureg32[PREC ? 1 : KS][4];
   bf16x8 ureg16[PREC ? KS : 1];
   fwd_load_u<PREC, KS>(a, unit_base, l16, lq, ureg32, ureg16);
-
-  // integer stack of the group's rows, kept by workgroup 0 one step ahead of the floats,
-  // unless the producer trace was computed before the kernel (then top[] is final and the
-  // polls below return at their first load)
-  const bool tracer = !a.traced && (w == 0) && ((int)threadIdx.x < BG) && (row0 + (int)threadIdx.x < B);
-  const int my_row = row0 + (int)threadIdx.x;
-  const size_t stk_base = (size_t)my_row * (T + 1);
-  int my_p = 0, my_top = -1, op_next = 0;
-  if (tracer) {
-    const int op0 = a.ops[my_row];
-    op_next = (T > 1) ? a.ops[(size_t)B + my_row] : 0;
-    a.stack[stk_base] = -1;                        // slot 0: the initial state
-    a.stack[stk_base + 1] = 0;
-    my_p = max(0, op0);
-    my_top = (op0 == 1) ? 0 : -1;                  // a pop at step 0 is rejected by the scan
-    a.top[my_row] = my_top;
-  }
 
   // rows of this lane in the MFMA output layout: tile ti covers rows ti*16 .. ti*16+15
   int lrow[NT];
@@ -158,19 +141,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   };
   auto top_at = [&](int t, int ti) -> int {
     const int b = lrow[ti] < B ? lrow[ti] : 0;
-    return (int)ld_coh_b32(r_top, (uint32_t)(((size_t)t * B + b) * 4));
-  };
-  auto poll_top = [&](int tt, int ti, int s) -> int {
-    int spins = 0;
-    while (s == (int)kTopPending) {
-      if (spin_out(spins, a.ctl, a.spin_limit)) {
-        s_abort[2] = 1;
-        return -1;
-      }
-      const int b = lrow[ti] < B ? lrow[ti] : 0;
-      s = (int)__hip_atomic_load((uint32_t*)a.top + (size_t)tt * B + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return s;
+    return a.top[(size_t)t * B + b];
   };
 
   // c_prev of tile ti at step ts+1 given its producer s and the state c just produced
@@ -197,8 +168,9 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   f32x4 acc_pend = f32x4{0.f, 0.f, 0.f, 0.f};
   float4 xw_last = float4{0.f, 0.f, 0.f, 0.f};
   float cp_last = 0.f;
+  bool keep_last = false;                          // the last tile's pending step was a push
   long long stamp[4] = {0, 0, 0, 0};
-  if (threadIdx.x < 3) s_abort[threadIdx.x] = 0;
+  if (threadIdx.x < 2) s_abort[threadIdx.x] = 0;
   __syncthreads();
   pipe_copy<PREC, SEG, LDS_LD>(a, hs, src_cur[0], row0, wave, lane);
 
@@ -209,14 +181,13 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
     const bool more = t + 1 < T;
     float4 xw_nxt[NT];
     int src_nxt[NT];
-    int tp_next = 0;
 #pragma unroll
     for (int p = 0; p < NT; ++p) {
       elem_t* buf = hs + (p & 1) * BUF;
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       if (!pipe_complete<PREC, SEG, LDS_LD>(a, buf, src_cur[p], row0 + 16 * p, wave, lane)) s_abort[p & 1] = 1;
       __syncthreads();
-      if (s_abort[p & 1] || (p == 0 && s_abort[2])) {
+      if (s_abort[p & 1]) {
         stop = true;
         break;
       }
@@ -230,39 +201,26 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
         if (p < 2) stamp[2 * p] = wall_clock64();
       }
       if (p == 0) {
-        // producer indices of step t+1 (top[t], published by the tracer a step ago) and the
-        // next step's input projection: in flight during this step
+        // producer indices of step t+1 (top[t]) and the next step's input projection: in
+        // flight during this step
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) src_nxt[ti] = top_at(t, ti);
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
-        // trace for step t+1 (stack[p+1] <- t+1, p <- p + op, top <- stack[p]); published in the last pass
-        if (tracer && more) {
-          const int op = op_next;
-          op_next = (t + 2 < T) ? a.ops[(size_t)(t + 2) * B + my_row] : 0;
-          a.stack[stk_base + my_p + 1] = t + 1;
-          my_p = max(0, my_p + op);
-          tp_next = (op == 1) ? t + 1 : (op == 0 ? my_top : a.stack[stk_base + my_p]);
-        }
         // deferred cell update of the last tile of step t-1
         if (t > 0) {
           float c = 0.f;
-          if (lok[NT - 1]) c = fwd_cell<PREC>(a, acc_pend, xw_last, cp_last, t - 1, lrow[NT - 1], u);
+          if (lok[NT - 1]) c = fwd_cell<PREC>(a, acc_pend, xw_last, cp_last, t - 1, lrow[NT - 1], u, keep_last);
           cp_cur[NT - 1] = next_cp(NT - 1, src_cur[NT - 1], t - 1, c);
         }
       } else {
         // deferred cell update of tile p-1 of this step; its producers at step t+1 are needed now
         const int q = p - 1;
         float c = 0.f;
-        if (lok[q]) c = fwd_cell<PREC>(a, acc_pend, xw_cur[q], cp_cur[q], t, lrow[q], u);
-        int s = more ? poll_top(t, q, src_nxt[q]) : -1;
-        if (s < -1 || s > t) s = -1;
+        if (lok[q]) c = fwd_cell<PREC>(a, acc_pend, xw_cur[q], cp_cur[q], t, lrow[q], u, src_nxt[q] == t);
+        const int s = more ? checked_src(src_nxt[q], t, a.ctl) : -1;
         src_nxt[q] = s;
         cp_cur[q] = next_cp(q, s, t, c);
-      }
-      if (p == NT - 1 && tracer && more) {
-        a.top[(size_t)(t + 1) * B + my_row] = tp_next;
-        my_top = tp_next;
       }
       // next copy: tile p+1 of this step, or tile 0 of the next step (harmless after the last step)
       const int nsrc = (p + 1 < NT) ? src_cur[(p + 1) % NT] : src_nxt[0];
@@ -306,11 +264,8 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
     if (stop) break;
 
     // producers of the last tile at step t+1, needed by its cell update in the next step's first pass
-    {
-      int s = more ? poll_top(t, NT - 1, src_nxt[NT - 1]) : -1;
-      if (s < -1 || s > t) s = -1;
-      src_nxt[NT - 1] = s;
-    }
+    keep_last = src_nxt[NT - 1] == t;
+    src_nxt[NT - 1] = more ? checked_src(src_nxt[NT - 1], t, a.ctl) : -1;
     xw_last = xw_cur[NT - 1];
     cp_last = cp_cur[NT - 1];
 #pragma unroll
@@ -321,7 +276,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   }
   if (!stop && T > 0) {
     // the last tile of the last step
-    if (lok[NT - 1]) (void)fwd_cell<PREC>(a, acc_pend, xw_last, cp_last, T - 1, lrow[NT - 1], u);
+    if (lok[NT - 1]) (void)fwd_cell<PREC>(a, acc_pend, xw_last, cp_last, T - 1, lrow[NT - 1], u, keep_last);
     if (clk && threadIdx.x == 0) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) clk[(T - 1) * 4 + k] = stamp[k];

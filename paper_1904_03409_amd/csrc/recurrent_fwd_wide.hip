@@ -24,8 +24,8 @@
 //
 // Exchange: the bf16 state rows (slot s+1 = step s, slot 0 = h0) start filled with all-one
 // bits; a copied granule that still holds them is copied again until the producer's store
-// has arrived (see common.h). Producer indices come from k_trace before the kernel, so no
-// workgroup keeps the integer stack; they are staged in LDS three steps at a time.
+// has arrived (see common.h). Producer indices come from the op scan before the kernel, so
+// no workgroup keeps the integer stack; they are staged in LDS three steps at a time.
 //
 // Registers hold the U slice (128 gate columns x K in bf16: 256 per lane at K = 1024,
 // pinned to AGPRs) and little else: every per-pass load goes into LDS by DMA (the h_prev
@@ -224,7 +224,9 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
   // produced at a step <= ts by this lane (already stored) or the initial state
   auto c_fetch = [&](int ts, int pe, int topn) {
     const int bc = min(row0 + 16 * pe + l16, B - 1);
-    const int sn = (topn < -1 || topn > ts) ? -1 : topn;
+    // topn = ts + 1: step ts+1 produces its top itself (a push); the c fetched is unused
+    const int sc = checked_src(topn, ts + 1, a.ctl);
+    const int sn = sc > ts ? -1 : sc;
     const float* cs = (sn < 0 ? a.c0 : a.ccell) + (uint32_t)((max(sn, 0) * B + bc) * H + uc);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // earlier reads of the slot have returned
     dma4(cs, lds_addr(stp(pe, 2) + wave * 64));
@@ -268,13 +270,14 @@ __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
     __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(cv[0]), f2u(cv[1])}, r_c, o4, so4, 0);
     __builtin_amdgcn_raw_buffer_store_b32((uint32_t)f32_to_bf16_bits(hv[0]) | ((uint32_t)f32_to_bf16_bits(hv[1]) << 16),
                                           rx, ok ? e0 * 2u : kOOB, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b128(v4u{f2u(act[0][0]), f2u(act[0][1]), f2u(act[0][2]), f2u(act[0][3])}, rs,
-                                           ok ? e0 * 16u : kOOB, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b128(v4u{f2u(act[1][0]), f2u(act[1][1]), f2u(act[1][2]), f2u(act[1][3])}, rs,
-                                           ok ? e0 * 16u + 16u : kOOB, 0, 0);
     // Algorithm 1's return value: the state at the pointer after step te. c_top here; h_top
-    // of a push here, of the other steps by a gather after the kernel
+    // of a push here, of the other steps by a gather after the kernel. The gate activations
+    // are kept for a push only (the backward reads no others).
     const bool push = topv == te;
+    __builtin_amdgcn_raw_buffer_store_b128(v4u{f2u(act[0][0]), f2u(act[0][1]), f2u(act[0][2]), f2u(act[0][3])}, rs,
+                                           ok && push ? e0 * 16u : kOOB, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(v4u{f2u(act[1][0]), f2u(act[1][1]), f2u(act[1][2]), f2u(act[1][3])}, rs,
+                                           ok && push ? e0 * 16u + 16u : kOOB, 0, 0);
     const float ct0 = push ? cv[0] : pc[0], ct1 = push ? cv[1] : pc[1];
     __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(hv[0]), f2u(hv[1])}, r_ht, push ? o4 : kOOB, so4, 0);
     __builtin_amdgcn_raw_buffer_store_b64(v2u{f2u(ct0), f2u(ct1)}, r_ct, o4, so4, 0);

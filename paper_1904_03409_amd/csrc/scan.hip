@@ -7,97 +7,76 @@
 #include "common.h"
 
 __global__ void __launch_bounds__(256) k_init_ctl(uint32_t* ctl) {
-  for (int i = threadIdx.x; i < CTL_WORDS; i += blockDim.x) ctl[i] = (i == CTL_STATUS) ? 0x7fffffffu : 0u;
+  for (int i = threadIdx.x; i < CTL_WORDS; i += blockDim.x) ctl[i] = (i == CTL_STATUS) ? kStatusOk : 0u;
 }
 
-// Block of 256 threads = 16 columns x 16 time segments. Two passes over each segment:
-// segment sums, a scan of the 16 sums per column in LDS, then the pointer values.
-__global__ void __launch_bounds__(256) k_scan(const int8_t* __restrict__ ops, int T, int B, int32_t* __restrict__ ptr,
-                                              int32_t* __restrict__ depth_end, uint32_t* ctl) {
-  __shared__ int s_sum[16][17];
-  __shared__ int s_first_bad[16], s_first_uf[16], s_maxd;
-  const int c = threadIdx.x & 15, seg = threadIdx.x >> 4;
-  const int b = blockIdx.x * 16 + c;
-  const int L = (T + 15) / 16;
-  const int t0 = seg * L, t1 = min(T, t0 + L);
-  if (threadIdx.x < 16) { s_first_bad[threadIdx.x] = 0x7fffffff; s_first_uf[threadIdx.x] = 0x7fffffff; }
-  if (threadIdx.x == 0) s_maxd = 0;
-  int sum = 0;
-  if (b < B) {
-    for (int t = t0; t < t1; ++t) {
-      int op = ops[(size_t)t * B + b];
-      sum += (op >= -1 && op <= 1) ? op : 0;
-    }
-  }
-  s_sum[c][seg] = sum;
-  __syncthreads();
-  int off = 0;
-  for (int s = 0; s < seg; ++s) off += s_sum[c][s];
-  int first_bad = 0x7fffffff, first_uf = 0x7fffffff, maxd = 0;
-  if (b < B) {
-    if (seg == 0) ptr[b] = 0;
-    int p = off, npush = 0;
-    for (int t = t0; t < t1; ++t) {
-      int op = ops[(size_t)t * B + b];
-      if (op < -1 || op > 1) { if (first_bad == 0x7fffffff) first_bad = t; op = 0; }
-      npush += op == 1;
-      p += op;
-      if (p < 0 && first_uf == 0x7fffffff) first_uf = t;
-      ptr[(size_t)(t + 1) * B + b] = p;
-      maxd = max(maxd, p);
-    }
-    if (t1 == T && t0 < t1) depth_end[b] = p;      // the pointer after the last step
-    if (npush) atomicAdd(&ctl[CTL_NPUSHF], (uint32_t)npush);
-    atomicMin(&s_first_bad[c], first_bad);
-    atomicMin(&s_first_uf[c], first_uf);
-    atomicMax(&s_maxd, maxd);
-  }
-  __syncthreads();
-  if (seg == 0 && b < B) {
-    int fb = s_first_bad[c], fu = s_first_uf[c];
-    int code = 0;
-    if (fb != 0x7fffffff || fu != 0x7fffffff) code = (fu < fb) ? ST_EUNDERFLOW : ST_EOPS;
-    if (code) atomicMin((int*)&ctl[CTL_STATUS], b * 8 + code);
-  }
-  if (threadIdx.x == 0) atomicMax(&ctl[CTL_MAXDEPTH], (uint32_t)s_maxd);
-}
-
-// Producer trace from the ops alone (section 3: the unified update p <- p + op on an
-// integer stack of step indices): top[t][b] = the step that produced the state at the
-// pointer after step t, -1 for the initial state. One thread per batch element keeps its
-// stack of cap slots in LDS (slot 0 = the initial state); the ops of CH steps are staged in
-// LDS at a time. Ops were validated by k_scan, and cap exceeds the deepest pointer.
-__global__ void __launch_bounds__(64) k_trace(const int8_t* __restrict__ ops, int T, int B, int cap,
-                                              int32_t* __restrict__ top) {
-  constexpr int CH = 64;
-  extern __shared__ int s_stk[];                  // [blockDim.x][cap]
-  __shared__ int8_t s_ops[CH][64];
-  const int R = blockDim.x;
-  const int b = blockIdx.x * R + threadIdx.x;
-  int* stk = s_stk + threadIdx.x * cap;
-  int p = 0, tp = -1;
-  stk[0] = -1;
+// Op validation, pointer scan and producer trace in one pass (section 3: the unified update
+// p <- p + op on an integer stack of step indices). One thread per batch element walks its
+// op stream: ptr[t+1][b] = p after step t, top[t][b] = the step that produced the state at
+// the pointer after step t (-1 = the initial state). The element's stack of step indices
+// has cap = T + 1 slots (slot 0 = the initial state), in LDS (LDS = true: blockDim.x stacks of
+// cap ints) or in the work space (gstack [B][cap]). Each thread loads its next
+// CH ops as independent byte loads (consecutive lanes read consecutive bytes), so a chunk
+// costs one memory round trip. An invalid op is reported (EOPS) and walked as a hold; a pop
+// at p = 0 is reported (EUNDERFLOW) and walked as a hold, so every trace value stays a valid
+// producer index even then. Also: the number of pushes (CTL_NPUSHF), the deepest pointer
+// (CTL_MAXDEPTH) and the pointer after the last step (depth_end, for the backward).
+template <bool LDS>
+__global__ void __launch_bounds__(64) k_scan(const int8_t* __restrict__ ops, int T, int B, int cap,
+                                             int32_t* __restrict__ ptr, int32_t* __restrict__ top,
+                                             int32_t* __restrict__ depth_end, int32_t* __restrict__ gstack,
+                                             uint32_t* ctl) {
+  constexpr int CH = 32;
+  extern __shared__ int s_stk[];
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  // LDS stacks are indexed through s_stk itself (LDS instructions: a pop's read does not wait
+  // for the pointer and trace stores in flight)
+  const size_t sbase = LDS ? (size_t)threadIdx.x * cap : (size_t)b * cap;
+  auto stk = [&](int i) -> int& { return LDS ? s_stk[sbase + i] : gstack[sbase + i]; };
+  int p = 0, tp = -1, npush = 0, maxd = 0;
+  int first_bad = 0x7fffffff, first_uf = 0x7fffffff;
+  stk(0) = -1;
+  ptr[b] = 0;
   for (int t0 = 0; t0 < T; t0 += CH) {
-    const int n = min(CH, T - t0);
-    __syncthreads();
-    for (int i = 0; i < n; ++i) s_ops[i][threadIdx.x] = b < B ? ops[(size_t)(t0 + i) * B + b] : (int8_t)0;
-    __syncthreads();
-    if (b < B) {
-      for (int i = 0; i < n; ++i) {
-        const int op = s_ops[i][threadIdx.x];
-        if (op == 1) {
-          ++p;
-          if (p < cap) stk[p] = t0 + i;
-          tp = t0 + i;
-        } else if (op == -1) {
-          p = p > 0 ? p - 1 : 0;
-          tp = stk[min(p, cap - 1)];
-        }
-        top[(size_t)(t0 + i) * B + b] = tp;
+    int8_t v[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) v[i] = (t0 + i < T) ? ops[(size_t)(t0 + i) * B + b] : (int8_t)0;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int t = t0 + i;
+      if (t >= T) break;
+      int op = v[i];
+      if (op < -1 || op > 1) {
+        if (first_bad == 0x7fffffff) first_bad = t;
+        op = 0;
       }
+      if (op == 1) {
+        ++p;
+        stk(p) = t;
+        tp = t;
+        ++npush;
+      } else if (op == -1) {
+        if (p == 0) {
+          if (first_uf == 0x7fffffff) first_uf = t;
+        } else {
+          --p;
+          tp = stk(p);
+        }
+      }
+      maxd = max(maxd, p);
+      ptr[(size_t)(t + 1) * B + b] = p;
+      top[(size_t)t * B + b] = tp;
     }
   }
+  depth_end[b] = p;
+  if (npush) atomicAdd(&ctl[CTL_NPUSHF], (uint32_t)npush);
+  atomicMax(&ctl[CTL_MAXDEPTH], (uint32_t)maxd);
+  if (first_bad != 0x7fffffff || first_uf != 0x7fffffff)
+    atomicMin((int*)&ctl[CTL_STATUS], b * 8 + (first_uf < first_bad ? ST_EUNDERFLOW : ST_EOPS));
 }
+template __global__ void k_scan<true>(const int8_t*, int, int, int, int32_t*, int32_t*, int32_t*, int32_t*, uint32_t*);
+template __global__ void k_scan<false>(const int8_t*, int, int, int, int32_t*, int32_t*, int32_t*, int32_t*, uint32_t*);
 
 // h_top / c_top materialisation: the state returned at step t (Algorithm 1's return value)
 // is the one produced at step top[t][b], or the initial state when top is -1.
@@ -105,7 +84,7 @@ __global__ void __launch_bounds__(64) k_trace(const int8_t* __restrict__ ops, in
 // are (the wide forward kernel writes them).
 __global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ top, const float* __restrict__ cellv,
                                                     const float* __restrict__ init, float* __restrict__ out, int T,
-                                                    int B, int H, int skip_push) {
+                                                    int B, int H, int skip_push, uint32_t* ctl) {
   const size_t n = (size_t)T * B * H;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     size_t tb = i / H;
@@ -114,7 +93,7 @@ __global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ 
     int s = top[tb];
     int t = (int)(tb / B);
     if (skip_push && s == t) continue;
-    if (s < -1 || s > t) { out[i] = __builtin_nanf(""); continue; }   // not a valid producer
+    s = checked_src(s, t, ctl);
     out[i] = (s < 0) ? init[(size_t)b * H + u] : cellv[((size_t)s * B + b) * H + u];
   }
 }
@@ -124,31 +103,27 @@ __global__ void __launch_bounds__(256) k_gather_top(const int32_t* __restrict__ 
 __global__ void __launch_bounds__(256) k_gather_top4(const int32_t* __restrict__ top, const float* __restrict__ hcell,
                                                      const float* __restrict__ h0, float* __restrict__ htop,
                                                      const float* __restrict__ ccell, const float* __restrict__ c0,
-                                                     float* __restrict__ ctop, int T, int B, int H, int skip_h) {
+                                                     float* __restrict__ ctop, int T, int B, int H, int skip_h,
+                                                     uint32_t* ctl) {
   const int H4 = H / 4;
   const size_t n = (size_t)T * B * H4;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     const size_t tb = i / H4;
     const int u4 = (int)(i - tb * H4);
     const int b = (int)(tb % B), t = (int)(tb / B);
-    const int s = top[tb];
-    const bool bad = s < -1 || s > t;             // not a valid producer
-    const float nan = __builtin_nanf("");
-    const size_t src = (s < 0 || bad) ? (size_t)b * H4 + u4 : ((size_t)s * B + b) * H4 + u4;
-    if (htop && !(skip_h && s == t)) {
-      const float4 v = bad ? float4{nan, nan, nan, nan} : (s < 0 ? ((const float4*)h0)[src] : ((const float4*)hcell)[src]);
-      ((float4*)htop)[i] = v;
-    }
-    if (ctop) {
-      const float4 v = bad ? float4{nan, nan, nan, nan} : (s < 0 ? ((const float4*)c0)[src] : ((const float4*)ccell)[src]);
-      ((float4*)ctop)[i] = v;
-    }
+    const int s0 = top[tb];
+    const int s = checked_src(s0, t, ctl);
+    const size_t src = s < 0 ? (size_t)b * H4 + u4 : ((size_t)s * B + b) * H4 + u4;
+    if (htop && !(skip_h && s0 == t)) ((float4*)htop)[i] = s < 0 ? ((const float4*)h0)[src] : ((const float4*)hcell)[src];
+    if (ctop) ((float4*)ctop)[i] = s < 0 ? ((const float4*)c0)[src] : ((const float4*)ccell)[src];
   }
 }
 
-// W [I][4H] (gate-major columns) -> Wp [I][4H] gate-interleaved, as fp32 or bf16.
+// W [I][4H] (gate-major columns) -> Wp [I][4H] gate-interleaved, as fp32 or bf16, and its
+// transpose WpT [4H][I] in bf16 (each output may be null).
 __global__ void __launch_bounds__(256) k_permute_w(const float* __restrict__ W, float* __restrict__ Wp32,
-                                                   bf16_t* __restrict__ Wp16, int I, int H) {
+                                                   bf16_t* __restrict__ Wp16, bf16_t* __restrict__ WpT16, int I,
+                                                   int H) {
   const size_t n = (size_t)I * 4 * H;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     size_t row = i / (4 * (size_t)H);
@@ -156,6 +131,7 @@ __global__ void __launch_bounds__(256) k_permute_w(const float* __restrict__ W, 
     float v = W[row * 4 * H + perm_to_orig(np, H)];
     if (Wp32) Wp32[i] = v;
     if (Wp16) Wp16[i] = f32_to_bf16_bits(v);
+    if (WpT16) WpT16[(size_t)np * I + row] = f32_to_bf16_bits(v);
   }
 }
 
@@ -197,78 +173,16 @@ __global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ in, b
     out[i] = f32_to_bf16_bits(in[i]);
 }
 
-// Clears the backward's control words: slot counters, group barrier counters, abort flags.
+// Clears the backward's control words: slot counters, group barrier counters, the wait flags
+// and the index flag (the op status of the forward stays: the backward reports only its own).
 __global__ void __launch_bounds__(256) k_zero_ctl_bwd(uint32_t* __restrict__ ctl) {
   for (int i = threadIdx.x; i < 16; i += blockDim.x) ctl[CTL_XCC_SLOT_B + i] = 0u;
   for (int i = threadIdx.x; i < 16 * MAX_GROUPS; i += blockDim.x) ctl[CTL_BAR_B + i] = 0u;
-  if (threadIdx.x < 2) ctl[CTL_ABORT + threadIdx.x] = 0u;
-}
-
-// Operand of the input-projection GEMM: out [rows][KA] = [x | nones columns of 1 | 0], in
-// fp32 (out32) or bf16 (out16, x rounded as k_to_bf16 does).
-__global__ void __launch_bounds__(256) k_augment_x(const float* __restrict__ x, size_t rows, int I, int KA, int nones,
-                                                   float* __restrict__ out32, bf16_t* __restrict__ out16) {
-  // eight output columns per thread when I and KA are multiples of 8 and x is 16-byte aligned
-  if (I % 8 == 0 && KA % 8 == 0 && ((uintptr_t)x & 15u) == 0) {
-    const int K8 = KA / 8;
-    const size_t n8 = rows * (size_t)K8;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (size_t)gridDim.x * blockDim.x) {
-      const size_t r = i / (size_t)K8;
-      const int c = (int)(i - r * (size_t)K8) * 8;
-      float v[8];
-      if (c < I) {
-        const float4 a = *(const float4*)(x + r * (size_t)I + c), b = *(const float4*)(x + r * (size_t)I + c + 4);
-        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = (c + j < I + nones) ? 1.f : 0.f;
-      }
-      if (out32) {
-        *(float4*)(out32 + r * (size_t)KA + c) = float4{v[0], v[1], v[2], v[3]};
-        *(float4*)(out32 + r * (size_t)KA + c + 4) = float4{v[4], v[5], v[6], v[7]};
-      } else {
-        bf16_t q[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) q[j] = f32_to_bf16_bits(v[j]);
-        *(uint4*)(out16 + r * (size_t)KA + c) = *(const uint4*)q;
-      }
-    }
-    return;
-  }
-  const size_t n = rows * (size_t)KA;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-    const size_t r = i / (size_t)KA;
-    const int c = (int)(i - r * (size_t)KA);
-    const float v = c < I ? x[r * (size_t)I + c] : (c < I + nones ? 1.f : 0.f);
-    if (out32) out32[i] = v;
-    else out16[i] = f32_to_bf16_bits(v);
-  }
-}
-
-// Bias rows under the gate-interleaved Wp: row j < nparts holds the j-th part of b (fp32: b
-// itself; bf16: b = p0 + p1 + p2 with p0 = bf16(b), p1 = bf16(b - p0), p2 = bf16(b - p0 - p1),
-// each difference exact in fp32), the other rows up to nrows are 0.
-__global__ void __launch_bounds__(256) k_bias_rows(const float* __restrict__ b, int H, int nparts, int nrows,
-                                                   float* __restrict__ out32, bf16_t* __restrict__ out16) {
-  const int H4 = 4 * H;
-  const size_t n = (size_t)nrows * H4;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-    const int j = (int)(i / (size_t)H4);
-    const int col = (int)(i - (size_t)j * H4);
-    float rem = b ? b[perm_to_orig(col, H)] : 0.f;
-    float part = 0.f;
-    if (out32) {
-      part = j == 0 ? rem : 0.f;
-      out32[i] = part;
-    } else {
-      bf16_t bits = 0;
-      for (int q = 0; q <= j && q < nparts; ++q) {
-        bits = f32_to_bf16_bits(rem);
-        const float pv = __uint_as_float((uint32_t)bits << 16);
-        if (q < j) rem -= pv;
-      }
-      out16[i] = j < nparts ? bits : (bf16_t)0;
-    }
+  if (threadIdx.x == 0) {
+    ctl[CTL_STATUS] = kStatusOk;
+    ctl[CTL_ABORT] = 0u;
+    ctl[CTL_TIMEOUT] = 0u;
+    ctl[CTL_BADIDX] = 0u;
   }
 }
 
@@ -353,44 +267,15 @@ __global__ void __launch_bounds__(256) k_zero_nonpush_rows(const int8_t* __restr
 __global__ void __launch_bounds__(256) k_gather_hprev(const int32_t* __restrict__ top, const float* __restrict__ hcell,
                                                       const float* __restrict__ h0, const int32_t* __restrict__ prow,
                                                       const uint32_t* __restrict__ count, float* __restrict__ out,
-                                                      int T, int B, int H) {
+                                                      int T, int B, int H, uint32_t* ctl) {
   const size_t n = (size_t)min(*count, (uint32_t)T * (uint32_t)B) * H;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     const size_t k = i / H;
     const int u = (int)(i - k * H);
     const int tb = prow[k];
     const int t = tb / B, b = tb - t * B;
-    int s = (t == 0) ? -1 : top[tb - B];
-    if (s < -1 || s >= t) s = -1;                 // only a valid producer is ever indexed
+    const int s = (t == 0) ? -1 : checked_src(top[tb - B], t - 1, ctl);
     out[i] = (s < 0) ? h0[(size_t)b * H + u] : hcell[((size_t)s * B + b) * H + u];
-  }
-}
-
-// Row gather / scatter over the push rows (k < *count): dst[k] = src[prow[k]] and
-// dst[prow[k]] = src[k], rows of `cols` floats (four at a time when cols % 4 == 0).
-__global__ void __launch_bounds__(256) k_gather_rows(const float* __restrict__ src, const int32_t* __restrict__ prow,
-                                                     const uint32_t* __restrict__ count, size_t max_rows, int cols,
-                                                     int scatter, float* __restrict__ dst) {
-  const size_t rows = min((size_t)*count, max_rows);
-  if (cols % 4 == 0) {
-    const int c4 = cols / 4;
-    const size_t n = rows * c4;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-      const size_t k = i / c4;
-      const int c = (int)(i - k * c4);
-      const size_t r = (size_t)prow[k];
-      if (scatter) ((float4*)dst)[r * c4 + c] = ((const float4*)src)[i];
-      else ((float4*)dst)[i] = ((const float4*)src)[r * c4 + c];
-    }
-  } else {
-    const size_t n = rows * cols;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-      const size_t k = i / cols;
-      const int c = (int)(i - k * cols);
-      const size_t r = (size_t)prow[k];
-      if (scatter) dst[r * cols + c] = src[i];
-      else dst[i] = src[r * cols + c];
-    }
   }
 }
 
@@ -405,7 +290,7 @@ __global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__
                                                         const int32_t* __restrict__ prow,
                                                         const uint32_t* __restrict__ count, int ldo,
                                                         const int32_t* __restrict__ gtop, int B,
-                                                        bf16_t* __restrict__ out) {
+                                                        bf16_t* __restrict__ out, uint32_t* ctl) {
   __shared__ bf16_t tile[64][66];
   const int rows = (int)min(*count, (uint32_t)ldo);
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
@@ -418,8 +303,7 @@ __global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__
       const int pr = prow[r];
       if (gtop) {
         const int t = pr / B, b = pr - t * B;
-        int s = (t == 0) ? -1 : gtop[(size_t)pr - B];
-        if (s < -1 || s >= t) s = -1;                        // only a valid producer is ever indexed
+        const int s = (t == 0) ? -1 : checked_src(gtop[(size_t)pr - B], t - 1, ctl);
         v = ((const bf16_t*)src)[((size_t)(s + 1) * B + b) * ld + c];
       } else if (src_f32) {
         v = f32_to_bf16_bits(((const float*)src)[(size_t)pr * ld + c]);

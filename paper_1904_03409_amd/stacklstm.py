@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libstacklstm.so")
 SLSTM_FP32 = 0
 SLSTM_BF16_GEMM = 1
 STATUS = {0: "SLSTM_OK", 1: "SLSTM_EINVAL", 2: "SLSTM_EOPS", 3: "SLSTM_EUNDERFLOW", 4: "SLSTM_EWORKSPACE",
-          5: "SLSTM_ENORESIDENT", 6: "SLSTM_EDEVICE", 7: "SLSTM_ETIMEOUT"}
+          5: "SLSTM_ENORESIDENT", 6: "SLSTM_EDEVICE", 7: "SLSTM_ETIMEOUT", 8: "SLSTM_EINDEX"}
 EXPORTS = ("stacklstm_workspace_bytes", "stacklstm_fwd", "stacklstm_bwd", "stacklstm_sync_status",
            "stacklstm_status_string", "stacklstm_plan")
 

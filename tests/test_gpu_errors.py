@@ -56,15 +56,16 @@ def test_workspace_dims_and_null():
 
 def test_spin_limit_timeout_reported():
     """A one-poll barrier limit forced from the host: the kernels give up, every
-    workgroup leaves its loop, and the call reports SLSTM_ETIMEOUT."""
+    workgroup leaves its loop, and the call reports SLSTM_ETIMEOUT (also through
+    stacklstm_sync_status)."""
     need_gpu()
+    from paper_1904_03409_amd import stacklstm as s
     wl = wk.make("parser")
     r, rc = _run(wl, spin_limit=1)
-    assert rc in (0, 7)
     assert rc == 7
+    assert s.stacklstm_sync_status(r.workspace) == 7
     torch.cuda.synchronize()
     # the same buffers run normally afterwards
-    from paper_1904_03409_amd import stacklstm as s
     r2, rc2 = _run(wl)
     assert rc2 == 0
     assert s.stacklstm_sync_status(r2.workspace) == 0
@@ -101,3 +102,30 @@ def test_empty_T():
     assert np.all(out["ptr"] == 0)
     for k in ("dW", "dU", "db", "dh0", "dc0"):
         assert np.all(out[k] == 0)
+
+
+@pytest.mark.parametrize("precision", [0, 1])
+def test_corrupted_top_reported(precision):
+    """A producer table that is not the forward's (indices past their step, below -1) passed
+    to stacklstm_bwd: every kernel still finishes (each bad index is replaced by -1 before any
+    access), and the call returns SLSTM_EINDEX instead of OK. The same work space then runs a
+    normal backward with status OK."""
+    need_gpu()
+    from paper_1904_03409_amd import stacklstm as s
+    wl = wk.make("tiny")
+    r, rc = _run(wl, precision=precision)
+    assert rc == 0
+    torch.cuda.synchronize()
+    good = r.top.clone()
+    bad = good.clone()
+    bad[5:, 1] = 1000                 # past every step
+    bad[9, 3] = -7                    # below the initial state's -1
+    print(f"[gpu] corrupted top, tiny, precision={precision}", flush=True)
+    rc = s.stacklstm_bwd(r.dims, r.x, r.ops, r.W, r.U, r.h0, r.c0, r.h_cell, r.c_cell, bad, r.workspace, r.dh_top,
+                         r.dc_top, r.dx, r.dW, r.dU, r.db, r.dh0, r.dc0, check=False)
+    assert rc == 8
+    assert s.stacklstm_sync_status(r.workspace) == 8
+    rc = s.stacklstm_bwd(r.dims, r.x, r.ops, r.W, r.U, r.h0, r.c0, r.h_cell, r.c_cell, good, r.workspace, r.dh_top,
+                         r.dc_top, r.dx, r.dW, r.dU, r.db, r.dh0, r.dc0, check=False)
+    assert rc == 0
+    assert s.stacklstm_sync_status(r.workspace) == 0
