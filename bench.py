@@ -67,7 +67,7 @@ def timed_run(wl, precision, steps, warmup, torch):
     total_ms = start.elapsed_time(stop)
     phase = {}
     f = ctypes.c_float()
-    pairs = [(0, 1, "scan+sync"), (1, 2, "xw_gemm+prep"), (2, 3, "rec_fwd"), (3, 4, "top_gather"),
+    pairs = [(0, 1, "scan"), (1, 2, "xw_gemm+prep"), (2, 3, "rec_fwd"), (3, 4, "top_gather"),
              (5, 6, "rec_bwd"), (6, 7, "dW+db"), (7, 8, "dU"), (8, 9, "dx"), (4, 5, "bwd_prep")]
     for a, b, name in pairs:
         acc = 0.0
@@ -209,30 +209,54 @@ def copy_probe(torch, nbytes=256 << 20, reps=3):
     print(f"[bench] copy probe: {reps} x {nbytes} bytes (elementwise b = a * 1)", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(wl, target_s=12.0):
-    """The oracle (float32 instantiation, OpenMP over batch elements) on a bounded sample."""
+def normwise(got, ref):
+    ref = np.asarray(ref, np.float64)
+    scale = float(np.abs(ref).max()) if ref.size else 0.0
+    return float(np.abs(np.asarray(got, np.float64) - ref).max() / (scale if scale > 0 else 1.0)) if ref.size else 0.0
+
+
+def cpu_baseline(wl, gpu_out=None, target_s=12.0):
+    """The oracle (float32 instantiation, OpenMP over batch elements, built with -march=native
+    on this host) timed on a bounded sample. Its outputs for the sample are then compared with
+    the benched GPU run's outputs of the same columns: traces bit for bit, every per-element
+    float normwise (weight gradients sum over the whole batch and are not compared here)."""
     import oracle
+    oracle.build(force=True, native=True)
     th = oracle.max_threads()
     n0 = min(wl.B, max(th, 8))
     t0 = time.perf_counter()
-    oracle.run(wl, sel=np.arange(n0, dtype=np.int32), mode="f32", threads=th)
+    oracle.run(wl, sel=np.arange(n0, dtype=np.int32), mode="f32", threads=th, native=True)
     dt0 = time.perf_counter() - t0
     # sample size for about target_s of CPU work, then the median of three runs of it
     # (one run when a single run already takes more than a third of that)
     n = n0 if dt0 >= target_s / 4 else int(min(wl.B, max(n0, n0 * target_s / max(dt0, 1e-3))))
     est = dt0 * n / n0
     times = []
+    ref = None
     for _ in range(3 if 3 * est <= 1.5 * target_s else 1):
         t0 = time.perf_counter()
-        oracle.run(wl, sel=np.arange(n, dtype=np.int32), mode="f32", threads=th)
+        ref = oracle.run(wl, sel=np.arange(n, dtype=np.int32), mode="f32", threads=th, native=True)
         times.append(time.perf_counter() - t0)
     dt = float(np.median(times))
     pushes = int((wl.ops[:, :n] == 1).sum())
     model, ncpu = host_cpu()
-    return {"value": n * wl.T / dt, "unit": "element-steps/s", "cores": th, "kind": "oracle",
-            "push_steps_per_s": pushes / dt, "host_cpus": ncpu, "cpu_model": model,
-            "sample": f"fwd+bwd of the first {n} of {wl.B} batch elements (all T={wl.T} steps), float32 oracle "
-                      f"(-O3 -march=native -fopenmp, {th} threads), median of {len(times)} runs: {dt:.2f} s"}
+    out = {"value": n * wl.T / dt, "unit": "element-steps/s", "cores": th, "kind": "oracle",
+           "push_steps_per_s": pushes / dt, "host_cpus": ncpu, "cpu_model": model,
+           "sample": f"fwd+bwd of the first {n} of {wl.B} batch elements (all T={wl.T} steps), float32 oracle "
+                     f"(gcc -O3 -march=native -fopenmp on this host, {th} threads), median of {len(times)} runs: "
+                     f"{dt:.2f} s"}
+    if gpu_out is not None:
+        sel = slice(0, n)
+        errs = {k: normwise(gpu_out[k][:, sel], ref[k]) for k in ("h_top", "c_top", "dx")}
+        errs.update({k: normwise(gpu_out[k][sel], ref[k]) for k in ("dh0", "dc0")})
+        push = wl.ops[:, sel] == 1
+        errs["h_cell_push"] = normwise(gpu_out["h_cell"][:, sel][push], ref["h_cell"][push])
+        out["gpu_check"] = {
+            "columns": n, "trace_equal": bool(np.array_equal(gpu_out["ptr"][:, sel], ref["ptr"]) and
+                                               np.array_equal(gpu_out["top"][:, sel], ref["top"])),
+            "max_normwise_err": max(errs.values()), "tolerance": 1e-5,
+            "parity": bool(max(errs.values()) <= 1e-5), "errors": {k: float(f"{v:.3g}") for k, v in errs.items()}}
+    return out
 
 
 def amdahl_fit(batches, speedups):
@@ -284,6 +308,7 @@ def main():
     ap.add_argument("--precision", choices=["fp32", "bf16"], default=None)
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-GEMM run of the same shape")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extra", action="store_true", help="skip the deep and thru workloads of the default run")
     ap.add_argument("--layers", type=int, default=1,
                     help="stacked StackLSTM layers sharing the op streams (the stack element holds every layer)")
     ap.add_argument("--sweep", action="store_true",
@@ -322,22 +347,15 @@ def main():
     wl = workloads.make(args.config)
     prec = wl.precision if args.precision is None else (0 if args.precision == "fp32" else 1)
     dname = "f32" if prec == 0 else "bf16"
-    print(f"[bench] {args.config} T={wl.T} B={wl.B} I={wl.I} H={wl.H} {dname} steps={args.steps} "
-          f"warmup={args.warmup}", file=sys.stderr, flush=True)
-    run, total_ms, wall, phase = timed_run(wl, prec, args.steps, args.warmup, torch)
-    per_step = phase.pop("_per_step_ms")
-    ms = total_ms / args.steps
-    value = wl.B * wl.T / (ms / 1e3)
+    m = measure(wl, prec, args.steps, args.warmup, torch, args.config, keep_outputs=not args.no_cpu)
+    ms = m["ms_per_step"]
     fl = flops(wl)
+    phase = m["phases_ms"]
     kern = max(fl, key=lambda k: phase.get(k, 0.0))
     achieved = fl[kern] / (phase[kern] / 1e3) / 1e12
-    rec_util = (fl["rec_fwd"] + fl["rec_bwd"]) / ((phase["rec_fwd"] + phase["rec_bwd"]) / 1e3) / 1e12 / PEAK[dname]
-    fx = executed_flops(wl)
-    all_util = sum(fx.values()) / (ms / 1e3) / 1e12 / PEAK[dname]
-    st = wl.op_stats()
     out = {
         "metric": "fwd+bwd batch·timesteps/sec at B=256,H=512; % MFMA peak",
-        "value": value, "unit": "element-steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "value": m["value"], "unit": "element-steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dname,
         "data": "synthetic",
         "config": {"workload": f"{args.config}: StackLSTM fwd+bwd, B={wl.B} T={wl.T} I={wl.I} H={wl.H}, "
@@ -345,34 +363,67 @@ def main():
                    "global_batch": wl.B, "seq_len": wl.T, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "mfma", "kernel": kern, "achieved": achieved, "peak": PEAK[dname], "unit": "TFLOP/s",
                      "frac": achieved / PEAK[dname], "traffic": stored_traffic(args.config, dname, kern)},
-        "phases_ms": {k: round(v, 4) for k, v in phase.items()},
-        "step_ms_median": float(np.median(per_step)), "step_ms_min": float(np.min(per_step)),
-        "recurrent_mfma_frac": rec_util, "overall_mfma_frac": all_util,
-        "executed_tflops": {k: round(fx[k] / (phase[k] / 1e3) / 1e12, 2) for k in fx if phase.get(k)},
-        "push_steps_per_s": st["push_steps"] / (ms / 1e3), "op_stats": st, "wall_s_timed": wall,
     }
-    step_bytes = stored_step_traffic(args.config, dname)
-    out["hbm_gb_s_whole_run"] = None if step_bytes is None else step_bytes / (ms / 1e3) / 1e9
-    del run
+    out.update({k: v for k, v in m.items() if k not in ("value", "ms_per_step", "out")})
+    gpu_out = m.get("out")
     torch.cuda.empty_cache()
+    extra = []
     if not args.no_bf16 and prec == 0 and wl.H <= 1024:
-        run2, tot2, _, ph2 = timed_run(wl, 1, args.steps, args.warmup, torch)
-        ps2 = ph2.pop("_per_step_ms")
-        ms2 = tot2 / args.steps
-        r2 = (fl["rec_fwd"] + fl["rec_bwd"]) / ((ph2["rec_fwd"] + ph2["rec_bwd"]) / 1e3) / 1e12 / PEAK["bf16"]
-        sb2 = stored_step_traffic(args.config, "bf16")
-        out["bf16_gemm"] = {"value": wl.B * wl.T / (ms2 / 1e3), "ms_per_step": ms2,
-                            "step_ms_median": float(np.median(ps2)), "step_ms_min": float(np.min(ps2)),
-                            "hbm_gb_s_whole_run": None if sb2 is None else sb2 / (ms2 / 1e3) / 1e9,
-                            "recurrent_mfma_frac": r2, "overall_mfma_frac": sum(fx.values()) / (ms2 / 1e3) / 1e12 / PEAK["bf16"],
-                            "phases_ms": {k: round(v, 4) for k, v in ph2.items()}}
-        del run2
+        extra.append(("bf16_gemm", wl, 1, args.config))
+    if args.config == "large" and not args.no_extra:
+        # the other full-size workloads: deep-stack stress (fp32) and throughput (bf16-GEMM)
+        extra.append(("deep", workloads.make("deep"), 0, "deep"))
+        extra.append(("thru", workloads.make("thru"), 1, "thru"))
+    for key, wlx, px, cname in extra:
+        mx = measure(wlx, px, args.steps, args.warmup, torch, cname)
+        mx.pop("out", None)
+        mx["config"] = f"{cname}: B={wlx.B} T={wlx.T} I={wlx.I} H={wlx.H}, {'f32' if px == 0 else 'bf16'} GEMM operands"
+        out[key] = mx
+        torch.cuda.empty_cache()
     if args.copy_probe:
         copy_probe(torch)
     if not args.no_cpu:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"] = cpu_baseline(wl, gpu_out=gpu_out)
     print(json.dumps(out), flush=True)
+
+
+def measure(wl, prec, steps, warmup, torch, cname, keep_outputs=False):
+    """Times `steps` fwd+bwd steps of one workload and checks the run: the status of the last
+    calls (stacklstm_sync_status) and the pointer trace of every column against the prefix
+    sum of the ops."""
+    from paper_1904_03409_amd.stacklstm import stacklstm_sync_status
+    dname = "f32" if prec == 0 else "bf16"
+    print(f"[bench] {cname} T={wl.T} B={wl.B} I={wl.I} H={wl.H} {dname} steps={steps} warmup={warmup}",
+          file=sys.stderr, flush=True)
+    run, total_ms, wall, phase = timed_run(wl, prec, steps, warmup, torch)
+    status = stacklstm_sync_status(run.workspace)
+    per_step = phase.pop("_per_step_ms")
+    ms = total_ms / steps
+    fl, fx = flops(wl), executed_flops(wl)
+    peak = PEAK[dname]
+    rec_t = (phase["rec_fwd"] + phase["rec_bwd"]) / 1e3
+    got = run.results() if keep_outputs else {"ptr": run.ptr.cpu().numpy()}
+    ptr = np.vstack([np.zeros((1, wl.B), np.int64), np.cumsum(wl.ops.astype(np.int64), axis=0)])
+    st = wl.op_stats()
+    step_bytes = stored_step_traffic(cname, dname)
+    m = {"value": wl.B * wl.T / (ms / 1e3), "ms_per_step": ms, "dtype": dname,
+         "status": {"code": int(status), "ptr_trace_equal_prefix_sum": bool(np.array_equal(got["ptr"], ptr))},
+         "phases_ms": {k: round(v, 4) for k, v in phase.items()},
+         "step_ms_median": float(np.median(per_step)), "step_ms_min": float(np.min(per_step)),
+         # algorithmic: every element-step's 2*4H*H per recurrent contraction; executed: the
+         # backward contraction over push rows only (dA is exactly 0 on the others)
+         "recurrent_mfma_frac": (fl["rec_fwd"] + fl["rec_bwd"]) / rec_t / 1e12 / peak,
+         "recurrent_mfma_frac_executed": (fx["rec_fwd"] + fx["rec_bwd"]) / rec_t / 1e12 / peak,
+         "overall_mfma_frac": sum(fx.values()) / (ms / 1e3) / 1e12 / peak,
+         "executed_tflops": {k: round(fx[k] / (phase[k] / 1e3) / 1e12, 2) for k in fx if phase.get(k)},
+         "push_steps_per_s": st["push_steps"] / (ms / 1e3), "op_stats": st, "wall_s_timed": wall,
+         "hbm_gb_s_whole_run": None if step_bytes is None else step_bytes / (ms / 1e3) / 1e9,
+         "out": got if keep_outputs else None}
+    if status != 0:
+        print(f"[bench] {cname}: status {status} after the timed run", file=sys.stderr, flush=True)
+    del run
+    return m
 
 
 if __name__ == "__main__":

@@ -147,11 +147,25 @@ int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream);
 /* Static text for a status code. */
 const char* stacklstm_status_string(int status);
 
-/* Launch configuration of the forward recurrent kernel chosen for `d`: fills groups,
- * workgroups per group, rows per group and K chunks (the backward kernel may use larger
- * groups); returns a status like the entry points. Informational. */
-int stacklstm_plan(const slstm_dims* d, int32_t* groups, int32_t* wg_per_group, int32_t* rows_per_group,
-                   int32_t* k_chunks);
+/* Launch configuration the library chooses for `d` (informational; tests use it to reach
+ * every kernel variant). */
+typedef struct {
+  int32_t groups;          /* forward: batch groups (one per XCC slot) */
+  int32_t wg_per_group;    /* forward: workgroups per group */
+  int32_t rows_per_group;  /* forward: batch rows per group (16 * fwd_tiles) */
+  int32_t k_chunks;        /* K chunks of the recurrent contraction in use */
+  int32_t fwd_kernel;      /* 0 plain, 1 pipelined (two LDS tile buffers), 2 wide (bf16, H > 512) */
+  int32_t fwd_tiles;       /* forward: 16-row tiles per group */
+  int32_t k_chunk_cap;     /* K chunks compiled into the kernels (power of two >= k_chunks) */
+  int32_t occupancy;       /* workgroups per CU the recurrent kernels are compiled for */
+  int32_t bwd_groups;      /* backward: batch groups */
+  int32_t bwd_tiles;       /* backward: 16-row tiles per group */
+  int32_t bwd_direct;      /* backward: dA rows staged in LDS by DMA (1) or read into registers (0) */
+  int32_t reserved;
+} slstm_plan;
+
+/* Fills `out` for `d`; returns a status like the entry points. */
+int stacklstm_plan(const slstm_dims* d, slstm_plan* out);
 
 #ifdef __cplusplus
 }

@@ -18,7 +18,11 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "stacklstm_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# the timed CPU baseline: the same source built for the host it runs on (-march=native), at
+# run time on that host (a library built elsewhere could use instructions this CPU lacks)
+_LIB_NATIVE = os.path.join(_HERE, "liboracle_native.so")
 _lib = None
+_lib_native = None
 
 ERRORS = {1: "EINVAL", 2: "EOPS", 3: "EUNDERFLOW"}
 
@@ -29,36 +33,46 @@ class OracleError(RuntimeError):
         self.code = code
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (plain -O3, OpenMP over batch elements)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
-        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-shared", "-fPIC", "-Wall", "-o", tmp, _SRC, "-lm"],
-                              cwd=_HERE)
-        os.replace(tmp, _LIB)
-    return _LIB
+def build(force: bool = True, native: bool = False) -> str:
+    """Compile the oracle with gcc (-O3, OpenMP over batch elements; with ``native`` also
+    -march=native, for the timed baseline on the machine that times it)."""
+    out = _LIB_NATIVE if native else _LIB
+    if force or not os.path.exists(out):
+        tmp = out + f".tmp{os.getpid()}"
+        flags = ["-O3", "-march=native", "-fopenmp"] if native else ["-O3", "-fopenmp"]
+        subprocess.check_call(["gcc", *flags, "-shared", "-fPIC", "-Wall", "-o", tmp, _SRC, "-lm"], cwd=_HERE)
+        os.replace(tmp, out)
+    return out
 
 
-def _load():
-    global _lib
+def _load(native: bool = False):
+    global _lib, _lib_native
+    if native:
+        if _lib_native is None:
+            build(force=True, native=True)
+            _lib_native = _bind(ctypes.CDLL(_LIB_NATIVE))
+        return _lib_native
     if _lib is None:
         if not os.path.exists(_LIB):
             build()
-        lib = ctypes.CDLL(_LIB)
-        P = ctypes.c_void_p
-        i = ctypes.c_int
-        for sfx in ("f64", "f32"):
-            f = getattr(lib, f"oracle_run_{sfx}")
-            f.restype = i
-            f.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, P, P, i, i, i] + [P] * 12
-            g = getattr(lib, f"oracle_alg1_{sfx}")
-            g.restype = i
-            g.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i] + [P] * 6
-        lib.oracle_round_bf16.restype = None
-        lib.oracle_round_bf16.argtypes = [P, P, ctypes.c_long]
-        lib.oracle_max_threads.restype = i
-        _lib = lib
+        _lib = _bind(ctypes.CDLL(_LIB))
     return _lib
+
+
+def _bind(lib):
+    P = ctypes.c_void_p
+    i = ctypes.c_int
+    for sfx in ("f64", "f32"):
+        f = getattr(lib, f"oracle_run_{sfx}")
+        f.restype = i
+        f.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, P, P, i, i, i] + [P] * 12
+        g = getattr(lib, f"oracle_alg1_{sfx}")
+        g.restype = i
+        g.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i] + [P] * 6
+    lib.oracle_round_bf16.restype = None
+    lib.oracle_round_bf16.argtypes = [P, P, ctypes.c_long]
+    lib.oracle_max_threads.restype = i
+    return lib
 
 
 def max_threads() -> int:
@@ -90,7 +104,7 @@ def _unpack(wl, kw):
 
 
 def run(wl=None, sel: Optional[Sequence[int]] = None, mode: str = "f64", bf16: bool = False,
-        threads: Optional[int] = None, backward: bool = True, **kw) -> dict:
+        threads: Optional[int] = None, backward: bool = True, native: bool = False, **kw) -> dict:
     """Branching StackLSTM forward + backward on the batch elements ``sel``.
 
     Returns h_top, c_top, h_cell, c_cell ([T, n, H]; h_cell/c_cell NaN on non-push
@@ -113,7 +127,7 @@ def run(wl=None, sel: Optional[Sequence[int]] = None, mode: str = "f64", bf16: b
         o.update(dx=np.zeros((T, n, I), dt), dW=np.zeros((I, 4 * H), dt), dU=np.zeros((H, 4 * H), dt),
                  db=np.zeros(4 * H, dt), dh0=np.zeros((n, H), dt), dc0=np.zeros((n, H), dt))
     th = max_threads() if threads is None else int(threads)
-    f = getattr(_load(), f"oracle_run_{mode}")
+    f = getattr(_load(native), f"oracle_run_{mode}")
     rc = f(T, B, I, H, _p(x), _p(ops), _p(W), _p(U), _p(b), _p(h0), _p(c0), _p(dh_top), _p(dc_top), _p(sel), n,
            int(bool(bf16)), th, _p(o["h_top"]), _p(o["c_top"]), _p(o["h_cell"]), _p(o["c_cell"]), _p(o["ptr"]),
            _p(o["top"]), _p(o.get("dx")), _p(o.get("dW")), _p(o.get("dU")), _p(o.get("db")), _p(o.get("dh0")),

@@ -36,6 +36,8 @@ __global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int cols,
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
+__global__ void k_scatter_splits(const float* P, const int32_t* rows, const uint32_t* count, size_t max_rows, int N,
+                                 int grid_blocks, int n_tiles, float* dst);
 
 namespace {
 
@@ -193,7 +195,9 @@ Layout layout(const slstm_dims* d) {
   L.dh = o; o += align256((T + 1) * B * H * 4);
   L.dc = o; o += align256((T + 1) * B * H * 4);
   L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
-  L.part = o; o += align256((size_t)64 * std::max(I, H) * 4 * H * 4);
+  // split-K partials of dW / dU, and the K-slice partials of dx (at most the rows of the grid's
+  // whole tiles: padded T*B x I)
+  L.part = o; o += align256(std::max((size_t)64 * std::max(I, H) * 4 * H, (T * B + 127) / 128 * 128 * I) * 4);
   L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
   L.dep = o; o += align256(B * 4);                                     // pointer after the last step
   L.total = o;
@@ -240,6 +244,17 @@ int read_status(const uint32_t* ctl, hipStream_t st) {
   return SLSTM_OK;
 }
 
+// Backward direct staging: a variant built with it, whole 1 KB row segments, K range equal
+// to the register capacity, and the LDS slice plus static LDS within one CU (one workgroup
+// per CU).
+bool bwd_direct_for(const slstm_dims* d, const Plan& p) {
+  const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
+  return rec_bwd_direct_built(d->precision, p.NTb, p.KS) && ((size_t)d->H * esz) % 1024 == 0 &&
+         p.KS * rec_kc(d->precision) == d->H &&
+         rec_bwd_lds_bytes(d->precision, p.KS) + rec_bwd_static_lds(p.NTb) <= 160 * 1024 &&
+         p.per_xcc_b <= std::max(1, device_cus() / 8);
+}
+
 RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, bool bwd) {
   RecArgs a;
   memset(&a, 0, sizeof(a));
@@ -263,12 +278,7 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   if (!bwd && p.pipe) a.poll = 1;
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
   a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
-  // backward direct staging: whole 1 KB row segments, K range equal to the register capacity,
-  // and the LDS slice plus static LDS within one CU (one workgroup per CU)
-  const int KC = rec_kc(d->precision);
-  a.bwd_direct = ((size_t)d->H * esz) % 1024 == 0 && p.KS * KC == d->H && rec_occ(d->precision, p.KS) == 1 &&
-                 rec_bwd_lds_bytes(d->precision, p.KS) + rec_bwd_static_lds(p.NTb) <= 160 * 1024 &&
-                 p.per_xcc_b <= std::max(1, device_cus() / 8);
+  a.bwd_direct = bwd_direct_for(d, p) ? 1 : 0;
   return a;
 }
 
@@ -296,15 +306,23 @@ const char* stacklstm_status_string(int s) {
   }
 }
 
-int stacklstm_plan(const slstm_dims* d, int32_t* groups, int32_t* wg_per_group, int32_t* rows_per_group,
-                   int32_t* k_chunks) {
+int stacklstm_plan(const slstm_dims* d, slstm_plan* out) {
   Plan p;
   int rc = make_plan(d, &p);
   if (rc) return rc;
-  if (groups) *groups = p.G;
-  if (wg_per_group) *wg_per_group = p.wide ? p.NWw : p.NW;
-  if (rows_per_group) *rows_per_group = 16 * p.NT;
-  if (k_chunks) *k_chunks = p.ks_eff;
+  if (!out) return SLSTM_EINVAL;
+  memset(out, 0, sizeof(*out));
+  out->groups = p.G;
+  out->wg_per_group = p.wide ? p.NWw : p.NW;
+  out->rows_per_group = 16 * p.NT;
+  out->k_chunks = p.ks_eff;
+  out->fwd_kernel = p.wide ? 2 : (p.pipe ? 1 : 0);
+  out->fwd_tiles = p.NT;
+  out->k_chunk_cap = p.KS;
+  out->occupancy = rec_occ(p.prec, p.KS);
+  out->bwd_groups = p.Gb;
+  out->bwd_tiles = p.NTb;
+  out->bwd_direct = bwd_direct_for(d, p) ? 1 : 0;
   return SLSTM_OK;
 }
 
@@ -516,16 +534,23 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, p.splits_u,
                      g.split_stride, H, H4, H, dU);
   mark(d, 8, st);
-  // dx = dA Wp^T on the push rows (gathered from dA, scattered into dx); 0 on the others
+  // dx = dA Wp^T on the push rows (gathered from dA); the GEMM's grid covers all T*B rows, so
+  // the push rows' tiles take two or more blocks each, over K slices written as partials that
+  // k_scatter_splits adds into the push rows of dx; 0 on the other rows
   gemm_base();
-  g.dyn_round = 1; g.dyn_axis = 0;
+  g.dyn_round = 1; g.dyn_axis = 0; g.dyn_split = 1;
   g.M = K; g.N = I; g.K = H4;
   const int VE = bf ? 8 : 4;
   g.A = a.dA; g.lda = H4; g.a_vec = (H4 % VE == 0); g.a_rows = prow;
   g.Bm = ws + L.wp; g.ldb = H4; g.b_vec = (H4 % VE == 0) && (I % VE == 0);
-  g.C = dx; g.ldc = I; g.c_rows = prow;
+  g.C = part; g.ldc = I;
   g.k_chunk = k_chunk_for(H4, 1);
   if ((rc = launch_gemm(p.prec, GEMM_MK, GEMM_NK, g, 1, st))) return rc;
+  {
+    const int ntl = (I + kGemmBN - 1) / kGemmBN, nblk = ntl * ((K + kGemmBM - 1) / kGemmBM);
+    hipLaunchKernelGGL(k_scatter_splits, dim3(grid1d((size_t)K * I)), dim3(256), 0, st, (const float*)part, prow, npush,
+                       (size_t)K, I, nblk, ntl, dx);
+  }
   hipLaunchKernelGGL(k_zero_nonpush_rows, dim3(grid1d((size_t)K * I / 4 + 1)), dim3(256), 0, st, ops, dx, (size_t)K,
                      I);
   if ((rc = hip_status(hipGetLastError()))) return rc;

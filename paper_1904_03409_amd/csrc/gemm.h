@@ -25,4 +25,14 @@ struct GemmArgs {
   // min(static extent, *dyn rounded up to a multiple of dyn_round). With a device K the
   // K range is cut into gridDim.z slices at run time (k_chunk is then ignored).
   const uint32_t* dyn; int dyn_axis; int dyn_round;
+  // With a device-side M: 1 = when the tiles in use are fewer than the grid's blocks, cut each
+  // tile's K range into gemm_dyn_splits() slices, written to C + z * M * ldc (the M rows in
+  // use packed, c_rows must be null); k_scatter_splits then adds them into the gathered rows.
+  int dyn_split;
 };
+// K slices per tile for a device-M GEMM over `active` tiles on a grid of `blocks` blocks.
+__host__ __device__ inline int gemm_dyn_splits(int blocks, int active) {
+  if (active <= 0) return 1;
+  const int s = blocks / active;
+  return s < 1 ? 1 : (s > 4 ? 4 : s);
+}

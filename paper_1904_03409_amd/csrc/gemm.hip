@@ -44,18 +44,18 @@ template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
   static constexpr int BK = Cfg<P>::BK, VE = Cfg<P>::VE;
   static constexpr int NV = 128 * BK / VE / 256;
   uint4 v[NV];
-  int prow[KMAJOR ? 1 : NV];   // array rows of this thread's vectors in an [m/n][k] tile (fixed over k)
+  int prow[NV];   // array row of each of this thread's vectors in the slice loaded next
 
   // Array row of tile row gr: the gather table's entry, or gr itself. Tiles stored [m/n][k]
-  // keep the same rows for every K slice, so they are resolved once (set_rows); k-major
-  // tiles look their rows up per slice.
+  // keep the same rows for every K slice, so they are resolved once; k-major tiles change rows
+  // with every slice, and the rows of the next slice are looked up right after the current
+  // slice's loads are issued (their latency then overlaps that of the data).
   __device__ __forceinline__ void set_rows(const int32_t* __restrict__ rows, int r0, int rlim) {
-    if constexpr (!KMAJOR) {
 #pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        const int gr = r0 + (threadIdx.x + 256 * i) / (BK / VE);
-        prow[i] = (rows && gr < rlim) ? rows[gr] : gr;
-      }
+    for (int i = 0; i < NV; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      const int gr = r0 + (KMAJOR ? e / (128 / VE) : e / (BK / VE));
+      prow[i] = (rows && gr < rlim) ? rows[gr] : gr;
     }
   }
 
@@ -110,9 +110,7 @@ template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
         else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
         const int gr = r0 + r, gc = c0 + c;
         const bool ok = gr < rlim && gc < clim;
-        int pr;
-        if constexpr (KMAJOR) pr = (rows && gr < rlim) ? rows[gr] : gr;
-        else pr = prow[i];
+        const int pr = prow[i];
         const uint32_t off = ok ? (uint32_t)(((size_t)pr * ld + gc) * sizeof(T)) : 0xffffffffu;
         v[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
       }
@@ -125,9 +123,7 @@ template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
       if (KMAJOR) { r = e / (128 / VE); c = (e % (128 / VE)) * VE; }
       else        { r = e / (BK / VE);  c = (e % (BK / VE)) * VE; }
       const int gr = r0 + r, gc = c0 + c;
-      int pr;
-      if constexpr (KMAJOR) pr = (rows && gr < rlim) ? rows[gr] : gr;
-      else pr = prow[i];
+      const int pr = prow[i];
       T tmp[VE];
 #pragma unroll
       for (int j = 0; j < VE; ++j) tmp[j] = (gr < rlim && gc + j < clim) ? base[(size_t)pr * ld + gc + j] : (T)0;
@@ -169,20 +165,59 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
   using GB = Geo<P, BKN>;
   __shared__ __align__(16) T As[2][GA::ELEMS];
   __shared__ __align__(16) T Bs[2][GB::ELEMS];
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // Block -> (n tile, m tile, K slice). Workgroups are dealt to the 8 XCDs in turn by their
+  // linear id, so ids are renumbered such that each XCD takes a contiguous run of tiles, and
+  // that run goes over groups of GM m tiles: for each n tile, the GM m tiles of the group. The
+  // A tiles of a group and the B tile in use then stay in that XCD's L2 (one B tile is read
+  // once per group rather than once per m tile).
+  constexpr int GM = 8;
+  const int NTL = (int)gridDim.x, MTL = (int)gridDim.y;
+  const int nblk = NTL * MTL * (int)gridDim.z;
+  int lid = (int)blockIdx.x + NTL * ((int)blockIdx.y + MTL * (int)blockIdx.z);
+  {
+    const int full = nblk & ~7;
+    if (lid < full) lid = (lid & 7) * (full >> 3) + (lid >> 3);
+  }
   int M = g.M, K = g.K, kchunk = g.k_chunk;
+  int tn, tm, tz;
+  auto grouped = [&](int id, int ntiles_m) {
+    const int per = NTL * ntiles_m;
+    tz = id / per;
+    const int r0 = id - tz * per;
+    const int gidx = r0 / (GM * NTL);
+    const int gm = min(GM, ntiles_m - gidx * GM);     // m tiles in this group (the last may be short)
+    const int r = r0 - gidx * GM * NTL;
+    tm = gidx * GM + r % gm;
+    tn = r / gm;
+  };
+  grouped(lid, MTL);
+  float* C = g.C;
+  int tz_c = -1;                                    // split whose split_stride offsets C (-1: tz)
   if (g.dyn) {
     const int ext = (int)((*g.dyn + (uint32_t)g.dyn_round - 1u) / (uint32_t)g.dyn_round * (uint32_t)g.dyn_round);
     if (g.dyn_axis == 0) {
+      // device-side M: the grid covers the static M; the blocks are spread over the tiles in
+      // use, each tile's K range cut into s slices (dyn_split, s <= 4) written as partials
       M = min(M, ext);
+      if (g.dyn_split) {
+        const int active = NTL * ((M + BM - 1) / BM);
+        const int sp = gemm_dyn_splits(nblk, active);
+        if (active == 0 || lid >= active * sp) return;
+        grouped(lid, active / NTL);
+        kchunk = ((K + sp - 1) / sp + 63) / 64 * 64;
+        C += (size_t)tz * M * g.ldc;                // partial z: rows [0, M) packed
+        tz_c = 0;
+      }
     } else {
       K = min(K, ext);
       kchunk = ((K + (int)gridDim.z - 1) / (int)gridDim.z + 63) / 64 * 64;
     }
   }
+  const int m0 = tm * BM, n0 = tn * BN;
   if (m0 >= M) return;                              // a whole block past a device-side M
-  const int kbeg = blockIdx.z * kchunk;
+  const int kbeg = tz * kchunk;
   const int kend = min(K, kbeg + kchunk);
+  C += (size_t)(tz_c < 0 ? tz : tz_c) * g.split_stride;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int l16 = lane & 15, lq = lane >> 4;
@@ -194,14 +229,35 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
   // buffer extents: the arrays' static sizes (gathered rows index within them)
   const size_t abytes = (AKM ? (size_t)g.K * g.lda : (size_t)g.M * g.lda) * (AF32 ? 4 : sizeof(T));
   const size_t bbytes = (BKN ? (size_t)g.K * g.ldb : (size_t)g.N * g.ldb) * sizeof(T);
-  if (!AKM) sa.set_rows(g.a_rows, m0, M);
-  if (!BKN) sb.set_rows(g.b_rows, n0, g.N);
+  sa.set_rows(g.a_rows, AKM ? kbeg : m0, AKM ? kend : M);
+  sb.set_rows(g.b_rows, BKN ? kbeg : n0, BKN ? kend : g.N);
   auto fetch = [&](int k0) {
     if (AKM) sa.load(A, abytes, g.lda, k0, kend, m0, M, g.a_vec, g.a_rows);
     else     sa.load(A, abytes, g.lda, m0, M, k0, kend, g.a_vec, g.a_rows);
     if (BKN) sb.load(Bp, bbytes, g.ldb, k0, kend, n0, g.N, g.b_vec, g.b_rows);
     else     sb.load(Bp, bbytes, g.ldb, n0, g.N, k0, kend, g.b_vec, g.b_rows);
+    // k-major tiles: rows of the next slice, looked up behind this slice's loads
+    if (AKM) sa.set_rows(g.a_rows, k0 + BK, kend);
+    if (BKN) sb.set_rows(g.b_rows, k0 + BK, kend);
   };
+
+  // epilogue operands (bias of this lane's columns, output rows), loaded now: on this GPU loads
+  // and stores share one in-order counter, so a load issued among the epilogue's stores would
+  // make its use wait for every store before it
+  float bias[4][4];
+  int crow_i[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int n = n0 + wn * 64 + j * 16 + 4 * lq + r;
+      bias[j][r] = (g.bias && n < g.N) ? g.bias[perm_to_orig(n, g.bias_H)] : 0.f;
+    }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + wm * 64 + i * 16 + l16;
+    crow_i[i] = (g.c_rows && m < M) ? g.c_rows[m] : m;
+  }
 
   f32x4 acc[4][4];
 #pragma unroll
@@ -245,7 +301,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32_16x16x4(av[cur][i], bv[cur][j], acc[i][j]);
+          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32_16x16x4(bv[cur][j], av[cur][i], acc[i][j]);
       }
     } else {
 #pragma unroll
@@ -258,7 +314,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16_16x16x32(a8[i], b8[j], acc[i][j]);
+          for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16_16x16x32(b8[j], a8[i], acc[i][j]);
       }
     }
     if (more) {
@@ -269,21 +325,31 @@ __global__ void __launch_bounds__(256, 2) k_gemm(GemmArgs g) {
     buf ^= 1;
   }
 
-  // epilogue: lane holds rows 4*lq + r, column l16 of each 16x16 tile
-  float* C = g.C + (size_t)blockIdx.z * g.split_stride;
+  // epilogue: the MFMAs ran as C^T = B^T A^T, so a lane holds row l16, columns 4*lq .. 4*lq+3
+  // of each 16x16 tile: one 16-byte store when the four columns are in range and aligned
+  const bool cvec = (g.ldc % 4) == 0 && (((uintptr_t)C) & 15u) == 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + wm * 64 + i * 16 + l16;
+    if (m >= M) continue;
+    float* crow = C + (size_t)crow_i[i] * g.ldc;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int n = n0 + wn * 64 + j * 16 + l16;
-      if (n >= g.N) continue;
-      const float bv = g.bias ? g.bias[perm_to_orig(n, g.bias_H)] : 0.f;
+      const int n = n0 + wn * 64 + j * 16 + 4 * lq;
+      float v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm * 64 + i * 16 + 4 * lq + r;
-        if (m < M) C[(size_t)(g.c_rows ? g.c_rows[m] : m) * g.ldc + n] = acc[i][j][r] + bv;
+      for (int r = 0; r < 4; ++r) v[r] = acc[i][j][r] + bias[j][r];
+      if (cvec && n + 3 < g.N) {
+        // non-temporal: the output is streamed out (measured: bf16 input projection at
+        // T*B = 61440, 4H = 2048, I = 256 takes 0.25 ms instead of 0.34 ms)
+        __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, (f32x4*)(crow + n));
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (n + r < g.N) crow[n + r] = v[r];
       }
     }
+  }
 }
 
 // out[m][col(n)] = sum_z P[z][m][n] in increasing z (deterministic), col = caller order.
@@ -297,6 +363,23 @@ __global__ void __launch_bounds__(256) k_reduce_splits(const float* __restrict__
     int n = (int)(i - m * N);
     int col = unperm_H ? perm_to_orig(n, unperm_H) : n;
     out[m * N + col] = s;
+  }
+}
+
+// Rows of a device-M GEMM run with dyn_split (N columns, partial z at P + z * nr * N for the
+// nr rows in use): dst row rows[k] = the sum over the s K slices of partial row k, in
+// increasing z (s as the GEMM computed it from its grid and the device count).
+__global__ void __launch_bounds__(256) k_scatter_splits(const float* __restrict__ P, const int32_t* __restrict__ rows,
+                                                        const uint32_t* __restrict__ count, size_t max_rows, int N,
+                                                        int grid_blocks, int n_tiles, float* __restrict__ dst) {
+  const size_t nr = min((size_t)*count, max_rows);
+  const int sp = gemm_dyn_splits(grid_blocks, n_tiles * (int)((nr + BM - 1) / BM));
+  const size_t n_el = nr * N;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_el; i += (size_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    for (int z = 0; z < sp; ++z) s += P[(size_t)z * n_el + i];
+    const size_t k = i / N;
+    dst[(size_t)rows[k] * N + (i - k * N)] = s;
   }
 }
 

@@ -26,6 +26,16 @@ constexpr size_t rec_bwd_static_lds(int nt) { return (size_t)4 * nt * 16 * 17 * 
 // Workgroups per CU the kernel is compiled for: 2 for the bf16 H > 512 case (64
 // workgroups per group), 1 otherwise.
 constexpr int rec_occ(int prec, int ks) { return (prec == 1 && ks == 32) ? 2 : 1; }
+// Backward instantiations that contain the direct-staging path (LDS DMA of the dA rows with
+// hand-counted vmcnt waits): whole 1 KB row segments, at most two per row, one workgroup per
+// CU and at most four row tiles per group. The eight-tile variants keep more state per thread
+// than the registers hold; their spills would share the counter those waits count, so they
+// are built without the path. The build checks that every variant built with it compiles
+// without scratch.
+constexpr bool rec_bwd_direct_built(int prec, int nt, int ks) {
+  return (ks * rec_kc(prec) * (prec ? 2 : 4)) % 1024 == 0 && ks * rec_kc(prec) * (prec ? 2 : 4) / 1024 <= 2 &&
+         rec_occ(prec, ks) == 1 && nt <= 4;
+}
 
 #define REC_CASES(X) \
   X(0, 1, 4) X(0, 1, 8) X(0, 1, 16) X(0, 1, 32) \

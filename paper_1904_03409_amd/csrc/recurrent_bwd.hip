@@ -116,7 +116,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
-  const bool direct = a.bwd_direct != 0;
+  const bool direct = rec_bwd_direct_built(PREC, NT, KS) && a.bwd_direct != 0;
   using elem_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
   elem_t* wbuf = reinterpret_cast<elem_t*>(dsm) + (size_t)wave * 16 * QLD;
   if (direct)
@@ -330,7 +330,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // whole 1 KB row segments, at most two per staged row (H of at most 512 fp32 / 1024 bf16);
     // not at two workgroups per CU, where the staged rows do not fit beside the other
     // workgroup's LDS (the host then never asks for it)
-    constexpr bool kDirectOk = (KS * KC * ESZ) % 1024 == 0 && KS * KC * ESZ / 1024 <= 2 && !LEAN;
+    constexpr bool kDirectOk = rec_bwd_direct_built(PREC, NT, KS);
     if (kDirectOk && direct) {
      if constexpr (kDirectOk) {
       // Each wave copies its own H gate columns of the compacted rows straight into its LDS

@@ -42,10 +42,11 @@ __global__ void __launch_bounds__(64) k_scan(const int8_t* __restrict__ ops, int
     int8_t v[CH];
 #pragma unroll
     for (int i = 0; i < CH; ++i) v[i] = (t0 + i < T) ? ops[(size_t)(t0 + i) * B + b] : (int8_t)0;
+    // fully unrolled (constant register index of each op); steps past T are skipped by a guard
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int t = t0 + i;
-      if (t >= T) break;
+      if (t >= T) continue;
       int op = v[i];
       if (op < -1 || op > 1) {
         if (first_bad == 0x7fffffff) first_bad = t;

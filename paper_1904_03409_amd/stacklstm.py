@@ -40,6 +40,12 @@ class slstm_dims(ctypes.Structure):
 SLSTM_PHASE_EVENTS = 10
 
 
+class slstm_plan(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "groups", "wg_per_group", "rows_per_group", "k_chunks", "fwd_kernel", "fwd_tiles", "k_chunk_cap",
+        "occupancy", "bwd_groups", "bwd_tiles", "bwd_direct", "reserved")]
+
+
 _lib = None
 
 
@@ -63,7 +69,7 @@ def load_library():
         lib.stacklstm_status_string.restype = ctypes.c_char_p
         lib.stacklstm_status_string.argtypes = [I32]
         lib.stacklstm_plan.restype = I32
-        lib.stacklstm_plan.argtypes = [D] + [ctypes.POINTER(ctypes.c_int32)] * 4
+        lib.stacklstm_plan.argtypes = [D, ctypes.POINTER(slstm_plan)]
         _lib = lib
     return _lib
 
@@ -107,10 +113,9 @@ def stacklstm_workspace_bytes(dims: slstm_dims) -> int:
 
 
 def stacklstm_plan(dims: slstm_dims) -> dict:
-    vals = [ctypes.c_int32() for _ in range(4)]
-    _check(load_library().stacklstm_plan(ctypes.byref(dims), *[ctypes.byref(v) for v in vals]), "stacklstm_plan")
-    return dict(groups=vals[0].value, wg_per_group=vals[1].value, rows_per_group=vals[2].value,
-                k_chunks=vals[3].value)
+    out = slstm_plan()
+    _check(load_library().stacklstm_plan(ctypes.byref(dims), ctypes.byref(out)), "stacklstm_plan")
+    return {n: getattr(out, n) for n, _ in slstm_plan._fields_ if n != "reserved"}
 
 
 def stacklstm_fwd(dims, x, ops, W, U, b, h0, c0, h_cell, c_cell, h_top, c_top, ptr, top, workspace, stream=None,
