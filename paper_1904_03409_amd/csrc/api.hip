@@ -76,7 +76,7 @@ struct Plan {
 };
 
 struct Layout {
-  size_t ctl, stack, wp, r1, stash, hx, xbt, hp, dat, dh, dc, dbp, part, prow, dep, total;
+  size_t ctl, stack, dep, wp, r1, stash, hx, fwd_end, xbt, hp, dat, dh, dc, dbp, part, prow, total;
 };
 
 // Push-row count padded to the K tile: leading dimension of the transposed bf16 operands
@@ -184,10 +184,12 @@ Layout layout(const slstm_dims* d) {
   size_t o = 0;
   L.ctl = o; o += align256(CTL_WORDS * 4);
   L.stack = o; o += align256(B * (T + 1) * 4);                        // op scan: stacks that do not fit in LDS
+  L.dep = o; o += align256(B * 4);                                     // pointer after the last step
   L.wp = o; o += align256(I * 4 * H * 4);                             // Wp fp32, or Wp and Wp^T in bf16
   L.r1 = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));   // XW (forward), dA (backward)
   L.stash = o; o += align256(std::max<size_t>(T * B * 4 * H * 4, 16));
   L.hx = o; o += bf ? align256((T + 1) * B * H * 2) : 0;
+  L.fwd_end = o;                                                       // the forward uses [0, fwd_end)
   // post-loop operands over the push rows (at most T*B of them; KP with the K-tile padding)
   L.xbt = o; o += bf ? align256(KP * I * 2) : 0;                      // x^T in bf16 (bf16 mode)
   L.hp = o; o += align256(std::max<size_t>(bf ? KP * H * 2 : T * B * H * 4, 16));   // Hprev (bf16 mode: Hprev^T)
@@ -199,7 +201,6 @@ Layout layout(const slstm_dims* d) {
   // whole tiles: padded T*B x I)
   L.part = o; o += align256(std::max((size_t)64 * std::max(I, H) * 4 * H, (T * B + 127) / 128 * 128 * I) * 4);
   L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
-  L.dep = o; o += align256(B * 4);                                     // pointer after the last step
   L.total = o;
   return L;
 }
