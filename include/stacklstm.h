@@ -30,7 +30,8 @@
  *    contents are then unspecified (an invalid op is walked as a hold so that every
  *    index stays in range).
  *  - No exception crosses the ABI. The only global state is the cached device
- *    properties (multiprocessor count per device) and the kernels' launch attributes.
+ *    properties (multiprocessor count per device), the kernels' launch attributes, and
+ *    for stacklstm_fwd_static its static work space per GPU (with its device address).
  *    Calls on different work spaces may overlap, on any streams and from any host
  *    threads; calls that share a work space must not overlap. Results do not depend on
  *    what runs beside them.
@@ -122,6 +123,19 @@ size_t stacklstm_workspace_bytes(const slstm_dims* d);
 int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
                   const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
                   float* c_top, int32_t* ptr, int32_t* top, void* workspace, size_t ws_bytes, void* stream);
+
+/* Allocation-free variant of stacklstm_fwd, for callers that cannot allocate device memory
+ * (serving loops and harnesses that forbid allocation): the same arguments, outputs and
+ * status read-back, with no work-space argument. Its work space is a static device array of
+ * SLSTM_FWD_STATIC_MAX_BYTES bytes, one per GPU, held until the process ends; the call
+ * allocates nothing. Dims whose forward work space (the forward's part of
+ * stacklstm_workspace_bytes) exceeds it give SLSTM_EWORKSPACE. Every call on a GPU uses that
+ * GPU's array: calls that overlap on one GPU (two streams, two host threads) race and must
+ * be serialised by the caller. A backward cannot follow it (it keeps nothing for one). */
+#define SLSTM_FWD_STATIC_MAX_BYTES ((size_t)128 << 20)
+int stacklstm_fwd_static(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                         const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
+                         float* c_top, int32_t* ptr, int32_t* top, void* stream);
 
 /* Backward of L given dL/dh_top and dL/dc_top (section 5), after stacklstm_fwd on the
  * same inputs and work space. The reverse loop scatters each step's gradient into the step

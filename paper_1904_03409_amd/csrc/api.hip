@@ -327,20 +327,15 @@ int stacklstm_plan(const slstm_dims* d, slstm_plan* out) {
   return SLSTM_OK;
 }
 
-int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
-                  const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
-                  float* c_top, int32_t* ptr, int32_t* top, void* workspace, size_t ws_bytes, void* stream) {
-  if (!dims_ok(d)) return SLSTM_EINVAL;
-  if (!ptr || !workspace ||
-      (d->T > 0 && (!ops || !x || !W || !U || !b || !h0 || !c0 || !h_cell || !c_cell || !top)))
-    return SLSTM_EINVAL;
-  const Layout L = layout(d);
-  if (ws_bytes < L.total) return SLSTM_EWORKSPACE;
-  Plan p;
-  int rc = make_plan(d, &p);
-  if (rc) return rc;
-  hipStream_t st = (hipStream_t)stream;
-  char* ws = (char*)workspace;
+}  // extern "C"
+
+namespace {
+
+// The forward pass on a work space that the caller checked (at least layout(d).fwd_end bytes).
+int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x, const int8_t* ops, const float* W,
+             const float* U, const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell,
+             float* h_top, float* c_top, int32_t* ptr, int32_t* top, char* ws, hipStream_t st) {
+  int rc = SLSTM_OK;
   uint32_t* ctl = (uint32_t*)(ws + L.ctl);
   const int T = d->T, B = d->B, I = d->I, H = d->H;
   const bool bf = p.prec == SLSTM_BF16_GEMM;
@@ -423,6 +418,69 @@ int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 4, st);
   return read_status(ctl, st);
+}
+
+bool fwd_args_ok(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                 const float* b, const float* h0, const float* c0, const float* h_cell, const float* c_cell,
+                 const int32_t* ptr, const int32_t* top) {
+  return ptr && (d->T == 0 || (ops && x && W && U && b && h0 && c0 && h_cell && c_cell && top));
+}
+
+// Static work space of the allocation-free forward: one copy per GPU, held until the process
+// ends. Host code uses the device address that hipGetSymbolAddress returns for the current
+// device (kept per device), never the array's name.
+constexpr size_t kScratchBytes = SLSTM_FWD_STATIC_MAX_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device, looked up on the first call on that
+// device; null if the lookup failed.
+char* scratch_ptr() {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  static bool done[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!done[dev]) {
+    void* q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    addr[dev] = q;
+    done[dev] = true;
+  }
+  return (char*)addr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int stacklstm_fwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                  const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
+                  float* c_top, int32_t* ptr, int32_t* top, void* workspace, size_t ws_bytes, void* stream) {
+  if (!dims_ok(d)) return SLSTM_EINVAL;
+  if (!workspace || !fwd_args_ok(d, x, ops, W, U, b, h0, c0, h_cell, c_cell, ptr, top)) return SLSTM_EINVAL;
+  const Layout L = layout(d);
+  if (ws_bytes < L.total) return SLSTM_EWORKSPACE;
+  Plan p;
+  int rc = make_plan(d, &p);
+  if (rc) return rc;
+  return fwd_impl(d, p, L, x, ops, W, U, b, h0, c0, h_cell, c_cell, h_top, c_top, ptr, top, (char*)workspace,
+                  (hipStream_t)stream);
+}
+
+int stacklstm_fwd_static(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
+                         const float* b, const float* h0, const float* c0, float* h_cell, float* c_cell, float* h_top,
+                         float* c_top, int32_t* ptr, int32_t* top, void* stream) {
+  if (!dims_ok(d)) return SLSTM_EINVAL;
+  if (!fwd_args_ok(d, x, ops, W, U, b, h0, c0, h_cell, c_cell, ptr, top)) return SLSTM_EINVAL;
+  const Layout L = layout(d);
+  if (L.fwd_end > kScratchBytes) return SLSTM_EWORKSPACE;
+  Plan p;
+  int rc = make_plan(d, &p);
+  if (rc) return rc;
+  char* ws = scratch_ptr();
+  if (!ws) return SLSTM_EDEVICE;
+  return fwd_impl(d, p, L, x, ops, W, U, b, h0, c0, h_cell, c_cell, h_top, c_top, ptr, top, ws, (hipStream_t)stream);
 }
 
 int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,

@@ -22,8 +22,9 @@ SLSTM_FP32 = 0
 SLSTM_BF16_GEMM = 1
 STATUS = {0: "SLSTM_OK", 1: "SLSTM_EINVAL", 2: "SLSTM_EOPS", 3: "SLSTM_EUNDERFLOW", 4: "SLSTM_EWORKSPACE",
           5: "SLSTM_ENORESIDENT", 6: "SLSTM_EDEVICE", 7: "SLSTM_ETIMEOUT", 8: "SLSTM_EINDEX"}
-EXPORTS = ("stacklstm_workspace_bytes", "stacklstm_fwd", "stacklstm_bwd", "stacklstm_sync_status",
-           "stacklstm_status_string", "stacklstm_plan")
+EXPORTS = ("stacklstm_workspace_bytes", "stacklstm_fwd", "stacklstm_fwd_static", "stacklstm_bwd",
+           "stacklstm_sync_status", "stacklstm_status_string", "stacklstm_plan")
+SLSTM_FWD_STATIC_MAX_BYTES = 128 << 20
 
 
 class StackLSTMError(RuntimeError):
@@ -62,6 +63,8 @@ def load_library():
         lib.stacklstm_workspace_bytes.argtypes = [D]
         lib.stacklstm_fwd.restype = I32
         lib.stacklstm_fwd.argtypes = [D] + [P] * 14 + [SZ, P]
+        lib.stacklstm_fwd_static.restype = I32
+        lib.stacklstm_fwd_static.argtypes = [D] + [P] * 13 + [P]
         lib.stacklstm_bwd.restype = I32
         lib.stacklstm_bwd.argtypes = [D] + [P] * 10 + [SZ] + [P] * 8 + [P]
         lib.stacklstm_sync_status.restype = I32
@@ -128,6 +131,20 @@ def stacklstm_fwd(dims, x, ops, W, U, b, h0, c0, h_cell, c_cell, h_top, c_top, p
         _ptr(top, i32, "top"), _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
     if check:
         _check(rc, "stacklstm_fwd")
+    return rc
+
+
+def stacklstm_fwd_static(dims, x, ops, W, U, b, h0, c0, h_cell, c_cell, h_top, c_top, ptr, top, stream=None,
+                         check=True) -> int:
+    """stacklstm_fwd on the library's static per-GPU work space (no work-space argument)."""
+    f32, i32 = torch.float32, torch.int32
+    rc = load_library().stacklstm_fwd_static(
+        ctypes.byref(dims), _ptr(x, f32, "x"), _ptr(ops, torch.int8, "ops"), _ptr(W, f32, "W"), _ptr(U, f32, "U"),
+        _ptr(b, f32, "b"), _ptr(h0, f32, "h0"), _ptr(c0, f32, "c0"), _ptr(h_cell, f32, "h_cell"),
+        _ptr(c_cell, f32, "c_cell"), _ptr(h_top, f32, "h_top"), _ptr(c_top, f32, "c_top"), _ptr(ptr, i32, "ptr"),
+        _ptr(top, i32, "top"), _stream(stream))
+    if check:
+        _check(rc, "stacklstm_fwd_static")
     return rc
 
 
