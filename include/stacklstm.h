@@ -175,7 +175,8 @@ typedef struct {
   int32_t bwd_groups;      /* backward: batch groups */
   int32_t bwd_tiles;       /* backward: 16-row tiles per group */
   int32_t bwd_direct;      /* backward: dA rows staged in LDS by DMA (1) or read into registers (0) */
-  int32_t reserved;
+  int32_t fused_x;         /* 1: the forward kernel contracts x_t W itself (no separate input
+                              projection GEMM; bf16, plain forward, one pass per step) */
 } slstm_plan;
 
 /* Fills `out` for `d`; returns a status like the entry points. */

@@ -70,6 +70,7 @@ bool al16(const void* q) { return ((uintptr_t)q & 15u) == 0; }
 struct Plan {
   int prec, KS, ks_eff, NW;
   int NT, G, per_xcc, pipe;   // pipe: the forward runs the pipelined kernel
+  int fuse, kx;               // fuse: the plain bf16 forward contracts x_t W itself (kx chunks of 32)
   int wide, NWw;              // wide: the forward runs the 32-unit kernel (NWw workgroups per group)
   int NTb, Gb, per_xcc_b;
   int splits_w, splits_u;
@@ -125,6 +126,8 @@ int make_plan(const slstm_dims* d, Plan* p) {
   // XCCs round-robin) are co-resident on one XCC at the kernel's occupancy
   // the pipelined forward needs whole 1 KB row segments (vector rows, every K chunk in use)
   const bool pipe_ok = d->H % (prec ? 8 : 4) == 0 && p->ks_eff == p->KS && p->KS >= 16;
+  p->kx = (d->I + 31) / 32;
+  p->fuse = 0;
   auto pick = [&](bool bwd, int* NT_out, int* G_out, int* per_out, int* pipe_out) -> int {
     for (int NT = 1; NT <= 8; NT *= 2) {
       int G = (d->B + 16 * NT - 1) / (16 * NT);
@@ -132,17 +135,25 @@ int make_plan(const slstm_dims* d, Plan* p) {
       int per_xcc = p->NW * ((G + 7) / 8);
       int occ = 0;
       const bool pipe = !bwd && pipe_ok && NT >= 2 && rec_pipe_built(prec, NT, p->KS);
+      // the plain bf16 forward fuses the input projection when one pass covers the group
+      const bool fuse = !bwd && !pipe && rec_fx_built(prec, p->KS) && rec_ntb(prec, NT, p->KS) == NT &&
+                        rec_fx_fits(16 * NT, p->kx);
       RecArgs dummy;
       memset(&dummy, 0, sizeof(dummy));
+      FxArgs fdummy;
+      memset(&fdummy, 0, sizeof(fdummy));
+      fdummy.fuse_x = fuse ? 1 : 0;
+      fdummy.kx = p->kx;
       hipError_t e = bwd    ? launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
                      : pipe ? launch_fwd_pipe(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
-                            : launch_fwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
+                            : launch_fwd(dummy, fdummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
       if (e != hipSuccess) return SLSTM_EDEVICE;
       if (per_xcc <= cu_per_xcc * occ) {
         *NT_out = NT;
         *G_out = G;
         *per_out = per_xcc;
         if (pipe_out) *pipe_out = pipe ? 1 : 0;
+        if (!bwd) p->fuse = fuse ? 1 : 0;
         return SLSTM_OK;
       }
     }
@@ -324,6 +335,7 @@ int stacklstm_plan(const slstm_dims* d, slstm_plan* out) {
   out->bwd_groups = p.Gb;
   out->bwd_tiles = p.NTb;
   out->bwd_direct = bwd_direct_for(d, p) ? 1 : 0;
+  out->fused_x = p.fuse;
   return SLSTM_OK;
 }
 
@@ -366,9 +378,10 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   void* wp = ws + L.wp;
   bf16_t* wpt = bf ? (bf16_t*)wp + (size_t)I * 4 * H : nullptr;
   hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W, bf ? nullptr : (float*)wp,
-                     bf ? (bf16_t*)wp : nullptr, wpt, I, H);
+                     bf ? (bf16_t*)wp : nullptr, p.fuse ? nullptr : wpt, I, H);
   float* xw = (float*)(ws + L.r1);
-  {
+  // (with the fused projection the recurrent kernel contracts x_t W itself: no XW)
+  if (!p.fuse) {
     GemmArgs g;
     memset(&g, 0, sizeof(g));
     g.M = T * B; g.N = 4 * H; g.K = I;
@@ -384,7 +397,14 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   // a3-a6: persistent recurrent kernel
   RecArgs a = rec_args(d, p, ws, L, false);
   if (bf) hipLaunchKernelGGL(k_h0_bf16, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, h0, (bf16_t*)a.hx, (size_t)B * H);
-  a.xw = xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell; a.top = top;
+  a.xw = p.fuse ? nullptr : xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell;
+  a.top = top;
+  FxArgs fa;
+  memset(&fa, 0, sizeof(fa));
+  if (p.fuse) {
+    fa.fuse_x = 1; fa.kx = p.kx; fa.x = x; fa.W = W; fa.bias = b;
+    fa.x_vec = (I % 4 == 0) && al16(x);
+  }
   // exchange buffers start as "not yet produced": all-one bits in the state rows the
   // workgroups read from each other
   if (a.poll || p.wide) {
@@ -398,7 +418,7 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   mark(d, 2, st);
   if ((rc = hip_status(p.wide   ? launch_fwd_wide(a, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
                        : p.pipe ? launch_fwd_pipe(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr)
-                                : launch_fwd(a, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr))))
+                                : launch_fwd(a, fa, p.prec, p.NT, p.KS, dim3(8 * p.per_xcc), st, nullptr))))
     return rc;
   mark(d, 3, st);
 

@@ -12,7 +12,7 @@ struct RecArgs {
   int coh_rows;
   int bwd_direct;        // backward stages dA rows with global_load_lds (host checks the LDS fits)
   int poll;              // 1: workgroups exchange rows by polling fill-marked data; 0: group barrier per step
-  const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward)
+  const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward; null when fused)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)
   const float* h0;       // [B][H]
@@ -37,4 +37,14 @@ struct RecArgs {
   float* dh0;            // [B][H]
   float* dc0;            // [B][H]
   long long* clk;        // optional per-step wall-clock stamps [grid][T][4] (profiling)
+};
+
+// Fused input projection of the plain bf16 forward (a second argument of that kernel only).
+struct FxArgs {
+  int fuse_x;            // 1: the kernel contracts x_t W itself (RecArgs::xw unused)
+  int kx;                // K chunks of 32 covering I
+  int x_vec;             // x rows read as float4 (I % 4 == 0, 16-byte aligned)
+  const float* x;        // [T][B][I]
+  const float* W;        // [I][4H] caller layout
+  const float* bias;     // [4H] caller layout
 };

@@ -26,7 +26,7 @@
 #include "rec_device.h"
 
 template <int PREC, int NT, int NTB, int KS, int OCC>
-__global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
+__global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
   constexpr int KC = PREC ? 32 : 16;               // K per chunk
   constexpr int KP = KS * KC;                      // K capacity of the U registers
   constexpr int ESZ = PREC ? 2 : 4;                // bytes per staged element
@@ -67,6 +67,73 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
   const bool direct = vec_ok && kmax == KP && (KP * ESZ) % 1024 == 0;
 
+  // ---- fused input projection (bf16, one pass per step): x_t W is contracted in the step
+  // itself. The workgroup's W slice (its 64 gate columns x I, bf16) sits in LDS after the
+  // h_prev tile, the x rows of a step in one of two LDS buffers after it; the x rows of step
+  // t+1 are loaded into registers at the start of step t and written to the other buffer at
+  // its end. The bias is added in the cell update.
+  constexpr bool FX_BUILT = rec_fx_built(PREC, KS);
+  const bool fx = FX_BUILT && f.fuse_x && NPASS == 1;
+  const int I = a.I, kx = f.kx, XLD = kx * 32 + 8, KXP = kx * 32;
+  bf16_t* wsl = reinterpret_cast<bf16_t*>(smem) + (size_t)ROWS_B * LDS_LD;   // [64][XLD]
+  bf16_t* xsb = wsl + (size_t)64 * XLD;                                      // [2][ROWS_B][XLD]
+  float4 bias4 = float4{0.f, 0.f, 0.f, 0.f};
+  constexpr int XJ = FX_BUILT ? 8 : 1;             // x vectors (4 floats) per thread and step, at most
+  float4 xr[XJ];
+  const int xn = ROWS_B * KXP / 4;                 // x vectors of one step's rows
+  auto load_x = [&](int tt) {
+#pragma unroll
+    for (int j = 0; j < XJ; ++j) {
+      const int e = (int)threadIdx.x + 256 * j;
+      xr[j] = float4{0.f, 0.f, 0.f, 0.f};
+      if (e >= xn) continue;
+      const int r = e / (KXP / 4), k = (e - r * (KXP / 4)) * 4, b = row0 + r;
+      if (b >= B || k >= I) continue;
+      const float* src = f.x + ((size_t)tt * B + b) * I + k;
+      if (f.x_vec) {
+        xr[j] = *(const float4*)src;
+      } else {
+        xr[j].x = src[0];
+        if (k + 1 < I) xr[j].y = src[1];
+        if (k + 2 < I) xr[j].z = src[2];
+        if (k + 3 < I) xr[j].w = src[3];
+      }
+    }
+  };
+  auto store_x = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < XJ; ++j) {
+      const int e = (int)threadIdx.x + 256 * j;
+      if (e >= xn) continue;
+      const int r = e / (KXP / 4), k = (e - r * (KXP / 4)) * 4;
+      const uint32_t lo = (uint32_t)f32_to_bf16_bits(xr[j].x) | ((uint32_t)f32_to_bf16_bits(xr[j].y) << 16);
+      const uint32_t hi = (uint32_t)f32_to_bf16_bits(xr[j].z) | ((uint32_t)f32_to_bf16_bits(xr[j].w) << 16);
+      *(uint2*)&xsb[((size_t)buf * ROWS_B + r) * XLD + k] = uint2{lo, hi};
+    }
+  };
+  // x_t W for every tile of the pass: A = W^T slice rows (unit, gate) of this wave, B = x rows
+  auto xpart = [&](f32x4* acc, int buf) {
+    for (int c = 0; c < kx; ++c) {
+      const bf16x8 wv = *(const bf16x8*)&wsl[(size_t)(wave * 16 + l16) * XLD + c * 32 + 8 * lq];
+#pragma unroll
+      for (int nt = 0; nt < NTB; ++nt) {
+        const bf16x8 xv = *(const bf16x8*)&xsb[((size_t)buf * ROWS_B + nt * 16 + l16) * XLD + c * 32 + 8 * lq];
+        acc[nt] = mfma_bf16_16x16x32(wv, xv, acc[nt]);
+      }
+    }
+  };
+  if (fx) {
+    // W slice: column m of the slice is gate m % 4 of unit 16w + m / 4 (the U slice's order)
+    for (int i = threadIdx.x; i < 64 * KXP; i += 256) {
+      const int m = i / KXP, k = i - m * KXP, unit = w * 16 + m / 4;
+      const float v = (unit < H && k < I) ? f.W[(size_t)k * H4 + (m & 3) * H + unit] : 0.f;
+      wsl[(size_t)m * XLD + k] = f32_to_bf16_bits(v);
+    }
+    if (u < H) bias4 = float4{f.bias[u], f.bias[H + u], f.bias[2 * H + u], f.bias[3 * H + u]};
+    load_x(0);
+    store_x(0);
+  }
+
   // rows of this lane in the MFMA output layout: tile ti covers rows ti*16 .. ti*16+15
   int lrow[NT];
   bool lok[NT];
@@ -95,7 +162,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
   float cp_cur[NT];
 #pragma unroll
   for (int ti = 0; ti < NT; ++ti) {
-    xw_cur[ti] = xw_at(0, ti);
+    xw_cur[ti] = fx ? bias4 : xw_at(0, ti);
     cp_cur[ti] = lok[ti] ? a.c0[(size_t)lrow[ti] * H + u] : 0.f;
   }
   if (!a.poll) {
@@ -125,14 +192,25 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
       // following it (vector loads complete in issue order)
 #pragma unroll
       for (int ti = 0; ti < NT; ++ti) src_nxt[ti] = top_at(t, ti);
+      if (fx) {
 #pragma unroll
-      for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
+        for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = bias4;
+        if (more) load_x(t + 1);
+      } else {
+#pragma unroll
+        for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
+      }
       asm volatile("" ::: "memory");
     }
 #pragma unroll
     for (int nb = 0; nb < NPASS; ++nb) {
+      f32x4 acc[NTB];
+#pragma unroll
+      for (int nt = 0; nt < NTB; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       // ---- gather this pass's h_prev rows into LDS; granules that still hold the fill are
-      // fetched again until their producers' stores have arrived
+      // fetched again until their producers' stores have arrived. With the fused input
+      // projection, its MFMAs run while the rows are in flight.
+      if (fx && !direct) xpart(acc, t & 1);
       if (direct) {
 #pragma unroll
         for (int i = 0; i < NSEG_W; ++i) {
@@ -149,6 +227,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
             else __builtin_amdgcn_global_load_lds(gp, (lds_ptr_t)lp, 16, 0, 0);
           }
         }
+        if (fx) xpart(acc, t & 1);
       } else {
         constexpr int VW = PREC ? 8 : 4;
         if (vec_ok) {
@@ -308,10 +387,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
         for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
       }
 
-      // ---- gates^T (16 cols x 16 rows per tile) = U^T h_prev^T; B fragments read one chunk ahead
-      f32x4 acc[NTB];
-#pragma unroll
-      for (int nt = 0; nt < NTB; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // ---- gates^T (16 cols x 16 rows per tile) += U^T h_prev^T; B fragments read one chunk ahead
       // all KS chunks run: U registers and staged LDS columns are zero beyond H
       if constexpr (PREC == 0) {
         float4 bcur[NTB], bnxt[NTB];
@@ -380,6 +456,8 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
     }
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) { xw_cur[ti] = xw_nxt[ti]; cp_cur[ti] = cp_nxt[ti]; }
+    // x rows of step t+1: the other buffer, last read in step t-1
+    if (fx && more) store_x((t + 1) & 1);
     if (!a.poll) {
       // barrier mode: every state of step t is complete past this point
       if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_abort[1]))
@@ -395,11 +473,16 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a) {
 
 // ---- instantiations and launcher: one kernel per (precision, row tiles per group, K chunks)
 template <int P, int NT, int KS>
-static hipError_t launch_fwd_t(const RecArgs& a, dim3 grid, hipStream_t st, int* occ_out) {
+static hipError_t launch_fwd_t(const RecArgs& a, const FxArgs& f, dim3 grid, hipStream_t st, int* occ_out) {
   constexpr int NTB = rec_ntb(P, NT, KS);
   constexpr int OCC = rec_occ(P, KS);
   auto kern = k_fwd<P, NT, NTB, KS, OCC>;
   size_t shm = rec_lds_bytes(P, NTB, KS);
+  if (f.fuse_x) {
+    // the fused projection: built variants, one pass per step, x rows within the staging registers
+    if (!rec_fx_built(P, KS) || NTB != NT || !rec_fx_fits(16 * NT, f.kx)) return hipErrorInvalidValue;
+    shm += rec_fx_lds_bytes(16 * NTB, f.kx);
+  }
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
   if (e != hipSuccess) return e;
   int occ = 0;
@@ -408,12 +491,15 @@ static hipError_t launch_fwd_t(const RecArgs& a, dim3 grid, hipStream_t st, int*
   if (occ_out) *occ_out = occ;
   if (!grid.x) return hipSuccess;  // occupancy query only
   RecArgs args = a;
-  void* kargs[] = {&args};
+  FxArgs fargs = f;
+  void* kargs[] = {&args, &fargs};
   return hipLaunchCooperativeKernel((const void*)kern, grid, dim3(256), kargs, (unsigned)shm, st);
 }
 
-hipError_t launch_fwd(const RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out) {
-#define CASE(P, NT_, KS_) if (prec == P && NT == NT_ && KS == KS_) return launch_fwd_t<P, NT_, KS_>(a, grid, st, occ_out);
+hipError_t launch_fwd(const RecArgs& a, const FxArgs& f, int prec, int NT, int KS, dim3 grid, hipStream_t st,
+                      int* occ_out) {
+#define CASE(P, NT_, KS_) \
+  if (prec == P && NT == NT_ && KS == KS_) return launch_fwd_t<P, NT_, KS_>(a, f, grid, st, occ_out);
   REC_CASES(CASE)
 #undef CASE
   return hipErrorInvalidValue;

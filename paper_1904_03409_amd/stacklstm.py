@@ -44,7 +44,7 @@ SLSTM_PHASE_EVENTS = 10
 class slstm_plan(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "groups", "wg_per_group", "rows_per_group", "k_chunks", "fwd_kernel", "fwd_tiles", "k_chunk_cap",
-        "occupancy", "bwd_groups", "bwd_tiles", "bwd_direct", "reserved")]
+        "occupancy", "bwd_groups", "bwd_tiles", "bwd_direct", "fused_x")]
 
 
 _lib = None
@@ -118,7 +118,7 @@ def stacklstm_workspace_bytes(dims: slstm_dims) -> int:
 def stacklstm_plan(dims: slstm_dims) -> dict:
     out = slstm_plan()
     _check(load_library().stacklstm_plan(ctypes.byref(dims), ctypes.byref(out)), "stacklstm_plan")
-    return {n: getattr(out, n) for n, _ in slstm_plan._fields_ if n != "reserved"}
+    return {n: getattr(out, n) for n, _ in slstm_plan._fields_}
 
 
 def stacklstm_fwd(dims, x, ops, W, U, b, h0, c0, h_cell, c_cell, h_top, c_top, ptr, top, workspace, stream=None,

@@ -72,16 +72,20 @@ def test_spin_limit_timeout_reported():
 
 
 def test_spin_limit_timeout_reported_polling():
-    """bf16 mode exchanges rows by polling fill-marked data: with a one-poll limit the first
-    wait that finds a row not yet written gives up (some wait of the deep workload always
-    does), the kernels leave their loops and the call reports SLSTM_ETIMEOUT; the same
-    buffers then run normally and match the oracle's trace."""
+    """The plain bf16 forward exchanges rows by polling fill-marked data: with a one-poll limit
+    the first wait that finds a row not yet written gives up (some wait of the deep-stack
+    streams always does when the input projection is not fused into the step: its MFMAs
+    would sit between the copy and the check), the kernels leave their loops and the call
+    reports SLSTM_ETIMEOUT; the same buffers then run normally."""
     need_gpu()
-    wl = wk.make("deep")
+    from paper_1904_03409_amd import stacklstm as s
+    deep = wk.make("deep")
+    wl = wk.custom(T=deep.T, B=deep.B, I=544, H=deep.H, seed=104, ops=deep.ops, wscale=0.08)
+    plan = s.stacklstm_plan(s.make_dims(wl.T, wl.B, wl.I, wl.H, 1, 0))
+    assert plan["fwd_kernel"] == 0 and plan["fused_x"] == 0, plan
     r, rc = _run(wl, precision=1, spin_limit=1)
     assert rc == 7
     torch.cuda.synchronize()
-    from paper_1904_03409_amd import stacklstm as s
     r2, rc2 = _run(wl, precision=1)
     assert rc2 == 0
     assert s.stacklstm_sync_status(r2.workspace) == 0

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 GRID_H = {0: [1, 40, 64, 100, 128, 200, 252, 256, 300, 508, 512],
           1: [1, 64, 100, 128, 200, 256, 300, 504, 512, 520, 1020, 1024]}
 GRID_B = [1, 17, 64, 100, 128, 129, 200, 256, 257, 300, 384, 400, 512, 513, 600, 700, 768, 769, 900, 1000, 1024]
-KEYS = ("fwd_kernel", "fwd_tiles", "k_chunk_cap", "occupancy", "bwd_tiles", "bwd_direct")
+KEYS = ("fwd_kernel", "fwd_tiles", "k_chunk_cap", "occupancy", "bwd_tiles", "bwd_direct", "fused_x")
 
 
 def reachable_variants():
@@ -84,7 +84,7 @@ def test_every_planner_variant(oracle_mod):
     need_gpu()
     variants = reachable_variants()
     print(f"[gpu] {len(variants)} variants: precision, fwd kernel, fwd tiles, K-chunk cap, occupancy, "
-          f"bwd tiles, bwd direct, all chunks used, 1 KB rows, 128-byte rows -> first (precision, H, B)", flush=True)
+          f"bwd tiles, bwd direct, fused x W, all chunks used, 1 KB rows, 128-byte rows -> first (precision, H, B)", flush=True)
     failures = {}
     cases = sorted(variants.items()) + [(("extra",), s) for s in EXTRA]
     for key, (prec, H, B) in cases:
