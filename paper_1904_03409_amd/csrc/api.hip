@@ -136,8 +136,11 @@ int make_plan(const slstm_dims* d, Plan* p) {
       int occ = 0;
       const bool pipe = !bwd && pipe_ok && NT >= 2 && rec_pipe_built(prec, NT, p->KS);
       // the plain bf16 forward fuses the input projection when one pass covers the group
+      // (x rows copied whole: I % 4 == 0, byte offsets within 32 bits)
       const bool fuse = !bwd && !pipe && rec_fx_built(prec, p->KS) && rec_ntb(prec, NT, p->KS) == NT &&
-                        rec_fx_fits(16 * NT, p->kx);
+                        rec_fx_fits(16 * NT, p->kx) && d->I % 4 == 0 &&
+                        (int64_t)d->T * d->B * d->I * 4 < ((int64_t)1 << 32) &&
+                        rec_lds_bytes(prec, NT, p->KS) + rec_fx_lds_bytes(16 * NT) <= (size_t)160 * 1024;
       RecArgs dummy;
       memset(&dummy, 0, sizeof(dummy));
       FxArgs fdummy;
@@ -147,7 +150,10 @@ int make_plan(const slstm_dims* d, Plan* p) {
       hipError_t e = bwd    ? launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
                      : pipe ? launch_fwd_pipe(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
                             : launch_fwd(dummy, fdummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
-      if (e != hipSuccess) return SLSTM_EDEVICE;
+      if (e != hipSuccess) {
+        (void)hipGetLastError();                  // a failed query leaves no error for later calls
+        return SLSTM_EDEVICE;
+      }
       if (per_xcc <= cu_per_xcc * occ) {
         *NT_out = NT;
         *G_out = G;
@@ -377,11 +383,13 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   // the GEMM's epilogue in fp32
   void* wp = ws + L.wp;
   bf16_t* wpt = bf ? (bf16_t*)wp + (size_t)I * 4 * H : nullptr;
+  // the fused projection copies x rows by 16-byte DMA: x must be 16-byte aligned, else XW
+  const bool fuse = p.fuse && al16(x);
   hipLaunchKernelGGL(k_permute_w, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, W, bf ? nullptr : (float*)wp,
-                     bf ? (bf16_t*)wp : nullptr, p.fuse ? nullptr : wpt, I, H);
+                     bf ? (bf16_t*)wp : nullptr, fuse ? nullptr : wpt, I, H);
   float* xw = (float*)(ws + L.r1);
   // (with the fused projection the recurrent kernel contracts x_t W itself: no XW)
-  if (!p.fuse) {
+  if (!fuse) {
     GemmArgs g;
     memset(&g, 0, sizeof(g));
     g.M = T * B; g.N = 4 * H; g.K = I;
@@ -397,13 +405,12 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   // a3-a6: persistent recurrent kernel
   RecArgs a = rec_args(d, p, ws, L, false);
   if (bf) hipLaunchKernelGGL(k_h0_bf16, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, h0, (bf16_t*)a.hx, (size_t)B * H);
-  a.xw = p.fuse ? nullptr : xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell;
+  a.xw = fuse ? nullptr : xw; a.ops = ops; a.U = U; a.h0 = h0; a.c0 = c0; a.hcell = h_cell; a.ccell = c_cell;
   a.top = top;
   FxArgs fa;
   memset(&fa, 0, sizeof(fa));
-  if (p.fuse) {
+  if (fuse) {
     fa.fuse_x = 1; fa.kx = p.kx; fa.x = x; fa.W = W; fa.bias = b;
-    fa.x_vec = (I % 4 == 0) && al16(x);
   }
   // exchange buffers start as "not yet produced": all-one bits in the state rows the
   // workgroups read from each other

@@ -18,13 +18,12 @@ constexpr int rec_ntb(int prec, int nt, int ks) {
 constexpr size_t rec_lds_bytes(int prec, int ntb, int ks) {
   return (size_t)16 * ntb * rec_lds_ld(prec, ks) * (prec ? 2 : 4);
 }
-// Fused input projection of the plain bf16 forward: the W slice (64 gate columns x kx*32
-// inputs) and two buffers of the step's x rows, bf16, 16-byte row padding.
-constexpr size_t rec_fx_lds_bytes(int rows, int kx) { return (size_t)(64 + 2 * rows) * (kx * 32 + 8) * 2; }
-// Plain bf16 forward variants built with it (K of at most 512), and the largest step it
-// stages: rows x kx*32 inputs of at most 8 four-float vectors per thread.
+// Fused input projection of the plain bf16 forward: a ring of three buffers of the step's x
+// rows (fp32, 1 KB + 16 B per row: I <= 256, i.e. at most 8 chunks of 32, the W slice's
+// register capacity).
+constexpr size_t rec_fx_lds_bytes(int rows) { return (size_t)3 * rows * 260 * 4; }
 constexpr bool rec_fx_built(int prec, int ks) { return prec == 1 && ks <= 16; }
-constexpr bool rec_fx_fits(int rows, int kx) { return rows * kx * 32 <= 8 * 4 * 256; }
+constexpr bool rec_fx_fits(int rows, int kx) { return kx <= 8 && rows > 0; }
 // Backward kernel: LDS for the staged dA rows of the direct path (4 waves x 16 rows of the
 // wave's K range); the direct path is used when this plus the static LDS fits one CU.
 constexpr size_t rec_bwd_lds_bytes(int prec, int ks) { return (size_t)4 * 16 * rec_lds_ld(prec, ks) * (prec ? 2 : 4); }

@@ -42,9 +42,8 @@ struct RecArgs {
 // Fused input projection of the plain bf16 forward (a second argument of that kernel only).
 struct FxArgs {
   int fuse_x;            // 1: the kernel contracts x_t W itself (RecArgs::xw unused)
-  int kx;                // K chunks of 32 covering I
-  int x_vec;             // x rows read as float4 (I % 4 == 0, 16-byte aligned)
-  const float* x;        // [T][B][I]
+  int kx;                // K chunks of 32 covering I (at most 8)
+  const float* x;        // [T][B][I], 16-byte aligned, I % 4 == 0
   const float* W;        // [I][4H] caller layout
   const float* bias;     // [4H] caller layout
 };

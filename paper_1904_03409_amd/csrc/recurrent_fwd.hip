@@ -67,71 +67,65 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
   const bool direct = vec_ok && kmax == KP && (KP * ESZ) % 1024 == 0;
 
-  // ---- fused input projection (bf16, one pass per step): x_t W is contracted in the step
-  // itself. The workgroup's W slice (its 64 gate columns x I, bf16) sits in LDS after the
-  // h_prev tile, the x rows of a step in one of two LDS buffers after it; the x rows of step
-  // t+1 are loaded into registers at the start of step t and written to the other buffer at
-  // its end. The bias is added in the cell update.
+  // ---- fused input projection (bf16, one pass per step, I <= 256): x_t W is contracted in
+  // the step itself. The W slice (this wave's 16 gate columns x I, bf16) sits in registers
+  // like the U slice. The x rows of a step are copied (fp32, by LDS DMA, one row per wave
+  // instruction, 1 KB + 16 B per row) into a ring of three LDS buffers two steps ahead: the
+  // copy of step t+2 is issued right after step t's row wait, so the next wait that covers it
+  // is step t+1's, one step later, and the data is in LDS for step t+2. The bias is added in
+  // the cell update.
   constexpr bool FX_BUILT = rec_fx_built(PREC, KS);
+  constexpr int XLD = 260;                         // LDS row stride of x (fp32): 1 KB + 16 B
   const bool fx = FX_BUILT && f.fuse_x && NPASS == 1;
-  const int I = a.I, kx = f.kx, XLD = kx * 32 + 8, KXP = kx * 32;
-  bf16_t* wsl = reinterpret_cast<bf16_t*>(smem) + (size_t)ROWS_B * LDS_LD;   // [64][XLD]
-  bf16_t* xsb = wsl + (size_t)64 * XLD;                                      // [2][ROWS_B][XLD]
+  const int I = a.I, kx = f.kx;
+  float* xsb = reinterpret_cast<float*>(smem + (size_t)ROWS_B * LDS_LD * ESZ);   // [3][ROWS_B][XLD]
   float4 bias4 = float4{0.f, 0.f, 0.f, 0.f};
-  constexpr int XJ = FX_BUILT ? 8 : 1;             // x vectors (4 floats) per thread and step, at most
-  float4 xr[XJ];
-  const int xn = ROWS_B * KXP / 4;                 // x vectors of one step's rows
-  auto load_x = [&](int tt) {
-#pragma unroll
-    for (int j = 0; j < XJ; ++j) {
-      const int e = (int)threadIdx.x + 256 * j;
-      xr[j] = float4{0.f, 0.f, 0.f, 0.f};
-      if (e >= xn) continue;
-      const int r = e / (KXP / 4), k = (e - r * (KXP / 4)) * 4, b = row0 + r;
-      if (b >= B || k >= I) continue;
-      const float* src = f.x + ((size_t)tt * B + b) * I + k;
-      if (f.x_vec) {
-        xr[j] = *(const float4*)src;
-      } else {
-        xr[j].x = src[0];
-        if (k + 1 < I) xr[j].y = src[1];
-        if (k + 2 < I) xr[j].z = src[2];
-        if (k + 3 < I) xr[j].w = src[3];
-      }
-    }
-  };
-  auto store_x = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < XJ; ++j) {
-      const int e = (int)threadIdx.x + 256 * j;
-      if (e >= xn) continue;
-      const int r = e / (KXP / 4), k = (e - r * (KXP / 4)) * 4;
-      const uint32_t lo = (uint32_t)f32_to_bf16_bits(xr[j].x) | ((uint32_t)f32_to_bf16_bits(xr[j].y) << 16);
-      const uint32_t hi = (uint32_t)f32_to_bf16_bits(xr[j].z) | ((uint32_t)f32_to_bf16_bits(xr[j].w) << 16);
-      *(uint2*)&xsb[((size_t)buf * ROWS_B + r) * XLD + k] = uint2{lo, hi};
+  bf16x8 wreg[FX_BUILT ? 8 : 1];
+  const rsrc_t r_x = make_rsrc(f.x, fx ? (size_t)T * B * I * 4 : 0);
+  const uint32_t x_voff = (fx && lane * 4 < I) ? (uint32_t)lane * 16u : kOOB;   // k >= I reads 0
+  auto dma_x = [&](int tt, int buf) {
+    for (int r = wave; r < ROWS_B; r += 4) {
+      const int b = row0 + r;
+      if (b >= B) break;                            // rows past the batch: outputs are masked
+      bdma16(r_x, x_voff, (uint32_t)(((size_t)tt * B + b) * I * 4),
+             lds_addr(xsb + ((size_t)buf * ROWS_B + r) * XLD));
     }
   };
   // x_t W for every tile of the pass: A = W^T slice rows (unit, gate) of this wave, B = x rows
+  // (fp32 in LDS, rounded to bf16 as they are read)
   auto xpart = [&](f32x4* acc, int buf) {
-    for (int c = 0; c < kx; ++c) {
-      const bf16x8 wv = *(const bf16x8*)&wsl[(size_t)(wave * 16 + l16) * XLD + c * 32 + 8 * lq];
+    if constexpr (FX_BUILT) {
 #pragma unroll
-      for (int nt = 0; nt < NTB; ++nt) {
-        const bf16x8 xv = *(const bf16x8*)&xsb[((size_t)buf * ROWS_B + nt * 16 + l16) * XLD + c * 32 + 8 * lq];
-        acc[nt] = mfma_bf16_16x16x32(wv, xv, acc[nt]);
+      for (int c = 0; c < 8; ++c) {
+        if (c < kx) {
+#pragma unroll
+          for (int nt = 0; nt < NTB; ++nt) {
+            const float* xp = xsb + ((size_t)buf * ROWS_B + nt * 16 + l16) * XLD + c * 32 + 8 * lq;
+            const float4 x0 = *(const float4*)xp, x1 = *(const float4*)(xp + 4);
+            bf16x8 xv;
+            xv[0] = f32_to_bf16(x0.x); xv[1] = f32_to_bf16(x0.y); xv[2] = f32_to_bf16(x0.z); xv[3] = f32_to_bf16(x0.w);
+            xv[4] = f32_to_bf16(x1.x); xv[5] = f32_to_bf16(x1.y); xv[6] = f32_to_bf16(x1.z); xv[7] = f32_to_bf16(x1.w);
+            acc[nt] = mfma_bf16_16x16x32(wreg[c], xv, acc[nt]);
+          }
+        }
       }
     }
   };
   if (fx) {
-    // W slice: column m of the slice is gate m % 4 of unit 16w + m / 4 (the U slice's order)
-    for (int i = threadIdx.x; i < 64 * KXP; i += 256) {
-      const int m = i / KXP, k = i - m * KXP, unit = w * 16 + m / 4;
-      const float v = (unit < H && k < I) ? f.W[(size_t)k * H4 + (m & 3) * H + unit] : 0.f;
-      wsl[(size_t)m * XLD + k] = f32_to_bf16_bits(v);
-    }
+    // W slice: row m = l16 of this wave's tile is gate m % 4 of unit unit_base + m / 4 (the U
+    // slice's order); chunk c holds inputs c*32 + 8lq .. +7, zero past I
+    const int unit = unit_base + (l16 >> 2), gate = l16 & 3;
+#pragma unroll
+    for (int c = 0; c < (FX_BUILT ? 8 : 1); ++c)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = c * 32 + 8 * lq + j;
+        wreg[c][j] = f32_to_bf16((unit < H && k < I) ? f.W[(size_t)k * H4 + gate * H + unit] : 0.f);
+      }
     if (u < H) bias4 = float4{f.bias[u], f.bias[H + u], f.bias[2 * H + u], f.bias[3 * H + u]};
-    load_x(0);
-    store_x(0);
+    dma_x(0, 0);
+    if (T > 1) dma_x(1, 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
 
   // rows of this lane in the MFMA output layout: tile ti covers rows ti*16 .. ti*16+15
@@ -195,7 +189,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
       if (fx) {
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = bias4;
-        if (more) load_x(t + 1);
       } else {
 #pragma unroll
         for (int ti = 0; ti < NT; ++ti) xw_nxt[ti] = xw_at(more ? t + 1 : t, ti);
@@ -210,7 +203,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
       // ---- gather this pass's h_prev rows into LDS; granules that still hold the fill are
       // fetched again until their producers' stores have arrived. With the fused input
       // projection, its MFMAs run while the rows are in flight.
-      if (fx && !direct) xpart(acc, t & 1);
+      if (fx && !direct) xpart(acc, t % 3);
       if (direct) {
 #pragma unroll
         for (int i = 0; i < NSEG_W; ++i) {
@@ -227,7 +220,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
             else __builtin_amdgcn_global_load_lds(gp, (lds_ptr_t)lp, 16, 0, 0);
           }
         }
-        if (fx) xpart(acc, t & 1);
+        if (fx) xpart(acc, t % 3);
       } else {
         constexpr int VW = PREC ? 8 : 4;
         if (vec_ok) {
@@ -378,6 +371,8 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
         break;
       }
       if (clk && threadIdx.x == 0 && nb == 0) clk[t * 4 + 1] = wall_clock64();
+      // x rows of step t+2 into the buffer step t-1 used (read before step t-1 ended)
+      if (fx && t + 2 < T) dma_x(t + 2, (t + 2) % 3);
       if (PREC == 0 && nb == 0) {
         // fp32 steps are long: the producer indices read at step t+1 (top[t], published one
         // step ago) and the next step's input projection are in flight during the MFMAs
@@ -456,8 +451,6 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
     }
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) { xw_cur[ti] = xw_nxt[ti]; cp_cur[ti] = cp_nxt[ti]; }
-    // x rows of step t+1: the other buffer, last read in step t-1
-    if (fx && more) store_x((t + 1) & 1);
     if (!a.poll) {
       // barrier mode: every state of step t is complete past this point
       if (group_barrier(&a.ctl[CTL_BAR_F + g * 16], (uint32_t)(a.NW * (t + 2)), a.ctl, a.spin_limit, &s_abort[1]))
@@ -481,7 +474,7 @@ static hipError_t launch_fwd_t(const RecArgs& a, const FxArgs& f, dim3 grid, hip
   if (f.fuse_x) {
     // the fused projection: built variants, one pass per step, x rows within the staging registers
     if (!rec_fx_built(P, KS) || NTB != NT || !rec_fx_fits(16 * NT, f.kx)) return hipErrorInvalidValue;
-    shm += rec_fx_lds_bytes(16 * NTB, f.kx);
+    shm += rec_fx_lds_bytes(16 * NTB);
   }
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
   if (e != hipSuccess) return e;
