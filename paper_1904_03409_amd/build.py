@@ -4,7 +4,12 @@ Every kernel's resource usage is read from the compiler's resource report, and t
 fails if a kernel that counts its own outstanding vector-memory operations (the wide
 forward, and the backward variants built with direct dA staging) uses scratch memory:
 spill loads and stores share that counter, so a counted wait would no longer wait for the
-loads it counts."""
+loads it counts.
+
+The device assembly of every source is kept (-save-temps) and scanned for one hazard the
+compiler has been seen to miss: an MFMA chain at the end of a basic block whose results are
+read at a branch target with fewer wait states than the compiler inserts for the same read
+in straight-line code (the read then returns a stale accumulator). The build fails on one."""
 from __future__ import annotations
 
 import os
@@ -57,14 +62,86 @@ def resource_report(text: str) -> dict:
     return out
 
 
+# wait states between an MFMA and a read of its result that hipcc inserts in straight-line code
+MFMA_WAITS = {"v_mfma_f32_16x16x4_f32": 10, "v_mfma_f32_16x16x32_bf16": 8}
+
+
+def _regs(tok: str) -> set:
+    m = re.fullmatch(r"([av])\[(\d+):(\d+)\]", tok)
+    if m:
+        return {(m.group(1), i) for i in range(int(m.group(2)), int(m.group(3)) + 1)}
+    m = re.fullmatch(r"([av])(\d+)", tok)
+    return {(m.group(1), int(m.group(2)))} if m else set()
+
+
+def _split(line: str):
+    parts = line.split(None, 1)
+    if not parts:
+        return "", []
+    return parts[0], ([t.strip() for t in parts[1].split(",")] if len(parts) > 1 else [])
+
+
+def _wait_states(line: str) -> int:
+    op, args = _split(line)
+    return int(args[0], 0) + 1 if op == "s_nop" else 1
+
+
+def mfma_branch_hazards(asm: str) -> list:
+    """Reads of MFMA results at a branch target with too few wait states since the MFMA.
+
+    For every branch whose block ends with an MFMA (no other branch in between), the wait
+    states from that MFMA to the branch are added to those from the target label up to the
+    first instruction that reads the MFMA's destination registers (following fall-through,
+    stopping at the next branch or MFMA); a total below MFMA_WAITS is reported."""
+    lines = [ln.split(";")[0].strip() for ln in asm.splitlines()]
+    labels = {ln[:-1]: i for i, ln in enumerate(lines) if re.fullmatch(r"\.?LBB\w+:", ln)}
+    out, fn = [], "?"
+    for i, ln in enumerate(lines):
+        if re.fullmatch(r"_Z\w+:", ln):
+            fn = ln[:-1]
+        m = re.match(r"(s_cbranch_\w+|s_branch)\s+(\.LBB\w+)", ln)
+        if not m or m.group(2) not in labels:
+            continue
+        w, dst, need = 1, None, 0
+        for t in reversed(lines[max(0, i - 32):i]):
+            if not t or t.endswith(":") or t.startswith(".") or t.startswith(";"):
+                continue
+            if t.startswith("v_mfma"):
+                op, args = _split(t)
+                dst, need = _regs(args[0]), MFMA_WAITS.get(op, 19)
+                break
+            if t.startswith(("s_cbranch", "s_branch", "s_setpc", "s_endpgm")):
+                break
+            w += _wait_states(t)
+        if not dst:
+            continue
+        for t in lines[labels[m.group(2)] + 1:labels[m.group(2)] + 64]:
+            if not t or t.endswith(":") or t.startswith("."):
+                continue
+            op, args = _split(t)
+            if op.startswith("v_mfma") or op.startswith(("s_cbranch", "s_branch", "s_endpgm")) or w >= need:
+                break
+            if set().union(*[_regs(a) for a in args[1:]]) & dst:
+                out.append(f"{fn}: {op} at {m.group(2)} reads an MFMA result after {w} wait states (needs {need})")
+                break
+            w += _wait_states(t)
+    return out
+
+
 def _compile(src: str):
     obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-save-temps", "-c", os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True, cwd=BUILD)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
         raise RuntimeError(f"hipcc failed for {src}")
-    return obj, resource_report(r.stderr)
+    stem = src[:-len(".hip")]
+    for f in os.listdir(BUILD):   # keep the device assembly and the objects only
+        if f.startswith(stem + "-") and not f.endswith("-gfx950.s") or f.startswith(src + "-"):
+            os.remove(os.path.join(BUILD, f))
+    with open(os.path.join(BUILD, f"{stem}-hip-amdgcn-amd-amdhsa-gfx950.s")) as fh:
+        hazards = mfma_branch_hazards(fh.read())
+    return obj, resource_report(r.stderr), hazards
 
 
 def build(jobs: int | None = None) -> str:
@@ -72,10 +149,13 @@ def build(jobs: int | None = None) -> str:
     jobs = jobs or min(len(SOURCES), max(1, (os.cpu_count() or 4)))
     with ThreadPoolExecutor(max_workers=jobs) as ex:
         res = list(ex.map(_compile, SOURCES))
-    objs = [o for o, _ in res]
-    bad = {k: v for _, rep in res for k, v in rep.items() if v > 0 and counted_waits(k)}
+    objs = [o for o, _, _ in res]
+    bad = {k: v for _, rep, _ in res for k, v in rep.items() if v > 0 and counted_waits(k)}
     if bad:
         raise RuntimeError(f"kernels with counted memory waits use scratch (bytes/lane): {bad}")
+    hazards = [h for _, _, hz in res for h in hz]
+    if hazards:
+        raise RuntimeError("MFMA results read too early after a branch:\n" + "\n".join(hazards[:20]))
     tmp = LIB + ".tmp"
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,-z,defs", "-o", tmp, *objs])
     os.replace(tmp, LIB)
@@ -87,7 +167,7 @@ def scratch_report() -> dict:
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         res = list(ex.map(_compile, SOURCES))
-    return {k: v for _, rep in res for k, v in rep.items()}
+    return {k: v for _, rep, _ in res for k, v in rep.items()}
 
 
 if __name__ == "__main__":

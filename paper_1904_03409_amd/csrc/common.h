@@ -54,6 +54,17 @@ __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
 __device__ __forceinline__ f32x4 mfma_bf16_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+// Results of an MFMA chain in AGPRs may be read only some wait states after its last
+// instruction (10 for the fp32 16x16x4 form, 8 for the bf16 16x16x32 form: the counts the
+// compiler itself inserts in straight-line code). The compiler's hazard pass misses them on
+// a branch edge that leaves the MFMA's block (measured: 3 wait states on the taken path
+// round a conditional store, and the fourth accumulator read stale). This drain issues 12
+// wait states after the chain, as an asm statement that takes the accumulators as operands
+// and so runs after the chain's last MFMA and before any read of its results; the compiler
+// sees the asm, not an MFMA, as their last writer.
+__device__ __forceinline__ void mfma_drain(f32x4& a, f32x4& b) {
+  asm volatile("s_nop 7\n\ts_nop 3" : "+a"(a), "+a"(b));
+}
 
 // Gate nonlinearities from the hardware base-2 exponential and reciprocal (about one ulp
 // each): sigma(z) = 1 / (1 + 2^(-z log2 e)); tanh(x) = 2 sigma(2x) - 1. Absolute error is

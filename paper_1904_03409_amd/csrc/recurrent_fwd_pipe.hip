@@ -258,6 +258,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
           acc = mfma_bf16_16x16x32(ureg16[c], fr[c % (PD + 1)], acc);
         }
       }
+      mfma_drain(acc0, acc1);
       acc_pend = acc0 + acc1;
       if (clk && threadIdx.x == 0 && p < 2) stamp[2 * p + 1] = wall_clock64();
     }
