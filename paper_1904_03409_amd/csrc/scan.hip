@@ -286,32 +286,73 @@ __global__ void __launch_bounds__(256) k_gather_hprev(const int32_t* __restrict_
 // r is src + r*ld (fp32 or bf16); with a producer table (gtop != null) row r = t*B + b is
 // the state read at step t (Hprev): h0[b] for t = 0, else the state produced at
 // top[t-1][b] (-1 = h0), taken from the bf16 state copy (slot s+1 = step s, slot 0 = h0).
-// 64x64 tiles through LDS: reads and writes are both along contiguous rows.
+// 64x64 tiles through LDS. When rows, columns and both base addresses allow it, every
+// global access moves 16 bytes (8 bf16 or 4 fp32 along a source row, 8 consecutive k of an
+// output row); otherwise one element per access.
 __global__ void __launch_bounds__(256) k_transpose_bf16(const void* __restrict__ src, int src_f32, int ld, int cols,
                                                         const int32_t* __restrict__ prow,
                                                         const uint32_t* __restrict__ count, int ldo,
                                                         const int32_t* __restrict__ gtop, int B,
                                                         bf16_t* __restrict__ out, uint32_t* ctl) {
-  __shared__ bf16_t tile[64][66];
+  __shared__ __align__(16) bf16_t tile[64][72];             // 144-byte rows: 16-byte aligned
   const int rows = (int)min(*count, (uint32_t)ldo);
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
   if (r0 >= rows + ((64 - (rows & 63)) & 63)) return;      // past the rounded extent
-  const int tc = threadIdx.x & 63, tr = threadIdx.x >> 6;   // 4 rows per pass
-  for (int i = tr; i < 64; i += 4) {
-    const int r = r0 + i, c = c0 + tc;
-    bf16_t v = 0;
-    if (r < rows && c < cols) {
-      const int pr = prow[r];
-      if (gtop) {
-        const int t = pr / B, b = pr - t * B;
-        const int s = (t == 0) ? -1 : checked_src(gtop[(size_t)pr - B], t - 1, ctl);
-        v = ((const bf16_t*)src)[((size_t)(s + 1) * B + b) * ld + c];
-      } else if (src_f32) {
-        v = f32_to_bf16_bits(((const float*)src)[(size_t)pr * ld + c]);
-      } else {
-        v = ((const bf16_t*)src)[(size_t)pr * ld + c];
+  const int E = src_f32 ? 4 : 8;                            // elements per 16 bytes of source
+  const bool vec = ((uintptr_t)src & 15u) == 0 && ((uintptr_t)out & 15u) == 0 && ld % E == 0 && cols % E == 0 &&
+                   ldo % 8 == 0;
+  // source row of tile row i (-1: zero row)
+  auto src_row = [&](int r) -> long long {
+    if (r >= rows) return -1;
+    const int pr = prow[r];
+    if (!gtop) return pr;
+    const int t = pr / B, b = pr - t * B;
+    const int s = (t == 0) ? -1 : checked_src(gtop[(size_t)pr - B], t - 1, ctl);
+    return (long long)(s + 1) * B + b;
+  };
+  if (vec) {
+    if (src_f32) {
+      const int tc = (threadIdx.x & 15) * 4, tr = threadIdx.x >> 4;   // 16 rows per pass
+      for (int i = tr; i < 64; i += 16) {
+        const long long sr = src_row(r0 + i);
+        const int c = c0 + tc;
+        uint2 v = uint2{0u, 0u};
+        if (sr >= 0 && c < cols) {
+          const float4 f = *(const float4*)((const float*)src + (size_t)sr * ld + c);
+          v.x = (uint32_t)f32_to_bf16_bits(f.x) | ((uint32_t)f32_to_bf16_bits(f.y) << 16);
+          v.y = (uint32_t)f32_to_bf16_bits(f.z) | ((uint32_t)f32_to_bf16_bits(f.w) << 16);
+        }
+        *(uint2*)&tile[i][tc] = v;
+      }
+    } else {
+      const int tc = (threadIdx.x & 7) * 8, tr = threadIdx.x >> 3;     // 32 rows per pass
+      for (int i = tr; i < 64; i += 32) {
+        const long long sr = src_row(r0 + i);
+        const int c = c0 + tc;
+        uint4 v = uint4{0u, 0u, 0u, 0u};
+        if (sr >= 0 && c < cols) v = *(const uint4*)((const bf16_t*)src + (size_t)sr * ld + c);
+        *(uint4*)&tile[i][tc] = v;
       }
     }
+    __syncthreads();
+    const int kk = (threadIdx.x & 7) * 8;                   // 8 consecutive k of one column
+    for (int ci = threadIdx.x >> 3; ci < 64; ci += 32) {
+      const int c = c0 + ci, r = r0 + kk;
+      if (c >= cols || r >= ldo) continue;
+      uint32_t w[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) w[m] = (uint32_t)tile[kk + 2 * m][ci] | ((uint32_t)tile[kk + 2 * m + 1][ci] << 16);
+      *(uint4*)&out[(size_t)c * ldo + r] = uint4{w[0], w[1], w[2], w[3]};
+    }
+    return;
+  }
+  const int tc = threadIdx.x & 63, tr = threadIdx.x >> 6;   // 4 rows per pass
+  for (int i = tr; i < 64; i += 4) {
+    const long long sr = src_row(r0 + i);
+    const int c = c0 + tc;
+    bf16_t v = 0;
+    if (sr >= 0 && c < cols)
+      v = src_f32 ? f32_to_bf16_bits(((const float*)src)[(size_t)sr * ld + c]) : ((const bf16_t*)src)[(size_t)sr * ld + c];
     tile[i][tc] = v;
   }
   __syncthreads();
