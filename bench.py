@@ -227,16 +227,17 @@ def cpu_baseline(wl, gpu_out=None, target_s=12.0):
     t0 = time.perf_counter()
     oracle.run(wl, sel=np.arange(n0, dtype=np.int32), mode="f32", threads=th, native=True)
     dt0 = time.perf_counter() - t0
-    # sample size for about target_s of CPU work, then the median of three runs of it
-    # (one run when a single run already takes more than a third of that)
+    # sample size for about target_s of CPU work (at most the whole batch), then runs of it
+    # until about target_s have been spent (at most 9); the median run is reported
     n = n0 if dt0 >= target_s / 4 else int(min(wl.B, max(n0, n0 * target_s / max(dt0, 1e-3))))
-    est = dt0 * n / n0
     times = []
     ref = None
-    for _ in range(3 if 3 * est <= 1.5 * target_s else 1):
+    while True:
         t0 = time.perf_counter()
         ref = oracle.run(wl, sel=np.arange(n, dtype=np.int32), mode="f32", threads=th, native=True)
         times.append(time.perf_counter() - t0)
+        if len(times) >= 9 or sum(times) + float(np.median(times)) > target_s:
+            break
     dt = float(np.median(times))
     pushes = int((wl.ops[:, :n] == 1).sum())
     model, ncpu = host_cpu()
