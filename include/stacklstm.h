@@ -177,6 +177,8 @@ typedef struct {
   int32_t bwd_direct;      /* backward: dA rows staged in LDS by DMA (1) or read into registers (0) */
   int32_t fused_x;         /* 1: the forward kernel contracts x_t W itself (no separate input
                               projection GEMM; bf16, plain forward, one pass per step) */
+  int32_t bwd_split;       /* 1: the backward contracts dA U^T over each workgroup's own gate
+                              columns and exchanges partial sums instead of dA rows */
 } slstm_plan;
 
 /* Fills `out` for `d`; returns a status like the entry points. */

@@ -45,8 +45,9 @@ def counted_waits(name: str) -> bool:
     """Kernels (mangled names) whose code counts outstanding vector-memory operations."""
     if name.startswith("_Z10k_fwd_wide"):
         return True
-    m = re.match(r"_Z5k_bwdILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)E", name)
-    return bool(m) and bwd_direct_built(int(m.group(1)), int(m.group(2)), int(m.group(3)))
+    # k_bwd<prec, NT, KS, OCC, GS>: the gate-split variants (GS = true) have no direct staging
+    m = re.match(r"_Z5k_bwdILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELb([01])E", name)
+    return bool(m) and m.group(5) == "0" and bwd_direct_built(int(m.group(1)), int(m.group(2)), int(m.group(3)))
 
 
 def resource_report(text: str) -> dict:

@@ -73,12 +73,15 @@ struct Plan {
   int fuse, kx;               // fuse: the plain bf16 forward contracts x_t W itself (kx chunks of 32)
   int wide, NWw;              // wide: the forward runs the 32-unit kernel (NWw workgroups per group)
   int NTb, Gb, per_xcc_b;
+  int gs;                     // the backward runs the gate-split contraction
   int splits_w, splits_u;
 };
 
 struct Layout {
   size_t ctl, stack, dep, wp, r1, stash, hx, fwd_end, xbt, hp, dat, dh, dc, dbp, part, prow, total;
 };
+
+Layout layout(const slstm_dims* d);
 
 // Push-row count padded to the K tile: leading dimension of the transposed bf16 operands
 size_t padded_rows(const slstm_dims* d) { return ((size_t)d->T * d->B + 63) / 64 * 64; }
@@ -128,6 +131,12 @@ int make_plan(const slstm_dims* d, Plan* p) {
   const bool pipe_ok = d->H % (prec ? 8 : 4) == 0 && p->ks_eff == p->KS && p->KS >= 16;
   p->kx = (d->I + 31) / 32;
   p->fuse = 0;
+  p->gs = 0;
+  // the backward's gate-split contraction covers exactly H units with whole M tiles; its
+  // partial sums (two step buffers of G x 16*NT rows x NW x H fp32) use the post-loop GEMMs'
+  // partials area
+  const Layout Lp = layout(d);
+  const bool gs_ok = p->ks_eff == p->KS && p->KS * KC == d->H;
   auto pick = [&](bool bwd, int* NT_out, int* G_out, int* per_out, int* pipe_out) -> int {
     for (int NT = 1; NT <= 8; NT *= 2) {
       int G = (d->B + 16 * NT - 1) / (16 * NT);
@@ -147,6 +156,9 @@ int make_plan(const slstm_dims* d, Plan* p) {
       memset(&fdummy, 0, sizeof(fdummy));
       fdummy.fuse_x = fuse ? 1 : 0;
       fdummy.kx = p->kx;
+      const bool gs = bwd && gs_ok && rec_bwd_gs_built(prec, NT, p->KS) &&
+                      (size_t)2 * G * 16 * NT * p->NW * d->H * 4 <= Lp.prow - Lp.part;
+      dummy.bwd_gs = gs ? 1 : 0;
       hipError_t e = bwd    ? launch_bwd(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
                      : pipe ? launch_fwd_pipe(dummy, prec, NT, p->KS, dim3(0), nullptr, &occ)
                             : launch_fwd(dummy, fdummy, prec, NT, p->KS, dim3(0), nullptr, &occ);
@@ -160,6 +172,7 @@ int make_plan(const slstm_dims* d, Plan* p) {
         *per_out = per_xcc;
         if (pipe_out) *pipe_out = pipe ? 1 : 0;
         if (!bwd) p->fuse = fuse ? 1 : 0;
+        if (bwd) p->gs = gs ? 1 : 0;
         return SLSTM_OK;
       }
     }
@@ -267,7 +280,7 @@ int read_status(const uint32_t* ctl, hipStream_t st) {
 // per CU).
 bool bwd_direct_for(const slstm_dims* d, const Plan& p) {
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
-  return rec_bwd_direct_built(d->precision, p.NTb, p.KS) && ((size_t)d->H * esz) % 1024 == 0 &&
+  return !p.gs && rec_bwd_direct_built(d->precision, p.NTb, p.KS) && ((size_t)d->H * esz) % 1024 == 0 &&
          p.KS * rec_kc(d->precision) == d->H &&
          rec_bwd_lds_bytes(d->precision, p.KS) + rec_bwd_static_lds(p.NTb) <= 160 * 1024 &&
          p.per_xcc_b <= std::max(1, device_cus() / 8);
@@ -297,6 +310,10 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   const int esz = d->precision == SLSTM_BF16_GEMM ? 2 : 4;
   a.coh_rows = ((size_t)d->H * esz) % 128 != 0;
   a.bwd_direct = bwd_direct_for(d, p) ? 1 : 0;
+  if (bwd && p.gs) {
+    a.bwd_gs = 1;
+    a.gs_part = (float*)(ws + L.part);   // free until the post-loop GEMMs
+  }
   return a;
 }
 
@@ -342,6 +359,7 @@ int stacklstm_plan(const slstm_dims* d, slstm_plan* out) {
   out->bwd_tiles = p.NTb;
   out->bwd_direct = bwd_direct_for(d, p) ? 1 : 0;
   out->fused_x = p.fuse;
+  out->bwd_split = p.gs;
   return SLSTM_OK;
 }
 

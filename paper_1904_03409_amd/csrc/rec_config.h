@@ -43,6 +43,16 @@ constexpr bool rec_bwd_direct_built(int prec, int nt, int ks) {
          rec_occ(prec, ks) == 1 && nt <= 4;
 }
 
+// Backward instantiations built with the gate-split contraction as well (the planner
+// chooses it when the contraction's K columns are exactly H: H = KS * KC; at least two M
+// tiles per wave, at most 32 workgroups per group, one workgroup per CU). fp32 only: there a
+// push row's dA is 8 KB against 2 KB of partial sums (large fp32 backward 1.68 -> 1.40 ms);
+// in bf16 the row is 4 KB, and the extra partial stores made the large backward slower
+// (1.26 -> 1.48 ms).
+constexpr bool rec_bwd_gs_built(int prec, int nt, int ks) {
+  return prec == 0 && ks * rec_kc(prec) >= 128 && ks * rec_kc(prec) <= 512 && nt <= 2 && rec_occ(prec, ks) == 1;
+}
+
 #define REC_CASES(X) \
   X(0, 1, 4) X(0, 1, 8) X(0, 1, 16) X(0, 1, 32) \
   X(0, 2, 4) X(0, 2, 8) X(0, 2, 16) X(0, 2, 32) \

@@ -12,6 +12,8 @@ struct RecArgs {
   int coh_rows;
   int bwd_direct;        // backward stages dA rows with global_load_lds (host checks the LDS fits)
   int poll;              // 1: workgroups exchange rows by polling fill-marked data; 0: group barrier per step
+  int bwd_gs;            // backward: gate-split contraction (partial sums exchanged instead of dA rows);
+                         // this int fills the padding before the first pointer (layout unchanged)
   const float* xw;       // [T*B][4H] gate-interleaved, bias included (forward; null when fused)
   const int8_t* ops;     // [T][B]
   const float* U;        // [H][4H] caller layout (gate-major columns)
@@ -23,7 +25,10 @@ struct RecArgs {
   float* stash;          // [T][B][4H] gate activations i, f, g, o, gate-interleaved
   int32_t* top;          // [T][B]     producer step of the state returned at step t (-1 = initial),
                          //            complete before the forward kernel starts (op scan)
-  float* htop;           // [T][B][H] or null: state at the top after step t (wide forward writes it)
+  union {
+    float* htop;         // forward: [T][B][H] or null: state at the top after step t (wide forward writes it)
+    float* gs_part;      // backward with bwd_gs: [2][G][16*NT][NW][H] partial sums of dA U^T by workgroup
+  };
   float* ctop;           // [T][B][H] (with htop)
   uint32_t* ctl;         // control block (status, barrier counters)
   // backward

@@ -25,6 +25,15 @@
 // sums are added in LDS in a fixed order. Every gradient element is owned by one thread,
 // so there are no atomics. Workgroup barriers that only order LDS accesses do not wait for
 // outstanding global loads.
+//
+// Gate-split variant (GS): the contraction is cut over gate columns instead. Workgroup w
+// holds U[:, its own 64 gate columns] (the columns its cell backward produces), contracts
+// its own dA rows (kept in LDS, no exchange of dA) into partial sums for every unit, stores
+// them, and after the group barrier adds the NW partials of its own 16 units in a fixed order
+// (quarters of the workgroups, each in workgroup order). Per push row a workgroup then reads
+// NW*16 floats (2 KB at H = 512) instead of the row's 4H dA values (8 KB fp32, 4 KB bf16).
+// The partials are double-buffered by step parity: a workgroup can be at most one step ahead
+// of the slowest reader, since the next barrier waits for it.
 #include "common.h"
 #include "recurrent.h"
 #include "rec_config.h"
@@ -36,7 +45,7 @@ namespace {
 __device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 }  // namespace
 
-template <int PREC, int NT, int KS, int OCC>
+template <int PREC, int NT, int KS, int OCC, bool GS>
 __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;
   constexpr int BG = NT * 16;
@@ -55,6 +64,10 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   __shared__ float s_db[16][16][4];
   __shared__ int s_g, s_w;
   __shared__ int s_abort;                          // a wait for dA rows gave up
+  // GS: this workgroup's dA rows (its 64 gate columns, by row of the group), fp32 or bf16
+  constexpr int SDL = PREC ? 72 : 68;                 // row stride (elements): 16-byte pad
+  using sd_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
+  __shared__ __align__(16) sd_t s_dA[GS ? BG : 1][GS ? SDL : 1];
 
   claim_group_slot(a.ctl + CTL_XCC_SLOT_B, a.G, a.NW, &s_g, &s_w);
   const int g = s_g, w = s_w;
@@ -68,13 +81,34 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   const rsrc_t r_dA = make_rsrc(a.dA, (size_t)T * B * H4 * ESZ);
 
   // ---- U^T slice: A(m = unit 16w + l16, k = gate column q*H + kk) = U[unit][caller column]
+  // (GS: A(m = unit wave*H/4 + mt*16 + l16, k = this workgroup's gate column 64w + kk); the
+  // same number of registers: H/64 M tiles of 64 / KC chunks per wave)
   const int a_unit = w * 16 + l16;
   const bool a_ok = a_unit < H;
   const float* Urow = a.U + (size_t)(a_ok ? a_unit : 0) * H4;
   float ureg32[PREC ? 1 : KS][4];
   bf16x8 ureg16[PREC ? KS : 1];
+  constexpr int GCH = 64 / KC;                      // GS: K chunks of the own gate columns
+  if constexpr (GS) {
+    static_assert(KS % GCH == 0 && (KS / GCH) % 2 == 0, "GS: whole M tiles, two at a time");
 #pragma unroll
-  for (int c = 0; c < KS; ++c) {
+    for (int e = 0; e < KS; ++e) {
+      const int mt = e / GCH, ch = e % GCH;
+      const int unit = wave * (KS / GCH) * 16 + mt * 16 + l16;
+      const float* Ur = a.U + (size_t)(unit < H ? unit : 0) * H4;
+      if constexpr (PREC == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          ureg32[e][j] = unit < H ? Ur[perm_to_orig(w * 64 + ch * 16 + 4 * lq + j, H)] : 0.f;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          ureg16[e][j] = f32_to_bf16(unit < H ? Ur[perm_to_orig(w * 64 + ch * 32 + 8 * lq + j, H)] : 0.f);
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < KS && !GS; ++c) {
     if constexpr (PREC == 0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -116,7 +150,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
   const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
-  const bool direct = rec_bwd_direct_built(PREC, NT, KS) && a.bwd_direct != 0;
+  const bool direct = rec_bwd_direct_built(PREC, NT, KS) && !GS && a.bwd_direct != 0;
   using elem_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
   elem_t* wbuf = reinterpret_cast<elem_t*>(dsm) + (size_t)wave * 16 * QLD;
   if (direct)
@@ -288,6 +322,17 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         gh[i] = gc[i] = 0.f;
         dep[i] += 1;
       }
+      if constexpr (GS) {
+        // the contraction's operand: this row's dA of the thread's unit (rows the list does
+        // not name are never read)
+        if constexpr (PREC == 0) {
+          *(float4*)&s_dA[prow[i]][4 * uu] = dA4;
+        } else {
+          bf16_t q[4] = {f32_to_bf16_bits(dA4.x), f32_to_bf16_bits(dA4.y), f32_to_bf16_bits(dA4.z),
+                         f32_to_bf16_bits(dA4.w)};
+          *(uint2*)&s_dA[prow[i]][4 * uu] = *(const uint2*)q;
+        }
+      }
       if (pok[i] && c_op[i] == 1) {               // only push rows are read (exchange, post-loop GEMMs)
         const size_t ao = ((size_t)t * B + b) * H4 + 4 * u;
         if constexpr (PREC == 0) {
@@ -309,7 +354,73 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       const int crow0 = cr < s_nlive ? s_crow[cr] : 0;
       soff0 = (((uint32_t)t * B + row0 + crow0) * H4 + wave * H) * ESZ;
     };
-    if (a.poll) {
+    if constexpr (GS) {
+      // own dA rows and the row list complete; partial sums of every unit for the listed rows
+      lds_sync();
+      const int nl = s_nlive;
+      // partials of compacted row ci: P[step parity][group][ci][workgroup][unit] (only the listed
+      // rows' slots are touched, so a step's partials stay small enough for the XCC's L2)
+      float* Pp = a.gs_part + (size_t)((t & 1) * a.G + g) * BG * a.NW * H;
+      for (int jt = 0; jt * 16 < nl; ++jt) {
+        const int ci = jt * 16 + l16;
+        const bool lv = ci < nl;
+        const int r = lv ? s_crow[ci] : 0;
+        constexpr int MT = KS / GCH;                // M tiles of this wave
+        float* prow_p = Pp + ((size_t)ci * a.NW + w) * H + wave * MT * 16 + 4 * lq;
+        if constexpr (PREC == 0) {
+          float4 bf[GCH];
+#pragma unroll
+          for (int ch = 0; ch < GCH; ++ch)
+            bf[ch] = lv ? *(const float4*)&s_dA[r][ch * 16 + 4 * lq] : float4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int mt = 0; mt < MT; mt += 2) {
+            f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
+#pragma unroll
+            for (int ch = 0; ch < GCH; ++ch) {
+              acc0 = mfma_f32_16x16x4(ureg32[mt * GCH + ch][0], bf[ch].x, acc0);
+              acc1 = mfma_f32_16x16x4(ureg32[(mt + 1) * GCH + ch][0], bf[ch].x, acc1);
+              acc0 = mfma_f32_16x16x4(ureg32[mt * GCH + ch][1], bf[ch].y, acc0);
+              acc1 = mfma_f32_16x16x4(ureg32[(mt + 1) * GCH + ch][1], bf[ch].y, acc1);
+              acc0 = mfma_f32_16x16x4(ureg32[mt * GCH + ch][2], bf[ch].z, acc0);
+              acc1 = mfma_f32_16x16x4(ureg32[(mt + 1) * GCH + ch][2], bf[ch].z, acc1);
+              acc0 = mfma_f32_16x16x4(ureg32[mt * GCH + ch][3], bf[ch].w, acc0);
+              acc1 = mfma_f32_16x16x4(ureg32[(mt + 1) * GCH + ch][3], bf[ch].w, acc1);
+            }
+            mfma_drain(acc0, acc1);
+            // lane: units 4*lq .. 4*lq+3 of M tiles mt and mt+1, row ci
+            if (lv) {
+              *(float4*)(prow_p + mt * 16) = float4{acc0[0], acc0[1], acc0[2], acc0[3]};
+              *(float4*)(prow_p + (mt + 1) * 16) = float4{acc1[0], acc1[1], acc1[2], acc1[3]};
+            }
+          }
+        } else {
+          bf16x8 bf[GCH];
+#pragma unroll
+          for (int ch = 0; ch < GCH; ++ch) {
+            uint4 z = uint4{0u, 0u, 0u, 0u};
+            if (lv) z = *(const uint4*)&s_dA[r][ch * 32 + 8 * lq];
+            bf[ch] = __builtin_bit_cast(bf16x8, z);
+          }
+#pragma unroll
+          for (int mt = 0; mt < MT; mt += 2) {
+            f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
+#pragma unroll
+            for (int ch = 0; ch < GCH; ++ch) {
+              acc0 = mfma_bf16_16x16x32(ureg16[mt * GCH + ch], bf[ch], acc0);
+              acc1 = mfma_bf16_16x16x32(ureg16[(mt + 1) * GCH + ch], bf[ch], acc1);
+            }
+            mfma_drain(acc0, acc1);
+            if (lv) {
+              *(float4*)(prow_p + mt * 16) = float4{acc0[0], acc0[1], acc0[2], acc0[3]};
+              *(float4*)(prow_p + (mt + 1) * 16) = float4{acc1[0], acc1[1], acc1[2], acc1[3]};
+            }
+          }
+        }
+      }
+      group_arrive(&a.ctl[CTL_BAR_B + g * 16]);
+      prefetch(t);
+      if (group_wait(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_abort)) break;
+    } else if (a.poll) {
       lds_sync();
       if (direct) row_offsets0();
     } else {
@@ -326,12 +437,36 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     constexpr int CG = LEAN ? 2 : 8;                // lean: measured fastest (fewer spills)
     constexpr int NG = (KS + CG - 1) / CG;
     const int nlive = s_nlive;
-    if (!direct || nlive == 0) prefetch(t);
+    if (!GS && (!direct || nlive == 0)) prefetch(t);
     // whole 1 KB row segments, at most two per staged row (H of at most 512 fp32 / 1024 bf16);
     // not at two workgroups per CU, where the staged rows do not fit beside the other
     // workgroup's LDS (the host then never asks for it)
-    constexpr bool kDirectOk = rec_bwd_direct_built(PREC, NT, KS);
-    if (kDirectOk && direct) {
+    constexpr bool kDirectOk = rec_bwd_direct_built(PREC, NT, KS) && !GS;
+    if constexpr (GS) {
+      // (the contraction ran before the barrier) The NW workgroups' partial sums of this
+      // workgroup's 16 units, per listed row: item (row, quarter q of the workgroups, 4 units)
+      // adds its NW/4 partials in workgroup order into red[q]; the four quarters are added as
+      // in the other variants. Every item's loads are issued together (one round trip).
+      const int NWr = a.NW, WPG = NWr / 4;          // at most 8 (NW <= 32)
+      const rsrc_t r_p = make_rsrc(a.gs_part + (size_t)((t & 1) * a.G + g) * BG * NWr * H, (size_t)BG * NWr * H * 4);
+      for (int it = threadIdx.x; it < nlive * 16; it += 256) {
+        const int ci = it >> 4, qg = (it >> 2) & 3, q4 = it & 3;
+        const uint32_t base = (uint32_t)((((size_t)ci * NWr + qg * WPG) * H + w * 16 + 4 * q4) * 4);
+        uint4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = ld_coh_b128(r_p, k < WPG ? base + (uint32_t)(k * H * 4) : kOOB);
+        float4 sum = float4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float4 f = __builtin_bit_cast(float4, v[k]);
+          sum.x += f.x; sum.y += f.y; sum.z += f.z; sum.w += f.w;
+        }
+        red[qg][ci][4 * q4] = sum.x;
+        red[qg][ci][4 * q4 + 1] = sum.y;
+        red[qg][ci][4 * q4 + 2] = sum.z;
+        red[qg][ci][4 * q4 + 3] = sum.w;
+      }
+    } else if (kDirectOk && direct) {
      if constexpr (kDirectOk) {
       // Each wave copies its own H gate columns of the compacted rows straight into its LDS
       // slice (buffer LDS DMA, 1 KB row segments, segment-major: segment s of the tile's rows
@@ -459,7 +594,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       }
      }
     } else
-    for (int jt = 0; jt < NT; ++jt) {
+    for (int jt = 0; jt < NT && !GS; ++jt) {
       if (jt * 16 >= nlive) break;
       const int ci = jt * 16 + l16;
       const bool lv = ci < nlive;
@@ -621,11 +756,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   }
 }
 
-template <int P, int NT, int KS>
-static hipError_t launch_bwd_t(const RecArgs& a, dim3 grid, hipStream_t st, int* occ_out) {
+template <int P, int NT, int KS, bool GS>
+static hipError_t launch_bwd_k(const RecArgs& a, dim3 grid, hipStream_t st, int* occ_out) {
   constexpr int OCC = rec_occ(P, KS);
-  auto kern = k_bwd<P, NT, KS, OCC>;
-  const size_t shm = a.bwd_direct ? rec_bwd_lds_bytes(P, KS) : 0;
+  auto kern = k_bwd<P, NT, KS, OCC, GS>;
+  const size_t shm = (!GS && a.bwd_direct) ? rec_bwd_lds_bytes(P, KS) : 0;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
   if (e != hipSuccess) return e;
   int occ = 0;
@@ -636,6 +771,16 @@ static hipError_t launch_bwd_t(const RecArgs& a, dim3 grid, hipStream_t st, int*
   RecArgs args = a;
   void* kargs[] = {&args};
   return hipLaunchCooperativeKernel((const void*)kern, grid, dim3(256), kargs, (unsigned)shm, st);
+}
+
+template <int P, int NT, int KS>
+static hipError_t launch_bwd_t(const RecArgs& a, dim3 grid, hipStream_t st, int* occ_out) {
+  if constexpr (rec_bwd_gs_built(P, NT, KS)) {
+    if (a.bwd_gs) return launch_bwd_k<P, NT, KS, true>(a, grid, st, occ_out);
+  } else {
+    if (a.bwd_gs) return hipErrorInvalidValue;
+  }
+  return launch_bwd_k<P, NT, KS, false>(a, grid, st, occ_out);
 }
 
 hipError_t launch_bwd(const RecArgs& a, int prec, int NT, int KS, dim3 grid, hipStream_t st, int* occ_out) {

@@ -44,7 +44,7 @@ SLSTM_PHASE_EVENTS = 10
 class slstm_plan(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "groups", "wg_per_group", "rows_per_group", "k_chunks", "fwd_kernel", "fwd_tiles", "k_chunk_cap",
-        "occupancy", "bwd_groups", "bwd_tiles", "bwd_direct", "fused_x")]
+        "occupancy", "bwd_groups", "bwd_tiles", "bwd_direct", "fused_x", "bwd_split")]
 
 
 _lib = None

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 GRID_H = {0: [1, 40, 64, 100, 128, 200, 252, 256, 300, 508, 512],
           1: [1, 64, 100, 128, 200, 256, 300, 504, 512, 520, 1020, 1024]}
 GRID_B = [1, 17, 64, 100, 128, 129, 200, 256, 257, 300, 384, 400, 512, 513, 600, 700, 768, 769, 900, 1000, 1024]
-KEYS = ("fwd_kernel", "fwd_tiles", "k_chunk_cap", "occupancy", "bwd_tiles", "bwd_direct", "fused_x")
+KEYS = ("fwd_kernel", "fwd_tiles", "k_chunk_cap", "occupancy", "bwd_tiles", "bwd_direct", "fused_x", "bwd_split")
 
 
 def reachable_variants():
