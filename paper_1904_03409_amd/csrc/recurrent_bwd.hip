@@ -185,10 +185,22 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // the cell operands (gates, c, c_prev) are read for push steps only
   auto ld_ops = [&](int t, int b, int op, int sp, float& gh_, float& gc_, float4& act, float& c, float& cp) {
     const size_t o = ((size_t)t * B + b) * H + ul;
-    gh_ = a.dh_top[o];
-    gc_ = a.dc_top ? a.dc_top[o] : 0.f;
+    // (GS: the operands read once and the dA rows kept for the post-loop GEMMs go through
+    // non-temporal accesses, which leaves more of the XCC's L2 to the partial sums that
+    // every step rewrites: large fp32 1.41 -> 1.375 ms, 0.88 -> 0.69 GB written per launch)
+    if constexpr (GS) {
+      gh_ = __builtin_nontemporal_load(a.dh_top + o);
+      gc_ = a.dc_top ? __builtin_nontemporal_load(a.dc_top + o) : 0.f;
+    } else {
+      gh_ = a.dh_top[o];
+      gc_ = a.dc_top ? a.dc_top[o] : 0.f;
+    }
     if (op == 1) {
-      act = *(const float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * ul);
+      if constexpr (GS) {
+        const f32x4 v = __builtin_nontemporal_load((const f32x4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * ul));
+        act = float4{v[0], v[1], v[2], v[3]};
+      }
+      else act = *(const float4*)(a.stash + ((size_t)t * B + b) * H4 + 4 * ul);
       c = a.ccell[o];
       cp = (sp < 0) ? a.c0[(size_t)b * H + ul] : a.ccell[((size_t)sp * B + b) * H + ul];
     }
@@ -336,7 +348,8 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       if (pok[i] && c_op[i] == 1) {               // only push rows are read (exchange, post-loop GEMMs)
         const size_t ao = ((size_t)t * B + b) * H4 + 4 * u;
         if constexpr (PREC == 0) {
-          *(float4*)((float*)a.dA + ao) = dA4;
+          if constexpr (GS) __builtin_nontemporal_store(f32x4{dA4.x, dA4.y, dA4.z, dA4.w}, (f32x4*)((float*)a.dA + ao));
+          else *(float4*)((float*)a.dA + ao) = dA4;
         } else {
           bf16_t q[4] = {f32_to_bf16_bits(dA4.x), f32_to_bf16_bits(dA4.y), f32_to_bf16_bits(dA4.z),
                          f32_to_bf16_bits(dA4.w)};
