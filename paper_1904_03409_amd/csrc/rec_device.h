@@ -59,6 +59,7 @@ __device__ __forceinline__ float fwd_cell(const RecArgs& a, const f32x4& acc, co
   a.hcell[o] = h;
   a.ccell[o] = c;
   if constexpr (PREC == 1) a.hx[o + (size_t)a.B * a.H] = f32_to_bf16_bits(h);
-  if (keep) *(float4*)(a.stash + ((size_t)t * a.B + b) * (4 * a.H) + 4 * u) = float4{gi, gf, gg, go};
+  // (the gate stash is read only by the backward: a non-temporal store)
+  if (keep) __builtin_nontemporal_store(f32x4{gi, gf, gg, go}, (f32x4*)(a.stash + ((size_t)t * a.B + b) * (4 * a.H) + 4 * u));
   return c;
 }

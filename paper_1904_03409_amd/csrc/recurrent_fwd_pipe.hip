@@ -137,7 +137,9 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   }
   auto xw_at = [&](int t, int ti) -> float4 {
     const int b = lok[ti] ? lrow[ti] : 0, uu = lok[ti] ? u : 0;
-    return *(const float4*)(a.xw + ((size_t)t * B + b) * H4 + 4 * uu);
+    // read once: non-temporal, so the stream does not push the exchanged rows out of L2
+    const f32x4 v = __builtin_nontemporal_load((const f32x4*)(a.xw + ((size_t)t * B + b) * H4 + 4 * uu));
+    return float4{v[0], v[1], v[2], v[3]};
   };
   auto top_at = [&](int t, int ti) -> int {
     const int b = lrow[ti] < B ? lrow[ti] : 0;
