@@ -37,13 +37,15 @@ template <int P, bool KMAJOR> struct Geo {
 };
 
 // Register staging of one operand tile: NV vectors of VE elements per thread. With F32SRC
-// (bf16 kernels only) the array holds fp32 values, rounded to bf16 (nearest even) as they are
-// loaded.
+// (bf16 kernels only) the stage holds the fp32 values as loaded (f32v) and rounds them to bf16
+// (nearest even) when it writes them to LDS, after the slice in between has been multiplied:
+// rounding them at load time made every fetch wait for its own loads.
 template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
   using T = typename Cfg<P>::T;
   static constexpr int BK = Cfg<P>::BK, VE = Cfg<P>::VE;
   static constexpr int NV = 128 * BK / VE / 256;
   uint4 v[NV];
+  uint4 f32v[F32SRC ? NV : 1][2];
   int prow[NV];   // array row of each of this thread's vectors in the slice loaded next
 
   // Array row of tile row gr: the gather table's entry, or gr itself. Tiles stored [m/n][k]
@@ -78,24 +80,20 @@ template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
         const int r = e / (BK / VE), c = (e % (BK / VE)) * VE;
         const int gr = r0 + r, gc = c0 + c;
         const int pr = prow[i];
-        bf16_t q[VE];
         if (vec) {
-          float f[8];
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
             const bool ok = gr < rlim && gc + 4 * hh < clim;
             const uint32_t off = ok ? (uint32_t)(((size_t)pr * ld + gc + 4 * hh) * 4) : 0xffffffffu;
-            const float4 v4 = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-            f[4 * hh] = v4.x; f[4 * hh + 1] = v4.y; f[4 * hh + 2] = v4.z; f[4 * hh + 3] = v4.w;
+            f32v[i][hh] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
           }
-#pragma unroll
-          for (int j = 0; j < VE; ++j) q[j] = f32_to_bf16_bits(f[j]);
         } else {
+          float f[8];
 #pragma unroll
-          for (int j = 0; j < VE; ++j)
-            q[j] = (gr < rlim && gc + j < clim) ? f32_to_bf16_bits(fb[(size_t)pr * ld + gc + j]) : (bf16_t)0;
+          for (int j = 0; j < VE; ++j) f[j] = (gr < rlim && gc + j < clim) ? fb[(size_t)pr * ld + gc + j] : 0.f;
+          f32v[i][0] = __builtin_bit_cast(uint4, float4{f[0], f[1], f[2], f[3]});
+          f32v[i][1] = __builtin_bit_cast(uint4, float4{f[4], f[5], f[6], f[7]});
         }
-        v[i] = *(const uint4*)q;
       }
       return;
     }
@@ -131,8 +129,18 @@ template <int P, bool KMAJOR, bool F32SRC = false> struct Stage {
     }
   }
 
-  __device__ __forceinline__ void store(T* __restrict__ s) const {
+  __device__ __forceinline__ void store(T* __restrict__ s) {
     using G = Geo<P, KMAJOR>;
+    if constexpr (F32SRC) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const float4 lo = __builtin_bit_cast(float4, f32v[i][0]), hi = __builtin_bit_cast(float4, f32v[i][1]);
+        const bf16_t q[8] = {f32_to_bf16_bits(lo.x), f32_to_bf16_bits(lo.y), f32_to_bf16_bits(lo.z),
+                             f32_to_bf16_bits(lo.w), f32_to_bf16_bits(hi.x), f32_to_bf16_bits(hi.y),
+                             f32_to_bf16_bits(hi.z), f32_to_bf16_bits(hi.w)};
+        v[i] = *(const uint4*)q;
+      }
+    }
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int e = threadIdx.x + 256 * i;
