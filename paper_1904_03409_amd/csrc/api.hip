@@ -106,9 +106,12 @@ int ks_bucket(int prec, int ks_eff) {
   return ks <= 32 ? ks : -1;
 }
 
+// Split-K slices of dW / dU: about 512 blocks, one round of the GEMM's two workgroups per CU
+// on 256 CUs (measured at large: 1024 blocks 0.26 / 0.37 ms fp32 dW + db / dU, 512 blocks
+// 0.24 / 0.36 ms, 384 or 256 blocks slower; bf16 0.13 / 0.09 -> 0.12 / 0.07 ms)
 int splits_for(int M, int N, int K) {
   int tiles = ((M + kGemmBM - 1) / kGemmBM) * ((N + kGemmBN - 1) / kGemmBN);
-  int s = std::max(1, 1024 / std::max(1, tiles));
+  int s = std::max(1, 512 / std::max(1, tiles));
   int max_s = std::max(1, (K + kGemmBK - 1) / kGemmBK);
   return std::min(std::min(s, 64), max_s);
 }
