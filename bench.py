@@ -228,7 +228,8 @@ def cpu_baseline(wl, gpu_out=None, target_s=12.0):
     oracle.run(wl, sel=np.arange(n0, dtype=np.int32), mode="f32", threads=th, native=True)
     dt0 = time.perf_counter() - t0
     # sample size for about target_s of CPU work (at most the whole batch), then runs of it
-    # until about target_s have been spent (at most 9); the median run is reported
+    # until about target_s have been spent (small workloads repeat many times); the median
+    # run is reported
     n = n0 if dt0 >= target_s / 4 else int(min(wl.B, max(n0, n0 * target_s / max(dt0, 1e-3))))
     times = []
     ref = None
@@ -236,7 +237,7 @@ def cpu_baseline(wl, gpu_out=None, target_s=12.0):
         t0 = time.perf_counter()
         ref = oracle.run(wl, sel=np.arange(n, dtype=np.int32), mode="f32", threads=th, native=True)
         times.append(time.perf_counter() - t0)
-        if len(times) >= 9 or sum(times) + float(np.median(times)) > target_s:
+        if len(times) >= 10000 or sum(times) + float(np.median(times)) > target_s:
             break
     dt = float(np.median(times))
     pushes = int((wl.ops[:, :n] == 1).sum())
