@@ -578,12 +578,6 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   int32_t* prow = (int32_t*)(ws + L.prow);
   const uint32_t* npush = ctl + CTL_NPUSH;
   hipLaunchKernelGGL(k_push_rows, dim3(1), dim3(1024), 0, st, ops, T * B, prow, ctl + CTL_NPUSH);
-  // dA rows start as "not yet produced" (all-one bits): the workgroups read them from each other
-  if (a.poll) {
-    const size_t da_bytes = (size_t)T * B * 4 * H * (bf ? 2 : 4);
-    hipLaunchKernelGGL(k_fill_pattern, dim3(grid1d(da_bytes / 16 + 1)), dim3(256), 0, st, (unsigned char*)a.dA,
-                       da_bytes, 0xffffffffu);
-  }
   mark(d, 5, st);
   if ((rc = hip_status(launch_bwd(a, p.prec, p.NTb, p.KS, dim3(8 * p.per_xcc_b), st, nullptr)))) return rc;
   mark(d, 6, st);

@@ -19,8 +19,8 @@
 //
 // Same work split as the forward: group of 16*NT rows on one XCC, workgroup w owns
 // hidden units [16w, 16w+16). dA U^T needs all 4H gate columns, so dA is exchanged
-// through L2: with a group barrier per step, or without one (dA starts filled with all-one
-// bits, and a reader fetches again every granule that still holds them). Wave q contracts
+// through L2, with a group barrier per step (each workgroup stores its push rows' dA, arrives,
+// waits for the others, then reads every push row of the group). Wave q contracts
 // gate columns [qH, (q+1)H) against its register-resident slice of U and the four partial
 // sums are added in LDS in a fixed order. Every gradient element is owned by one thread,
 // so there are no atomics. Workgroup barriers that only order LDS accesses do not wait for
@@ -43,6 +43,20 @@
 namespace {
 // Workgroup barrier for LDS data only: it does not wait for global loads or stores.
 __device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// Eight floats rounded to bf16 (nearest-even) in pairs, packed as they are converted.
+__device__ __forceinline__ bf16x8 pack_bf16x8(const float (&v)[8]) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 w;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    w[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{v[2 * j], v[2 * j + 1]}, bf16x2));
+  // (an empty asm on the packed words keeps the compiler from sinking the conversions to the
+  // first use, which would keep all the fp32 values live through the set-up)
+  asm volatile("" : "+v"(w));
+  return __builtin_bit_cast(bf16x8, w);
+}
 }  // namespace
 
 template <int PREC, int NT, int KS, int OCC, bool GS>
@@ -51,10 +65,14 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   constexpr int BG = NT * 16;
   constexpr int PAIRS = BG * 16 / 256;            // (row, unit) pairs per thread
   // Two workgroups per CU (bf16, H = 1024) leave 256 registers per lane, half of them for
-  // the U slice: the lean variant keeps only the current step's row info per pair and
-  // loads each step's operands at the step (in batches of LB pairs) instead of a step ahead.
+  // the U slice. The lean variant keeps per pair only the top state's gradient in registers;
+  // the row state (op and producer of the step, depth), the same for the 16 threads of a
+  // row, sits in LDS; each step's operands, and the spill slot a push reads, are loaded at the
+  // step (in batches of LB pairs), after every earlier store of the same thread, so the
+  // slot's last spill needs no forwarding.
   constexpr bool LEAN = OCC == 2;
-  constexpr int LB = PAIRS < 8 ? PAIRS : 8;
+  static_assert(BG <= 256, "one row-info thread per row");
+  constexpr int LB = PAIRS < 4 ? PAIRS : 4;
   static_assert(PAIRS % LB == 0, "whole load batches");
   // staged dA rows (direct path): per wave 16 compacted rows of its H gate columns
   constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
@@ -64,6 +82,8 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   __shared__ float s_db[16][16][4];
   __shared__ int s_g, s_w;
   __shared__ int s_abort;                          // a wait for dA rows gave up
+  // lean variant: op and producer of each row by step parity, depth of each row
+  __shared__ int s_rop[LEAN ? 2 : 1][LEAN ? BG : 1], s_rsp[LEAN ? 2 : 1][LEAN ? BG : 1], s_rdep[LEAN ? BG : 1];
   // GS: this workgroup's dA rows (its 64 gate columns, by row of the group), fp32 or bf16
   constexpr int SDL = PREC ? 72 : 68;                 // row stride (elements): 16-byte pad
   using sd_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
@@ -101,9 +121,10 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         for (int j = 0; j < 4; ++j)
           ureg32[e][j] = unit < H ? Ur[perm_to_orig(w * 64 + ch * 16 + 4 * lq + j, H)] : 0.f;
       } else {
+        float v[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          ureg16[e][j] = f32_to_bf16(unit < H ? Ur[perm_to_orig(w * 64 + ch * 32 + 8 * lq + j, H)] : 0.f);
+        for (int j = 0; j < 8; ++j) v[j] = unit < H ? Ur[perm_to_orig(w * 64 + ch * 32 + 8 * lq + j, H)] : 0.f;
+        ureg16[e] = pack_bf16x8(v);
       }
     }
   }
@@ -116,11 +137,13 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         ureg32[c][j] = (a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f;
       }
     } else {
+      float v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         int kk = c * 32 + 8 * lq + j;
-        ureg16[c][j] = f32_to_bf16((a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f);
+        v[j] = (a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f;
       }
+      ureg16[c] = pack_bf16x8(v);
     }
   }
 
@@ -137,12 +160,13 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   }
   // depth after the last step, per pair; the spill slots S[0 .. depth) of the states that
   // stay on the stack to the end start at 0
-  int dep[PAIRS];
+  int dep[LEAN ? 1 : PAIRS];
 #pragma unroll
   for (int i = 0; i < PAIRS; ++i) {
     const int b = pok[i] ? row0 + prow[i] : 0;
-    dep[i] = pok[i] ? min(max(a.depth_end[b], 0), T) : 0;
-    for (int d = 0; d < dep[i]; ++d) {
+    const int d0 = pok[i] ? min(max(a.depth_end[b], 0), T) : 0;
+    if constexpr (!LEAN) dep[i] = d0;
+    for (int d = 0; d < d0; ++d) {
       const size_t o = ((size_t)d * B + b) * H + u;
       a.dh_acc[o] = 0.f;
       a.dc_acc[o] = 0.f;
@@ -169,21 +193,22 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // a producer table that is not the forward's is reported (no access outside [-1, t))
     sp = checked_src(sp, t - 1, a.ctl);
   };
-  int c_op[PAIRS], c_sp[PAIRS];                          // step t row info
-  int n_op[PAIRS], n_sp[PAIRS], nn_op[PAIRS], nn_sp[PAIRS];
-  float c_gh[PAIRS], c_gc[PAIRS], c_c[PAIRS], c_cp[PAIRS];
+  constexpr int PR = LEAN ? 1 : PAIRS;                   // pairs with row info in registers
+  int c_op[PR], c_sp[PR];                                // step t row info
+  int n_op[PR], n_sp[PR], nn_op[PR], nn_sp[PR];
+  float c_gh[PR], c_gc[PR], c_c[PR], c_cp[PR];
   float4 c_act[PAIRS];
-  float n_gh[PAIRS], n_gc[PAIRS], n_c[PAIRS], n_cp[PAIRS];
+  float n_gh[PR], n_gc[PR], n_c[PR], n_cp[PR];
   float4 n_act[PAIRS];
   // gradient of the top state; last spill (value and depth); spill slot prefetched for a push
-  float gh[PAIRS], gc[PAIRS], lh[PAIRS], lc[PAIRS], ph[PAIRS], pc[PAIRS];
-  int ld[PAIRS];
+  float gh[PAIRS], gc[PAIRS], lh[PR], lc[PR], ph[PR], pc[PR];
+  int ld[PR];
   auto ld_row = [&](int t, int b, int& op, int& sp) {
     op = a.ops[(size_t)t * B + b];
     sp = (t == 0) ? -1 : a.top[(size_t)(t - 1) * B + b];
   };
   // the cell operands (gates, c, c_prev) are read for push steps only
-  auto ld_ops = [&](int t, int b, int op, int sp, float& gh_, float& gc_, float4& act, float& c, float& cp) {
+  auto ld_ops = [&](int t, int b, int ul, int op, int sp, float& gh_, float& gc_, float4& act, float& c, float& cp) {
     const size_t o = ((size_t)t * B + b) * H + ul;
     // (GS: the operands read once and the dA rows kept for the post-loop GEMMs go through
     // non-temporal accesses, which leaves more of the XCC's L2 to the partial sums that
@@ -208,55 +233,86 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // operands of step t-1 and row info of step t-2; the spill slot a push at step t-1 reads
   // (depth dep-1 after this step's update)
   auto prefetch = [&](int t) {
-    if constexpr (LEAN) return;
+    if constexpr (!LEAN) {
 #pragma unroll
-    for (int i = 0; i < PAIRS; ++i) {
-      const int b = pok[i] ? row0 + prow[i] : 0;
-      if (t > 0) {
-        ld_ops(t - 1, b, n_op[i], n_sp[i], n_gh[i], n_gc[i], n_act[i], n_c[i], n_cp[i]);
-        const size_t so = ((size_t)max(dep[i] - 1, 0) * B + b) * H + ul;
-        ph[i] = a.dh_acc[so];
-        pc[i] = a.dc_acc[so];
+      for (int i = 0; i < PAIRS; ++i) {
+        const int b = pok[i] ? row0 + prow[i] : 0;
+        if (t > 0) {
+          ld_ops(t - 1, b, ul, n_op[i], n_sp[i], n_gh[i], n_gc[i], n_act[i], n_c[i], n_cp[i]);
+          const size_t so = ((size_t)max(dep[i] - 1, 0) * B + b) * H + ul;
+          ph[i] = a.dh_acc[so];
+          pc[i] = a.dc_acc[so];
+        }
+        if (t > 1) ld_row(t - 2, b, nn_op[i], nn_sp[i]);   // validated at the rotation
       }
-      if (t > 1) ld_row(t - 2, b, nn_op[i], nn_sp[i]);   // validated at the rotation
     }
   };
 #pragma unroll
   for (int i = 0; i < PAIRS; ++i) {
-    const int b = pok[i] ? row0 + prow[i] : 0;
-    ld_row(T - 1, b, c_op[i], c_sp[i]);
-    valid_sp(T - 1, c_sp[i]);
+    gh[i] = gc[i] = 0.f;
     if constexpr (!LEAN) {
-      ld_ops(T - 1, b, c_op[i], c_sp[i], c_gh[i], c_gc[i], c_act[i], c_c[i], c_cp[i]);
+      const int b = pok[i] ? row0 + prow[i] : 0;
+      ld_row(T - 1, b, c_op[i], c_sp[i]);
+      valid_sp(T - 1, c_sp[i]);
+      ld_ops(T - 1, b, ul, c_op[i], c_sp[i], c_gh[i], c_gc[i], c_act[i], c_c[i], c_cp[i]);
       if (T > 1) {
         ld_row(T - 2, b, n_op[i], n_sp[i]);
         valid_sp(T - 2, n_sp[i]);
       }
+      lh[i] = lc[i] = 0.f;
+      ld[i] = -1;
+      // spill slot for a push at step T-1 (the parent sits at depth dep-1): stays-on-stack, 0
+      ph[i] = pc[i] = 0.f;
     }
-    gh[i] = gc[i] = lh[i] = lc[i] = 0.f;
-    ld[i] = -1;
-    // spill slot for a push at step T-1 (the parent sits at depth dep-1): stays-on-stack, 0
-    ph[i] = pc[i] = 0.f;
+  }
+  // lean variant: thread r < BG keeps row r's info of the next step in registers and writes
+  // the LDS row state; rows outside the batch hold at depth 0 (no op, nothing stored)
+  const int rr = threadIdx.x;
+  const bool rr_ok = LEAN && rr < BG && row0 + rr < B;
+  int r_nop = 0, r_nsp = -1;
+  if constexpr (LEAN) {
+    if (rr < BG) {
+      int op = 0, sp = -1;
+      if (rr_ok) {
+        ld_row(T - 1, row0 + rr, op, sp);
+        valid_sp(T - 1, sp);
+        if (T > 1) ld_row(T - 2, row0 + rr, r_nop, r_nsp);
+      }
+      s_rop[(T - 1) & 1][rr] = op;
+      s_rsp[(T - 1) & 1][rr] = sp;
+      s_rdep[rr] = rr_ok ? min(max(a.depth_end[row0 + rr], 0), T) : 0;
+    }
+    __syncthreads();
   }
 
   long long* clk = a.clk ? a.clk + (size_t)blockIdx.x * T * 4 : nullptr;
   for (int t = T - 1; t >= 0; --t) {
     if (clk && threadIdx.x == 0) clk[t * 4 + 0] = wall_clock64();
+    // lean variant: the pairs' rows and unit come from a copy of the thread index that the
+    // compiler cannot see through, so their address terms are recomputed at each step rather
+    // than held in registers (spilled) through the loop
+    int tq = threadIdx.x;
+    if constexpr (LEAN) asm volatile("" : "+v"(tq));
+    const int uq = LEAN ? w * 16 + (tq & 15) : u;
+    const int ulq = uq < H ? uq : 0;
+    auto prw = [&](int i) { return LEAN ? (tq >> 4) + 16 * i : prow[i]; };
+    auto pk = [&](int i) { return LEAN ? (row0 + (tq >> 4) + 16 * i < B) && (uq < H) : pok[i]; };
     // row tables of step t for the compaction (from the registers of the unit-0 threads)
-    if (uu == 0) {
+    if (uu == 0 && !LEAN) {
 #pragma unroll
-      for (int i = 0; i < PAIRS; ++i) {
+      for (int i = 0; i < PR; ++i) {
         s_op[prow[i]] = pok[i] ? c_op[i] : 0;
       }
     }
     lds_sync();
+    const int* const op_now = LEAN ? s_rop[t & 1] : s_op;
     if (wave == 0) {
       // list the push rows in row order (wave-wide ballot + prefix count)
       int base = 0;
 #pragma unroll
       for (int r0 = 0; r0 < BG; r0 += 64) {
         const int r = r0 + lane;
-        const bool live = (r < BG) && (s_op[r] == 1);
+        const bool live = (r < BG) && (op_now[r] == 1);
         const unsigned long long m = __ballot(live);
         const int ci = base + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
         if (live) { s_cidx[r] = ci; s_crow[ci] = r; }
@@ -266,87 +322,112 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     }
 
     // ---- cell backward for this workgroup's (row, unit) pairs
-    // lean variant: the operands of LB pairs (and the spill slot a push reads) are loaded
-    // together, then used
+    // lean variant: the row state and operands of LB pairs (and the spill slot a push reads)
+    // are loaded together, then used
     float e_gh[LEAN ? LB : 1], e_gc[LEAN ? LB : 1], e_c[LEAN ? LB : 1], e_cp[LEAN ? LB : 1];
     float e_ph[LEAN ? LB : 1], e_pc[LEAN ? LB : 1];
     float4 e_act[LEAN ? LB : 1];
+    int e_op[LEAN ? LB : 1], e_dep[LEAN ? LB : 1];
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
       if constexpr (LEAN) {
         if (i % LB == 0) {
 #pragma unroll
           for (int j = 0; j < LB; ++j) {
-            const int ii = i + j;
-            const int bl = pok[ii] ? row0 + prow[ii] : 0;
-            ld_ops(t, bl, c_op[ii], c_sp[ii], e_gh[j], e_gc[j], e_act[j], e_c[j], e_cp[j]);
-            const size_t so = ((size_t)max(dep[ii] - 1, 0) * B + bl) * H + ul;
+            const int r = prw(i + j);
+            const int bl = pk(i + j) ? row0 + r : 0;
+            e_op[j] = s_rop[t & 1][r];
+            e_dep[j] = s_rdep[r];
+            ld_ops(t, bl, ulq, e_op[j], s_rsp[t & 1][r], e_gh[j], e_gc[j], e_act[j], e_c[j], e_cp[j]);
+            const size_t so = ((size_t)max(e_dep[j] - 1, 0) * B + bl) * H + ulq;
             e_ph[j] = a.dh_acc[so];
             e_pc[j] = a.dc_acc[so];
           }
         }
       }
-      const int j = LEAN ? i % LB : 0;
-      const float o_gh = LEAN ? e_gh[j] : c_gh[i], o_gc = LEAN ? e_gc[j] : c_gc[i];
-      const float o_c = LEAN ? e_c[j] : c_c[i], o_cp = LEAN ? e_cp[j] : c_cp[i];
-      const float4 o_act = LEAN ? e_act[j] : c_act[i];
+      int op_i, dp;
+      float o_gh, o_gc, o_c, o_cp, sh, sc;
+      float4 o_act;
+      if constexpr (LEAN) {
+        const int j = i % LB;
+        op_i = e_op[j]; dp = e_dep[j];
+        o_gh = e_gh[j]; o_gc = e_gc[j]; o_c = e_c[j]; o_cp = e_cp[j]; o_act = e_act[j];
+        sh = e_ph[j]; sc = e_pc[j];
+      } else {
+        op_i = c_op[i]; dp = dep[i];
+        o_gh = c_gh[i]; o_gc = c_gc[i]; o_c = c_c[i]; o_cp = c_cp[i]; o_act = c_act[i];
+        sh = ph[i]; sc = pc[i];
+      }
       float4 dA4 = float4{0.f, 0.f, 0.f, 0.f};
-      const int b = row0 + prow[i];
+      const int b = row0 + prw(i);
+      const bool okp = pk(i);
       // dh_top[t], dc_top[t] belong to the state at the top after step t
       gh[i] += o_gh;
       gc[i] += o_gc;
-      if (c_op[i] == 1) {
+      if (op_i == 1) {
         // the state produced at step t: its whole gradient is (gh, gc)
         const float4 act = o_act;
         const float dh = gh[i];
         const float tc = tanhf_(o_c);
         const float dc = gc[i] + dh * act.w * (1.f - tc * tc);
-        // never the all-ones fill pattern: a NaN is stored as the canonical quiet NaN
-        dA4.x = canon_nan(dc * act.z * act.x * (1.f - act.x));
-        dA4.y = canon_nan(dc * o_cp * act.y * (1.f - act.y));
-        dA4.z = canon_nan(dc * act.x * (1.f - act.z * act.z));
-        dA4.w = canon_nan(dh * tc * act.w * (1.f - act.w));
-        if (pok[i]) { dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w; }
-        // the parent (depth dep-1) comes back to the top with its spilled gradient (the last
-        // spill if it was to that depth, else the prefetched slot) plus dc f; dA U^T follows
-        const bool fwd = ld[i] == dep[i] - 1;
-        const float sh = LEAN ? e_ph[j] : ph[i], sc = LEAN ? e_pc[j] : pc[i];
-        gh[i] = fwd ? lh[i] : sh;
-        gc[i] = (fwd ? lc[i] : sc) + dc * act.y;
-        dep[i] -= 1;
-      } else if (c_op[i] == -1) {
+        dA4.x = dc * act.z * act.x * (1.f - act.x);
+        dA4.y = dc * o_cp * act.y * (1.f - act.y);
+        dA4.z = dc * act.x * (1.f - act.z * act.z);
+        dA4.w = dh * tc * act.w * (1.f - act.w);
+        if (okp) { dbacc[0] += dA4.x; dbacc[1] += dA4.y; dbacc[2] += dA4.z; dbacc[3] += dA4.w; }
+        // the parent (depth dep-1) comes back to the top with its spilled gradient plus dc f;
+        // dA U^T follows. (Register variants: the last spill if it was to that depth, else
+        // the slot prefetched before that spill's store.)
+        if constexpr (LEAN) {
+          gh[i] = sh;
+          gc[i] = sc + dc * act.y;
+        } else {
+          const bool fwd = ld[i] == dp - 1;
+          gh[i] = fwd ? lh[i] : sh;
+          gc[i] = (fwd ? lc[i] : sc) + dc * act.y;
+        }
+        dp -= 1;
+      } else if (op_i == -1) {
         // the popped state comes back: the state below is spilled, the popped one starts at 0.
         // The depth stays in [0, T] for the forward's ops; ops that are not the forward's are
         // reported, with no store outside the spill slots. (Pairs outside the batch or the
-        // units follow row 0's ops from depth 0 and store nothing.)
-        if (pok[i] && (dep[i] < 0 || dep[i] > T)) {
-          raise_badidx(a.ctl);
-          dep[i] = 0;
+        // units store nothing.)
+        if (dp < 0 || dp > T) {
+          if (okp) raise_badidx(a.ctl);
+          dp = 0;
         }
-        if (pok[i]) {
-          const size_t o = ((size_t)dep[i] * B + b) * H + u;
+        if (okp) {
+          const size_t o = ((size_t)dp * B + b) * H + uq;
           a.dh_acc[o] = gh[i];
           a.dc_acc[o] = gc[i];
         }
-        lh[i] = gh[i];
-        lc[i] = gc[i];
-        ld[i] = dep[i];
+        if constexpr (!LEAN) {
+          lh[i] = gh[i];
+          lc[i] = gc[i];
+          ld[i] = dp;
+        }
         gh[i] = gc[i] = 0.f;
-        dep[i] += 1;
+        dp += 1;
+      }
+      // (lean: every thread of the row computed the same depth; one of them keeps it)
+      if constexpr (LEAN) {
+        if (uu == 0 && op_i != 0) s_rdep[prw(i)] = dp;
+      } else {
+        dep[i] = dp;
       }
       if constexpr (GS) {
         // the contraction's operand: this row's dA of the thread's unit (rows the list does
         // not name are never read)
         if constexpr (PREC == 0) {
-          *(float4*)&s_dA[prow[i]][4 * uu] = dA4;
+          *(float4*)&s_dA[prw(i)][4 * uu] = dA4;
         } else {
           bf16_t q[4] = {f32_to_bf16_bits(dA4.x), f32_to_bf16_bits(dA4.y), f32_to_bf16_bits(dA4.z),
                          f32_to_bf16_bits(dA4.w)};
-          *(uint2*)&s_dA[prow[i]][4 * uu] = *(const uint2*)q;
+          *(uint2*)&s_dA[prw(i)][4 * uu] = *(const uint2*)q;
         }
       }
-      if (pok[i] && c_op[i] == 1) {               // only push rows are read (exchange, post-loop GEMMs)
-        const size_t ao = ((size_t)t * B + b) * H4 + 4 * u;
+      if (okp && op_i == 1) {                   // only push rows are read (exchange, post-loop GEMMs)
+        const size_t ao = ((size_t)t * B + b) * H4 + 4 * uq;
         if constexpr (PREC == 0) {
           if constexpr (GS) __builtin_nontemporal_store(f32x4{dA4.x, dA4.y, dA4.z, dA4.w}, (f32x4*)((float*)a.dA + ao));
           else *(float4*)((float*)a.dA + ao) = dA4;
@@ -433,9 +514,6 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       group_arrive(&a.ctl[CTL_BAR_B + g * 16]);
       prefetch(t);
       if (group_wait(&a.ctl[CTL_BAR_B + g * 16], (uint32_t)(a.NW * (T - t)), a.ctl, a.spin_limit, &s_abort)) break;
-    } else if (a.poll) {
-      lds_sync();
-      if (direct) row_offsets0();
     } else {
       group_arrive(&a.ctl[CTL_BAR_B + g * 16]);
       if (direct) row_offsets0();
@@ -447,7 +525,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // chunks ahead, through the bounds-checked descriptor (a lane past the list or k past H
     // gets an out-of-range offset: value 0, no memory access). Two accumulators per tile
     // keep two independent MFMA chains.
-    constexpr int CG = LEAN ? 2 : 8;                // lean: measured fastest (fewer spills)
+    constexpr int CG = LEAN ? 4 : 8;                // lean: measured fastest (fewer spills)
     constexpr int NG = (KS + CG - 1) / CG;
     const int nlive = s_nlive;
     if (!GS && (!direct || nlive == 0)) prefetch(t);
@@ -512,43 +590,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
               bdma16(r_dA, lane * 16u, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
             }
           }
-        // granules (16 bytes of one lane) whose producer's store had not arrived when they were
-        // copied are fetched again, bypassing L1, until complete
-        auto settle = [&](int sj) {
-          uint32_t bad = 0;
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (r < nrows && pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
-              bad |= 1u << r;
-          int spins = 0;
-          while (__builtin_amdgcn_ballot_w64(bad != 0u)) {
-            if (spin_out(spins, a.ctl, a.spin_limit)) {
-              s_abort = 1;
-              break;
-            }
-            // a row segment with a pending granule is copied again whole: a lane given an
-            // out-of-range offset would write zeros over its LDS bytes, and the granules that
-            // had arrived read back the same values
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const uint32_t soff = (uint32_t)__builtin_amdgcn_readlane((int)soffv, r) + sj * 1024;
-              if (__builtin_amdgcn_ballot_w64((bad >> r) & 1u))
-                bdma16_sc1(r_dA, lane * 16u, soff, lds0 + (uint32_t)((r * QLD + sj * (1024 / ESZ)) * ESZ));
-            }
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-              if (((bad >> r) & 1u) &&
-                  !pending_granule<PREC>(*(const uint4*)(wbuf + r * QLD + sj * (1024 / ESZ) + lane * (16 / ESZ))))
-                bad &= ~(1u << r);
-          }
-        };
         // segment sj is in LDS once at most nrows * (SEGQ - 1 - sj) DMAs are outstanding; the
         // next step's operands are fetched after the tile's last wait (tile 0 only)
         auto seg_ready = [&](int sj) {
           if (sj == SEGQ - 1) wait_vm<0>();
           else wait_vm_upto16(nrows);   // SEGQ == 2: the second segment's nrows DMAs may be in flight
-          if (a.poll) settle(sj);
           if (sj == SEGQ - 1 && jt == 0) prefetch(t);
         };
         f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -613,51 +659,28 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       const bool lv = ci < nlive;
       const int r = lv ? s_crow[ci] : 0;
       const size_t rowo = ((size_t)t * B + row0 + r) * H4 + (size_t)wave * H;
+      // k bound of this lane (0 past the list): an element at k >= klim gets offset all-ones (out
+      // of range: value 0, no access), computed arithmetically so that no per-chunk condition
+      // masks are held in scalar registers
+      const int klim = lv ? H : 0;
+      auto oob = [&](int k) -> uint32_t { return (uint32_t)((klim - 1 - k) >> 31); };
       auto fetch = [&](int c) -> uint4 {
         const int kk = c * KC + (PREC ? 8 : 4) * lq;
-        const size_t el = rowo + kk;
+        const uint32_t el = (uint32_t)(rowo + kk);
         if (vec_ok) {
-          const uint32_t off = (lv && kk < H) ? (uint32_t)(el * ESZ) : kOOB;
+          const uint32_t off = el * ESZ | oob(kk);
           if (a.coh_rows) return ld_coh_b128(r_dA, off);
           return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r_dA, off, 0, 0));
         }
         uint4 raw;
         uint32_t* rw = (uint32_t*)&raw;
         if constexpr (PREC == 0) {
-          for (int j = 0; j < 4; ++j) rw[j] = ld_coh_b32(r_dA, (lv && kk + j < H) ? (uint32_t)((el + j) * 4) : kOOB);
+          for (int j = 0; j < 4; ++j) rw[j] = ld_coh_b32(r_dA, (el + j) * 4 | oob(kk + j));
         } else {
           for (int j = 0; j < 4; ++j) {
-            uint32_t lo = ld_coh_b16(r_dA, (lv && kk + 2 * j < H) ? (uint32_t)((el + 2 * j) * 2) : kOOB);
-            uint32_t hi = ld_coh_b16(r_dA, (lv && kk + 2 * j + 1 < H) ? (uint32_t)((el + 2 * j + 1) * 2) : kOOB);
+            const uint32_t lo = ld_coh_b16(r_dA, (el + 2 * j) * 2 | oob(kk + 2 * j));
+            const uint32_t hi = ld_coh_b16(r_dA, (el + 2 * j + 1) * 2 | oob(kk + 2 * j + 1));
             rw[j] = lo | (hi << 16);
-          }
-        }
-        return raw;
-      };
-      // the same granule through agent-scope atomic loads (re-read on every call, L1 bypassed)
-      auto fetch_poll = [&](int c) -> uint4 {
-        const int kk = c * KC + (PREC ? 8 : 4) * lq;
-        const size_t el = rowo + kk;
-        const char* base = (const char*)a.dA;
-        uint4 raw = uint4{0u, 0u, 0u, 0u};
-        if (!lv) return raw;
-        if (vec_ok) {
-          if (kk < H) raw = ld_poll_b128(base + el * ESZ);
-          return raw;
-        }
-        uint32_t* rw = (uint32_t*)&raw;
-        if constexpr (PREC == 0) {
-          for (int j = 0; j < 4; ++j)
-            if (kk + j < H)
-              rw[j] = __hip_atomic_load((uint32_t*)(base + (el + j) * 4), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-          for (int j = 0; j < 8; ++j) {
-            if (kk + j >= H) continue;
-            const size_t e = el + j;
-            const uint32_t wv = __hip_atomic_load((uint32_t*)(base + (e & ~(size_t)1) * 2), __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-            const uint32_t hv = (e & 1) ? (wv >> 16) : (wv & 0xffffu);
-            rw[j >> 1] |= hv << (16 * (j & 1));
           }
         }
         return raw;
@@ -673,28 +696,6 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         if (gi + 1 < NG) {
 #pragma unroll
           for (int j = 0; j < CG; ++j) nxt[j] = ((gi + 1) * CG + j < KS) ? fetch((gi + 1) * CG + j) : uint4{0u, 0u, 0u, 0u};
-        }
-        if (a.poll) {
-          // granules whose producer's store has not arrived yet are fetched again
-          bool any = false;
-#pragma unroll
-          for (int j = 0; j < CG; ++j)
-            if (gi * CG + j < KS && pending_granule<PREC>(cur[j])) any = true;
-          if (__builtin_amdgcn_ballot_w64(any)) {
-#pragma unroll
-            for (int j = 0; j < CG; ++j) {
-              const int c = gi * CG + j;
-              if (c >= KS) continue;
-              int spins = 0;
-              while (pending_granule<PREC>(cur[j])) {
-                if (spin_out(spins, a.ctl, a.spin_limit)) {
-                  s_abort = 1;
-                  break;
-                }
-                cur[j] = fetch_poll(c);
-              }
-            }
-          }
         }
 #pragma unroll
         for (int j = 0; j < CG; ++j) {
@@ -723,26 +724,31 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // dA U^T of the push rows: the parent's dh (the parent is now the top)
 #pragma unroll
     for (int i = 0; i < PAIRS; ++i) {
-      if (c_op[i] == 1) {
-        const int ci = s_cidx[prow[i]];
+      if (pk(i) && (LEAN ? op_now[prw(i)] : c_op[LEAN ? 0 : i]) == 1) {
+        const int ci = s_cidx[prw(i)];
         gh[i] += red[0][ci][uu] + red[1][ci][uu] + red[2][ci][uu] + red[3][ci][uu];
       }
     }
     if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
     // rotate: step t-1 becomes current
-#pragma unroll
-    for (int i = 0; i < PAIRS; ++i) {
-      if constexpr (LEAN) {
-        if (t > 0) {
-          ld_row(t - 1, pok[i] ? row0 + prow[i] : 0, c_op[i], c_sp[i]);
-          valid_sp(t - 1, c_sp[i]);
-        }
-        continue;
+    if constexpr (LEAN) {
+      // row info of step t-1 into the other parity's LDS slots (last read during step t+1),
+      // then the loads of step t-2's
+      if (rr < BG && t > 0) {
+        int sp = r_nsp;
+        if (rr_ok) valid_sp(t - 1, sp);
+        s_rop[(t - 1) & 1][rr] = rr_ok ? r_nop : 0;
+        s_rsp[(t - 1) & 1][rr] = rr_ok ? sp : -1;
+        if (rr_ok && t > 1) ld_row(t - 2, row0 + rr, r_nop, r_nsp);
       }
-      c_op[i] = n_op[i]; c_sp[i] = n_sp[i];
-      n_op[i] = nn_op[i]; n_sp[i] = nn_sp[i];
-      if (t > 2) valid_sp(t - 2, n_sp[i]);
-      c_gh[i] = n_gh[i]; c_gc[i] = n_gc[i]; c_act[i] = n_act[i]; c_c[i] = n_c[i]; c_cp[i] = n_cp[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < PAIRS; ++i) {
+        c_op[i] = n_op[i]; c_sp[i] = n_sp[i];
+        n_op[i] = nn_op[i]; n_sp[i] = nn_sp[i];
+        if (t > 2) valid_sp(t - 2, n_sp[i]);
+        c_gh[i] = n_gh[i]; c_gc[i] = n_gc[i]; c_act[i] = n_act[i]; c_c[i] = n_c[i]; c_cp[i] = n_cp[i];
+      }
     }
     lds_sync();
   }
