@@ -48,6 +48,21 @@ __device__ __forceinline__ bf16_t f32_to_bf16_bits(float f) {
   return __builtin_bit_cast(bf16_t, h);
 }
 
+// Eight floats rounded to bf16 (nearest-even) in pairs, packed as they are converted.
+__device__ __forceinline__ bf16x8 pack_bf16x8(const float (&v)[8]) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 w;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    w[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{v[2 * j], v[2 * j + 1]}, bf16x2));
+  // (an empty asm on the packed words keeps the compiler from sinking the conversions to the
+  // first use, which would keep all the fp32 values live through the set-up)
+  asm volatile("" : "+v"(w));
+  return __builtin_bit_cast(bf16x8, w);
+}
+
 __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }

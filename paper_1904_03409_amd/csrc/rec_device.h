@@ -33,11 +33,13 @@ __device__ __forceinline__ void fwd_load_u(const RecArgs& a, int unit_base, int 
         u32[c][j] = (a_ok && k < H) ? Ucol[(size_t)k * H4] : 0.f;
       }
     } else {
+      float v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int k = c * 32 + 8 * lq + j;
-        u16[c][j] = f32_to_bf16((a_ok && k < H) ? Ucol[(size_t)k * H4] : 0.f);
+        v[j] = (a_ok && k < H) ? Ucol[(size_t)k * H4] : 0.f;
       }
+      u16[c] = pack_bf16x8(v);
     }
   }
 }

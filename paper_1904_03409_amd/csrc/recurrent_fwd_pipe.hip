@@ -6,8 +6,8 @@
 // Batch rows are independent of each other, so the tiles of a group form NT independent
 // chains. A step runs the tiles one after the other (one pass per tile), and the copy of
 // the next tile's h_prev rows into LDS (global_load_lds, the other of two LDS buffers) is
-// started halfway through the current tile's MFMAs: the round trip to L2 and the wait for
-// the other workgroups' states overlap with matrix work instead of adding to it. The copy
+// started three quarters through the current tile's MFMAs: the round trip to L2 and the wait
+// for the other workgroups' states overlap with matrix work instead of adding to it. The copy
 // of tile 0 for step t+1 starts during the last tile of step t, by when every workgroup has
 // long finished tile 0 of step t.
 //
@@ -230,34 +230,46 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
       const int nrow0 = row0 + 16 * ((p + 1) % NT);
 
       // ---- gates^T (16 cols x 16 rows) = U^T h_prev^T: B fragments read PD chunks ahead, two
-      // accumulator chains (even and odd chunks)
+      // accumulator chains (even and odd chunks). The fragments of the chunks from COPY_AT on
+      // are read into registers first and the next tile's copy is issued right after them: no
+      // LDS read of this pass follows the copy, so nothing waits for it before the next pass.
       constexpr int PD = PREC ? 4 : 2;
+      constexpr int NPRE = KS - COPY_AT;
+      static_assert(COPY_AT >= PD && NPRE >= 1, "copy issued after the read-ahead ring has started");
       f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
       if constexpr (PREC == 0) {
-        float4 fr[PD + 1];
+        float4 fr[PD + 1], pre[NPRE];
 #pragma unroll
         for (int c = 0; c < PD; ++c) fr[c] = *(const float4*)&buf[l16 * LDS_LD + c * 16 + 4 * lq];
 #pragma unroll
         for (int c = 0; c < KS; ++c) {
-          if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const float4*)&buf[l16 * LDS_LD + (c + PD) * 16 + 4 * lq];
-          if (c == COPY_AT) pipe_copy<PREC, SEG, LDS_LD>(a, nbuf, nsrc, nrow0, wave, lane);
+          if (c + PD < COPY_AT) fr[(c + PD) % (PD + 1)] = *(const float4*)&buf[l16 * LDS_LD + (c + PD) * 16 + 4 * lq];
+          if (c == COPY_AT - PD) {
+#pragma unroll
+            for (int j = 0; j < NPRE; ++j) pre[j] = *(const float4*)&buf[l16 * LDS_LD + (COPY_AT + j) * 16 + 4 * lq];
+            pipe_copy<PREC, SEG, LDS_LD>(a, nbuf, nsrc, nrow0, wave, lane);
+          }
           f32x4& acc = (c & 1) ? acc1 : acc0;
-          const float4 bv = fr[c % (PD + 1)];
+          const float4 bv = c < COPY_AT ? fr[c % (PD + 1)] : pre[c < COPY_AT ? 0 : c - COPY_AT];
           acc = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc);
           acc = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc);
           acc = mfma_f32_16x16x4(ureg32[c][2], bv.z, acc);
           acc = mfma_f32_16x16x4(ureg32[c][3], bv.w, acc);
         }
       } else {
-        bf16x8 fr[PD + 1];
+        bf16x8 fr[PD + 1], pre[NPRE];
 #pragma unroll
         for (int c = 0; c < PD; ++c) fr[c] = *(const bf16x8*)&buf[l16 * LDS_LD + c * 32 + 8 * lq];
 #pragma unroll
         for (int c = 0; c < KS; ++c) {
-          if (c + PD < KS) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&buf[l16 * LDS_LD + (c + PD) * 32 + 8 * lq];
-          if (c == COPY_AT) pipe_copy<PREC, SEG, LDS_LD>(a, nbuf, nsrc, nrow0, wave, lane);
+          if (c + PD < COPY_AT) fr[(c + PD) % (PD + 1)] = *(const bf16x8*)&buf[l16 * LDS_LD + (c + PD) * 32 + 8 * lq];
+          if (c == COPY_AT - PD) {
+#pragma unroll
+            for (int j = 0; j < NPRE; ++j) pre[j] = *(const bf16x8*)&buf[l16 * LDS_LD + (COPY_AT + j) * 32 + 8 * lq];
+            pipe_copy<PREC, SEG, LDS_LD>(a, nbuf, nsrc, nrow0, wave, lane);
+          }
           f32x4& acc = (c & 1) ? acc1 : acc0;
-          acc = mfma_bf16_16x16x32(ureg16[c], fr[c % (PD + 1)], acc);
+          acc = mfma_bf16_16x16x32(ureg16[c], c < COPY_AT ? fr[c % (PD + 1)] : pre[c < COPY_AT ? 0 : c - COPY_AT], acc);
         }
       }
       mfma_drain(acc0, acc1);
