@@ -72,7 +72,7 @@ struct Plan {
   int NT, G, per_xcc, pipe;   // pipe: the forward runs the pipelined kernel
   int fuse, kx;               // fuse: the plain bf16 forward contracts x_t W itself (kx chunks of 32)
   int wide, NWw;              // wide: the forward runs the 32-unit kernel (NWw workgroups per group)
-  int NTb, Gb, per_xcc_b;
+  int NTb, Gb, per_xcc_b, NWb; // NWb: backward workgroups per group (32 units each in the lean variant)
   int gs;                     // the backward runs the gate-split contraction
   int splits_w, splits_u;
 };
@@ -126,6 +126,9 @@ int make_plan(const slstm_dims* d, Plan* p) {
   p->KS = ks_bucket(prec, p->ks_eff);
   if (p->KS < 0) return SLSTM_EINVAL;
   p->NW = (d->H + 15) / 16;
+  // the backward compiled for K = 32 bf16 chunks (lean variant) runs 512-thread workgroups
+  // of 32 units, one per CU; the others 256-thread workgroups of 16 units
+  p->NWb = rec_occ(prec, p->KS) == 2 ? (d->H + 31) / 32 : p->NW;
   const int cus = device_cus();
   const int cu_per_xcc = cus > 0 ? cus / 8 : 32;
   // smallest row tile count per group whose workgroups (NW per group, groups dealt to the 8
@@ -144,7 +147,7 @@ int make_plan(const slstm_dims* d, Plan* p) {
     for (int NT = 1; NT <= 8; NT *= 2) {
       int G = (d->B + 16 * NT - 1) / (16 * NT);
       if (G > MAX_GROUPS) continue;
-      int per_xcc = p->NW * ((G + 7) / 8);
+      int per_xcc = (bwd ? p->NWb : p->NW) * ((G + 7) / 8);
       int occ = 0;
       const bool pipe = !bwd && pipe_ok && NT >= 2 && rec_pipe_built(prec, NT, p->KS);
       // the plain bf16 forward fuses the input projection when one pass covers the group
@@ -293,7 +296,7 @@ RecArgs rec_args(const slstm_dims* d, const Plan& p, char* ws, const Layout& L, 
   RecArgs a;
   memset(&a, 0, sizeof(a));
   a.T = d->T; a.B = d->B; a.I = d->I; a.H = d->H;
-  a.G = bwd ? p.Gb : p.G; a.NW = p.NW; a.ks_eff = p.ks_eff;
+  a.G = bwd ? p.Gb : p.G; a.NW = bwd ? p.NWb : p.NW; a.ks_eff = p.ks_eff;
   a.spin_limit = d->spin_limit > 0 ? d->spin_limit : kDefaultSpin;
   a.ctl = (uint32_t*)(ws + L.ctl);
   a.stash = (float*)(ws + L.stash);

@@ -45,27 +45,44 @@ namespace {
 __device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 }  // namespace
 
+// Threads per workgroup: 512 for the lean variant (compiled for OCC = 2, see below), else 256.
+constexpr int bwd_threads(int occ) { return occ == 2 ? 512 : 256; }
+
 template <int PREC, int NT, int KS, int OCC, bool GS>
-__global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
+__global__ void __launch_bounds__(bwd_threads(OCC), OCC == 2 ? 1 : OCC) k_bwd(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;
   constexpr int BG = NT * 16;
-  constexpr int PAIRS = BG * 16 / 256;            // (row, unit) pairs per thread
-  // Two workgroups per CU (bf16, H = 1024) leave 256 registers per lane, half of them for
-  // the U slice. The lean variant keeps per pair only the top state's gradient in registers;
-  // the row state (op and producer of the step, depth), the same for the 16 threads of a
-  // row, sits in LDS; each step's operands, and the spill slot a push reads, are loaded at the
-  // step (in batches of LB pairs), after every earlier store of the same thread, so the
-  // slot's last spill needs no forwarding.
+  // Lean variant (bf16, K = 32 chunks, i.e. H up to 1024): 256 registers per lane, half of
+  // them for the U slice. One workgroup of 512 threads per CU owns 32 hidden units (eight
+  // waves; wave q contracts the q-th eighth of the 4H gate columns for both 16-unit halves),
+  // so a CU reads every exchanged dA row once (two 256-thread workgroups of 16 units would
+  // each read it). It keeps per pair only the top state's gradient in registers; the row
+  // state (op and producer of the step, depth), the same for the threads of a row, sits in
+  // LDS; each step's operands, and the spill slot a push reads, are loaded at the step (in
+  // batches of LB pairs), after every earlier store of the same thread, so the slot's last
+  // spill needs no forwarding. The wave partials of each 16-row tile are added in LDS right
+  // after the tile, into one sum per (row, unit).
   constexpr bool LEAN = OCC == 2;
-  static_assert(BG <= 256, "one row-info thread per row");
-  constexpr int LB = PAIRS < 4 ? PAIRS : 4;
+  constexpr int NTH = bwd_threads(OCC);           // threads
+  constexpr int UPW = LEAN ? 32 : 16;             // hidden units per workgroup
+  constexpr int NWV = NTH / 64;                   // waves
+  constexpr int MTW = LEAN ? 2 : 1;               // 16-unit M tiles per wave
+  constexpr int KW = LEAN ? KS / 2 : KS;          // K chunks per wave (a wave's gate columns)
+  constexpr int PAIRS = BG * UPW / NTH;           // (row, unit) pairs per thread
+  static_assert(NTH / UPW == 16, "rows r = tid / UPW + 16 i");
+  static_assert(!LEAN || (PREC == 1 && KS % 2 == 0 && !GS), "lean: bf16, whole K halves");
+  static_assert(BG <= NTH, "one row-info thread per row");
+  constexpr int LB = PAIRS < 2 ? PAIRS : 2;
   static_assert(PAIRS % LB == 0, "whole load batches");
   // staged dA rows (direct path): per wave 16 compacted rows of its H gate columns
   constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
   extern __shared__ __align__(16) unsigned char dsm[];
-  __shared__ float red[4][BG][17];
+  __shared__ float red[LEAN ? 1 : 4][LEAN ? 1 : BG][17];
+  // lean: the wave partials of a tile (two tiles in turn) and the per-(row, unit) sums
+  __shared__ float red_t[LEAN ? 2 : 1][LEAN ? NWV : 1][16][LEAN ? UPW + 1 : 1];
+  __shared__ float s_dh[LEAN ? BG : 1][LEAN ? UPW + 1 : 1];
   __shared__ int s_op[BG], s_crow[BG], s_cidx[BG], s_nlive;
-  __shared__ float s_db[16][16][4];
+  __shared__ float s_db[16][UPW][4];
   __shared__ int s_g, s_w;
   __shared__ int s_abort;                          // a wait for dA rows gave up
   // lean variant: op and producer of each row by step parity, depth of each row
@@ -89,11 +106,33 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
   // ---- U^T slice: A(m = unit 16w + l16, k = gate column q*H + kk) = U[unit][caller column]
   // (GS: A(m = unit wave*H/4 + mt*16 + l16, k = this workgroup's gate column 64w + kk); the
   // same number of registers: H/64 M tiles of 64 / KC chunks per wave)
-  const int a_unit = w * 16 + l16;
+  const int a_unit = w * UPW + l16;
   const bool a_ok = a_unit < H;
   const float* Urow = a.U + (size_t)(a_ok ? a_unit : 0) * H4;
   float ureg32[PREC ? 1 : KS][4];
-  bf16x8 ureg16[PREC ? KS : 1];
+  bf16x8 ureg16[PREC && !LEAN ? KS : 1];
+  // lean: wave q's gate columns [kcb, kcb + kspan) of the 4H (an eighth), M tile mt = units
+  // w*32 + 16 mt + l16; chunk c holds columns kcb + c*32 + 8lq .. +7
+  const int kcb = LEAN ? (wave * H4) / NWV : wave * H;
+  const int kspan = LEAN ? ((wave + 1) * H4) / NWV - kcb : H;
+  bf16x8 uw[LEAN ? MTW : 1][LEAN ? KW : 1];
+  if constexpr (LEAN) {
+#pragma unroll
+    for (int mt = 0; mt < MTW; ++mt) {
+      const int unit = w * UPW + mt * 16 + l16;
+      const float* Ur = a.U + (size_t)(unit < H ? unit : 0) * H4;
+#pragma unroll
+      for (int c = 0; c < KW; ++c) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int kk = c * 32 + 8 * lq + j;
+          v[j] = (unit < H && kk < kspan) ? Ur[perm_to_orig(kcb + kk, H)] : 0.f;
+        }
+        uw[mt][c] = pack_bf16x8(v);
+      }
+    }
+  }
   constexpr int GCH = 64 / KC;                      // GS: K chunks of the own gate columns
   if constexpr (GS) {
     static_assert(KS % GCH == 0 && (KS / GCH) % 2 == 0, "GS: whole M tiles, two at a time");
@@ -114,34 +153,36 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       }
     }
   }
+  if constexpr (!GS && !LEAN) {
 #pragma unroll
-  for (int c = 0; c < KS && !GS; ++c) {
-    if constexpr (PREC == 0) {
+    for (int c = 0; c < KS; ++c) {
+      if constexpr (PREC == 0) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int kk = c * 16 + 4 * lq + j;
-        ureg32[c][j] = (a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f;
+        for (int j = 0; j < 4; ++j) {
+          int kk = c * 16 + 4 * lq + j;
+          ureg32[c][j] = (a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f;
+        }
+      } else {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          int kk = c * 32 + 8 * lq + j;
+          v[j] = (a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f;
+        }
+        ureg16[c] = pack_bf16x8(v);
       }
-    } else {
-      float v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        int kk = c * 32 + 8 * lq + j;
-        v[j] = (a_ok && kk < H) ? Urow[perm_to_orig(wave * H + kk, H)] : 0.f;
-      }
-      ureg16[c] = pack_bf16x8(v);
     }
   }
 
-  // ---- this thread's (row, unit) pairs: unit fixed per thread, rows r = tid/16 + 16 i
-  const int uu = threadIdx.x & 15;
-  const int u = w * 16 + uu;
+  // ---- this thread's (row, unit) pairs: unit fixed per thread, rows r = tid/UPW + 16 i
+  const int uu = threadIdx.x % UPW;
+  const int u = w * UPW + uu;
   const int ul = (u < H) ? u : 0;                   // unit used in load addresses (in bounds)
   int prow[PAIRS];
   bool pok[PAIRS];
 #pragma unroll
   for (int i = 0; i < PAIRS; ++i) {
-    prow[i] = (threadIdx.x >> 4) + 16 * i;
+    prow[i] = threadIdx.x / UPW + 16 * i;
     pok[i] = (row0 + prow[i] < B) && (u < H);
   }
   // depth after the last step, per pair; the spill slots S[0 .. depth) of the states that
@@ -159,12 +200,13 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     }
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
-  const bool vec_ok = PREC ? (H % 8 == 0) : (H % 4 == 0);
+  // 16-byte fetches: whole vectors in every row (lean: also at each wave's first column)
+  const bool vec_ok = LEAN ? (H % 16 == 0) : PREC ? (H % 8 == 0) : (H % 4 == 0);
   const bool direct = rec_bwd_direct_built(PREC, NT, KS) && !GS && a.bwd_direct != 0;
   using elem_t = typename std::conditional<PREC == 1, bf16_t, float>::type;
   elem_t* wbuf = reinterpret_cast<elem_t*>(dsm) + (size_t)wave * 16 * QLD;
   if (direct)
-    for (int i = threadIdx.x; i < 4 * 16 * QLD * ESZ / 16; i += 256) ((uint4*)dsm)[i] = uint4{0u, 0u, 0u, 0u};
+    for (int i = threadIdx.x; i < 4 * 16 * QLD * ESZ / 16; i += NTH) ((uint4*)dsm)[i] = uint4{0u, 0u, 0u, 0u};
   if (threadIdx.x == 0) s_abort = 0;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -279,10 +321,10 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // than held in registers (spilled) through the loop
     int tq = threadIdx.x;
     if constexpr (LEAN) asm volatile("" : "+v"(tq));
-    const int uq = LEAN ? w * 16 + (tq & 15) : u;
+    const int uq = LEAN ? w * UPW + tq % UPW : u;
     const int ulq = uq < H ? uq : 0;
-    auto prw = [&](int i) { return LEAN ? (tq >> 4) + 16 * i : prow[i]; };
-    auto pk = [&](int i) { return LEAN ? (row0 + (tq >> 4) + 16 * i < B) && (uq < H) : pok[i]; };
+    auto prw = [&](int i) { return LEAN ? tq / UPW + 16 * i : prow[i]; };
+    auto pk = [&](int i) { return LEAN ? (row0 + tq / UPW + 16 * i < B) && (uq < H) : pok[i]; };
     // row tables of step t for the compaction (from the registers of the unit-0 threads)
     if (uu == 0 && !LEAN) {
 #pragma unroll
@@ -512,7 +554,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     // gets an out-of-range offset: value 0, no memory access). Two accumulators per tile
     // keep two independent MFMA chains.
     constexpr int CG = LEAN ? 4 : 8;                // lean: measured fastest (fewer spills)
-    constexpr int NG = (KS + CG - 1) / CG;
+    constexpr int NG = (KW + CG - 1) / CG;
     const int nlive = s_nlive;
     if (!GS && (!direct || nlive == 0)) prefetch(t);
     // whole 1 KB row segments, at most two per staged row (H of at most 512 fp32 / 1024 bf16);
@@ -526,7 +568,7 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       // in the other variants. Every item's loads are issued together (one round trip).
       const int NWr = a.NW, WPG = NWr / 4;          // at most 8 (NW <= 32)
       const rsrc_t r_p = make_rsrc(a.gs_part + (size_t)((t & 1) * a.G + g) * BG * NWr * H, (size_t)BG * NWr * H * 4);
-      for (int it = threadIdx.x; it < nlive * 16; it += 256) {
+      for (int it = threadIdx.x; it < nlive * 16; it += NTH) {
         const int ci = it >> 4, qg = (it >> 2) & 3, q4 = it & 3;
         const uint32_t base = (uint32_t)((((size_t)ci * NWr + qg * WPG) * H + w * 16 + 4 * q4) * 4);
         uint4 v[8];
@@ -644,11 +686,11 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
       const int ci = jt * 16 + l16;
       const bool lv = ci < nlive;
       const int r = lv ? s_crow[ci] : 0;
-      const size_t rowo = ((size_t)t * B + row0 + r) * H4 + (size_t)wave * H;
+      const size_t rowo = ((size_t)t * B + row0 + r) * H4 + (size_t)kcb;
       // k bound of this lane (0 past the list): an element at k >= klim gets offset all-ones (out
       // of range: value 0, no access), computed arithmetically so that no per-chunk condition
       // masks are held in scalar registers
-      const int klim = lv ? H : 0;
+      const int klim = lv ? kspan : 0;
       auto oob = [&](int k) -> uint32_t { return (uint32_t)((klim - 1 - k) >> 31); };
       auto fetch = [&](int c) -> uint4 {
         const int kk = c * KC + (PREC ? 8 : 4) * lq;
@@ -672,23 +714,31 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
         return raw;
       };
       f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = f32x4{0.f, 0.f, 0.f, 0.f};
+      f32x4 accl[LEAN ? MTW : 1][2];
+#pragma unroll
+      for (int mt = 0; mt < (LEAN ? MTW : 1); ++mt) accl[mt][0] = accl[mt][1] = acc0;
       uint4 bufA[CG], bufB[CG];
 #pragma unroll
-      for (int j = 0; j < CG; ++j) bufA[j] = (j < KS) ? fetch(j) : uint4{0u, 0u, 0u, 0u};
+      for (int j = 0; j < CG; ++j) bufA[j] = (j < KW) ? fetch(j) : uint4{0u, 0u, 0u, 0u};
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
         uint4 (&cur)[CG] = (gi & 1) ? bufB : bufA;
         uint4 (&nxt)[CG] = (gi & 1) ? bufA : bufB;
         if (gi + 1 < NG) {
 #pragma unroll
-          for (int j = 0; j < CG; ++j) nxt[j] = ((gi + 1) * CG + j < KS) ? fetch((gi + 1) * CG + j) : uint4{0u, 0u, 0u, 0u};
+          for (int j = 0; j < CG; ++j) nxt[j] = ((gi + 1) * CG + j < KW) ? fetch((gi + 1) * CG + j) : uint4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int j = 0; j < CG; ++j) {
           const int c = gi * CG + j;
-          if (c >= KS) continue;
+          if (c >= KW) continue;
           f32x4& acc = (j & 1) ? acc1 : acc0;
-          if constexpr (PREC == 0) {
+          if constexpr (LEAN) {
+            // one fragment of 16 rows feeds both 16-unit M tiles
+#pragma unroll
+            for (int mt = 0; mt < MTW; ++mt)
+              accl[mt][j & 1] = mfma_bf16_16x16x32(uw[mt][c], __builtin_bit_cast(bf16x8, cur[j]), accl[mt][j & 1]);
+          } else if constexpr (PREC == 0) {
             const float4 bv = __builtin_bit_cast(float4, cur[j]);
             acc = mfma_f32_16x16x4(ureg32[c][0], bv.x, acc);
             acc = mfma_f32_16x16x4(ureg32[c][1], bv.y, acc);
@@ -699,8 +749,27 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
           }
         }
       }
-      // lane holds units 4*lq + j of compacted row ci
-      if (lv) {
+      if constexpr (LEAN) {
+        // lane holds units 16 mt + 4*lq + j of tile row l16; the tile's wave partials (tiles
+        // alternate between two buffers: a buffer is written again two tiles later, after the
+        // barrier that follows the next tile's writes, by when every thread has summed it)
+        const int pb = jt & 1;
+        if (lv) {
+#pragma unroll
+          for (int mt = 0; mt < MTW; ++mt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) red_t[pb][wave][l16][mt * 16 + 4 * lq + j] = accl[mt][0][j] + accl[mt][1][j];
+        }
+        lds_sync();
+        const int rs = threadIdx.x / UPW, cs = jt * 16 + rs;
+        if (cs < nlive) {
+          float sum = 0.f;
+#pragma unroll
+          for (int q = 0; q < NWV; ++q) sum += red_t[pb][q][rs][uu];
+          s_dh[cs][uu] = sum;
+        }
+      } else if (lv) {
+        // lane holds units 4*lq + j of compacted row ci
 #pragma unroll
         for (int j = 0; j < 4; ++j) red[wave][ci][4 * lq + j] = acc0[j] + acc1[j];
       }
@@ -712,7 +781,8 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     for (int i = 0; i < PAIRS; ++i) {
       if (pk(i) && (LEAN ? op_now[prw(i)] : c_op[LEAN ? 0 : i]) == 1) {
         const int ci = s_cidx[prw(i)];
-        gh[i] += red[0][ci][uu] + red[1][ci][uu] + red[2][ci][uu] + red[3][ci][uu];
+        if constexpr (LEAN) gh[i] += s_dh[ci][uu];
+        else gh[i] += red[0][ci][uu] + red[1][ci][uu] + red[2][ci][uu] + red[3][ci][uu];
       }
     }
     if (clk && threadIdx.x == 0) clk[t * 4 + 3] = wall_clock64();
@@ -749,14 +819,14 @@ __global__ void __launch_bounds__(256, OCC) k_bwd(RecArgs a) {
     a.dh0[(size_t)b * H + u] = gh[i];
     a.dc0[(size_t)b * H + u] = gc[i];
   }
-  const int rgrp = threadIdx.x >> 4;                 // 16 row groups share a unit
+  const int rgrp = threadIdx.x / UPW;                // 16 row groups share a unit
   for (int j = 0; j < 4; ++j) s_db[rgrp][uu][j] = dbacc[j];
   __syncthreads();
-  if (threadIdx.x < 64) {
+  if (threadIdx.x < UPW * 4) {
     int uu2 = threadIdx.x >> 2, j = threadIdx.x & 3;
     float s = 0.f;
     for (int q = 0; q < 16; ++q) s += s_db[q][uu2][j];
-    int u2 = w * 16 + uu2;
+    int u2 = w * UPW + uu2;
     if (u2 < H) a.db_part[(size_t)g * H4 + 4 * u2 + j] = s;
   }
 }
@@ -769,13 +839,13 @@ static hipError_t launch_bwd_k(const RecArgs& a, dim3 grid, hipStream_t st, int*
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
   if (e != hipSuccess) return e;
   int occ = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, shm);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, bwd_threads(OCC), shm);
   if (e != hipSuccess) return e;
   if (occ_out) *occ_out = occ;
   if (!grid.x) return hipSuccess;
   RecArgs args = a;
   void* kargs[] = {&args};
-  return hipLaunchCooperativeKernel((const void*)kern, grid, dim3(256), kargs, (unsigned)shm, st);
+  return hipLaunchCooperativeKernel((const void*)kern, grid, dim3(bwd_threads(OCC)), kargs, (unsigned)shm, st);
 }
 
 template <int P, int NT, int KS>
