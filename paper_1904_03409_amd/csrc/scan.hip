@@ -168,10 +168,15 @@ __global__ void __launch_bounds__(256) k_h0_bf16(const float* __restrict__ h0, b
     hx[i] = f32_to_bf16_bits(h0[i]);
 }
 
-// fp32 -> bf16 (nearest even), elementwise
-__global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ in, bf16_t* __restrict__ out, size_t n) {
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    out[i] = f32_to_bf16_bits(in[i]);
+// fp32 -> bf16 (nearest even), eight elements per thread and iteration: 32 bytes read and
+// 16 written with vector accesses (in and out 16-byte aligned); the input is read once
+__global__ void __launch_bounds__(256) k_to_bf16x8(const float* __restrict__ in, bf16_t* __restrict__ out, size_t n8) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (size_t)gridDim.x * blockDim.x) {
+    const f32x4 lo = __builtin_nontemporal_load((const f32x4*)in + 2 * i);
+    const f32x4 hi = __builtin_nontemporal_load((const f32x4*)in + 2 * i + 1);
+    const float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    ((bf16x8*)out)[i] = pack_bf16x8(v);
+  }
 }
 
 // Clears the backward's control words: slot counters, group barrier counters, the wait flags
