@@ -34,6 +34,7 @@ __global__ void k_gather_hprev(const int32_t* top, const float* hcell, const flo
 __global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int cols, const int32_t* prow,
                                  const uint32_t* count, int ldo, const int32_t* gtop, int B, bf16_t* out, uint32_t* ctl);
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
+__global__ void k_gemm_wide(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
 __global__ void k_scatter_splits(const float* P, const int32_t* rows, const uint32_t* count, size_t max_rows, int N,
@@ -266,6 +267,28 @@ int launch_gemm(int prec, int AL, int BL, const GemmArgs& g, int splits, hipStre
   return SLSTM_EINVAL;
 }
 
+// The wide-tile bf16 GEMM takes MK x NK bf16 operands with 16-byte rows, no row gathers and
+// no device-side M.
+bool gemm_wide_ok(int prec, int AL, int BL, const GemmArgs& g) {
+  return prec == SLSTM_BF16_GEMM && AL == GEMM_MK && BL == GEMM_NK && g.a_vec && g.b_vec && !g.a_rows && !g.b_rows &&
+         !g.c_rows && !(g.dyn && g.dyn_axis == 0) && g.K % 8 == 0;
+}
+int wide_tiles(int M, int N) { return ((M + kGemmWideBM - 1) / kGemmWideBM) * ((N + kGemmWideBN - 1) / kGemmWideBN); }
+// split K of a wide-tile GEMM: one round of one workgroup per CU (256 blocks), at most 64
+// slices and one 64-deep K tile per slice
+int wide_splits(int M, int N, int K) {
+  const int s = std::max(1, 256 / std::max(1, wide_tiles(M, N)));
+  return std::min(std::min(s, 64), std::max(1, (K + 63) / 64));
+}
+int launch_gemm_wide(const GemmArgs& g, int splits, hipStream_t st) {
+  if (hipFuncSetAttribute((const void*)k_gemm_wide, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGemmWideLds) !=
+      hipSuccess)
+    return SLSTM_EDEVICE;
+  dim3 grid((g.N + kGemmWideBN - 1) / kGemmWideBN, (g.M + kGemmWideBM - 1) / kGemmWideBM, splits);
+  hipLaunchKernelGGL(k_gemm_wide, grid, dim3(256), kGemmWideLds, st, g);
+  return hip_status(hipGetLastError());
+}
+
 // K slice per split, a multiple of the GEMM's K tile (64 covers both precisions)
 int k_chunk_for(int K, int splits) { return ((K + splits - 1) / splits + 63) / 64 * 64; }
 
@@ -435,7 +458,12 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
       g.A = x16;
       al = GEMM_MK;
     }
-    if ((rc = launch_gemm(p.prec, al, bf ? GEMM_NK : GEMM_KN, g, 1, st))) return rc;
+    // (bf16 operands: the wide-tile GEMM when its 256 x 256 tiles alone fill the chip)
+    if (gemm_wide_ok(p.prec, al, GEMM_NK, g) && wide_tiles(g.M, g.N) >= 256) {
+      if ((rc = launch_gemm_wide(g, 1, st))) return rc;
+    } else if ((rc = launch_gemm(p.prec, al, bf ? GEMM_NK : GEMM_KN, g, 1, st))) {
+      return rc;
+    }
   }
 
   // a3-a6: persistent recurrent kernel
@@ -634,9 +662,15 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
             g.Bm = a.dA; g.ldb = H4; g.b_vec = 1; g.b_rows = prow; }
   g.C = part; g.ldc = H4;
   g.split_stride = (size_t)I * H4;
-  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, p.splits_w, st))) return rc;
-  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, p.splits_w,
-                     g.split_stride, I, H4, H, dW);
+  // (bf16: the wide-tile GEMM, with its own split count, when the output has 32 or more of its
+  // tiles: measured faster at the thru shape, slower at the large one, whose K slices are short)
+  const bool wide_w = gemm_wide_ok(p.prec, GEMM_MK, GEMM_NK, g) && wide_tiles(g.M, g.N) >= 32;
+  const int sw = wide_w ? wide_splits(g.M, g.N, g.K) : p.splits_w;
+  if ((rc = wide_w ? launch_gemm_wide(g, sw, st)
+                   : launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, sw, st)))
+    return rc;
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)I * H4)), dim3(256), 0, st, part, sw, g.split_stride, I, H4,
+                     H, dW);
   mark(d, 7, st);
   // dU = Hprev^T dA
   gemm_base();
@@ -646,9 +680,13 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
             g.b_rows = prow; }
   g.C = part; g.ldc = H4;
   g.split_stride = (size_t)H * H4;
-  if ((rc = launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, p.splits_u, st))) return rc;
-  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, p.splits_u,
-                     g.split_stride, H, H4, H, dU);
+  const bool wide_u = gemm_wide_ok(p.prec, GEMM_MK, GEMM_NK, g) && wide_tiles(g.M, g.N) >= 32;
+  const int su = wide_u ? wide_splits(g.M, g.N, g.K) : p.splits_u;
+  if ((rc = wide_u ? launch_gemm_wide(g, su, st)
+                   : launch_gemm(p.prec, bf ? GEMM_MK : GEMM_KM, bf ? GEMM_NK : GEMM_KN, g, su, st)))
+    return rc;
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid1d((size_t)H * H4)), dim3(256), 0, st, part, su, g.split_stride, H, H4,
+                     H, dU);
   mark(d, 8, st);
   // dx = dA Wp^T on the push rows (gathered from dA); the GEMM's grid covers all T*B rows, so
   // the push rows' tiles take two or more blocks each, over K slices written as partials that

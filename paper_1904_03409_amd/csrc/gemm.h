@@ -30,6 +30,10 @@ struct GemmArgs {
   // use packed, c_rows must be null); k_scatter_splits then adds them into the gathered rows.
   int dyn_split;
 };
+// Block tile of the wide bf16 GEMM (k_gemm_wide) and its dynamic LDS (two buffers of A and B
+// slices, 64 k + 8 padding per row)
+constexpr int kGemmWideBM = 256, kGemmWideBN = 256;
+constexpr size_t kGemmWideLds = (size_t)2 * (kGemmWideBM + kGemmWideBN) * (64 + 8) * 2;
 // K slices per tile for a device-M GEMM over `active` tiles on a grid of `blocks` blocks.
 __host__ __device__ inline int gemm_dyn_splits(int blocks, int active) {
   if (active <= 0) return 1;

@@ -391,6 +391,153 @@ __global__ void __launch_bounds__(256) k_scatter_splits(const float* __restrict_
   }
 }
 
+// Wide-tile bf16 GEMM for A stored MK and B stored NK, both bf16 with 16-byte rows: a
+// 256 x 256 block tile, four waves of 128 x 128 (64 MFMA tiles per wave, the accumulators in
+// AGPRs), 64-deep K slices double-buffered in LDS, one workgroup per CU. A wave reads 16 B
+// fragments per 64 MFMAs: a quarter of the LDS bytes per MFMA of k_gemm's 64 x 64 wave tile,
+// whose bf16 form is bound by LDS reads (about 32 B per cycle per wave, eight waves per CU,
+// against 128 B per cycle per CU). Split K (gridDim.z) and a device-side K as in k_gemm; no
+// row gathers and no device-side M.
+static_assert(kGemmWideBN == 256, "one bias column per thread");
+__global__ void __launch_bounds__(256, 1) k_gemm_wide(GemmArgs g) {
+  constexpr int BMW = kGemmWideBM, BNW = kGemmWideBN, BKW = 64, LDW = BKW + 8;   // LDS row stride: 16-byte pad
+  extern __shared__ __align__(16) unsigned char gsm[];
+  bf16_t* As = reinterpret_cast<bf16_t*>(gsm);     // [2][BMW][LDW]
+  bf16_t* Bs = As + 2 * BMW * LDW;                 // [2][BNW][LDW]
+  // block -> (n tile, m tile, K slice): XCD-contiguous runs over groups of GM m tiles, as k_gemm
+  constexpr int GM = 4;
+  const int NTL = (int)gridDim.x, MTL = (int)gridDim.y;
+  const int nblk = NTL * MTL * (int)gridDim.z;
+  int lid = (int)blockIdx.x + NTL * ((int)blockIdx.y + MTL * (int)blockIdx.z);
+  {
+    const int full = nblk & ~7;
+    if (lid < full) lid = (lid & 7) * (full >> 3) + (lid >> 3);
+  }
+  const int per = NTL * MTL;
+  const int tz = lid / per;
+  const int r0 = lid - tz * per;
+  const int gidx = r0 / (GM * NTL);
+  const int gm = min(GM, MTL - gidx * GM);
+  const int rg = r0 - gidx * GM * NTL;
+  const int tm = gidx * GM + rg % gm, tn = rg / gm;
+  int K = g.K, kchunk = g.k_chunk;
+  if (g.dyn) {                                      // device-side K (the host never passes a device M)
+    const int ext = (int)((*g.dyn + (uint32_t)g.dyn_round - 1u) / (uint32_t)g.dyn_round * (uint32_t)g.dyn_round);
+    K = min(K, ext);
+    kchunk = ((K + (int)gridDim.z - 1) / (int)gridDim.z + 63) / 64 * 64;
+  }
+  const int M = g.M, N = g.N;
+  const int m0 = tm * BMW, n0 = tn * BNW;
+  const int kbeg = tz * kchunk, kend = min(K, kbeg + kchunk);
+  float* C = g.C + (size_t)tz * g.split_stride;
+  const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int l16 = lane & 15, lq = lane >> 4;
+  const rsrc_t ra = make_rsrc(g.A, (size_t)M * g.lda * 2);
+  const rsrc_t rb = make_rsrc(g.Bm, (size_t)N * g.ldb * 2);
+  // staging of one slice: per operand 256 rows x 64 k, eight 16-byte vectors per thread
+  // (vector e = tid + 256 i: row e / 8, k 8 (e % 8)); outside the rows or K: offset beyond the
+  // buffer (reads 0, no access)
+  uint4 va[8], vb[8];
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int e = tid + 256 * i, r = e >> 3, gk = k0 + (e & 7) * 8;
+      const bool kin = gk < kend;
+      const uint32_t ao = (kin && m0 + r < M) ? (uint32_t)(((size_t)(m0 + r) * g.lda + gk) * 2) : 0xffffffffu;
+      const uint32_t bo = (kin && n0 + r < N) ? (uint32_t)(((size_t)(n0 + r) * g.ldb + gk) * 2) : 0xffffffffu;
+      va[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, ao, 0, 0));
+      vb[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, bo, 0, 0));
+    }
+  };
+  auto stage = [&](int b) {
+    bf16_t* as = As + b * BMW * LDW;
+    bf16_t* bs = Bs + b * BNW * LDW;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int e = tid + 256 * i, r = e >> 3, c = (e & 7) * 8;
+      *(uint4*)&as[r * LDW + c] = va[i];
+      *(uint4*)&bs[r * LDW + c] = vb[i];
+    }
+  };
+  // the block's bias columns, into LDS before the K loop (no registers held through it)
+  __shared__ float s_bias[BNW];
+  {
+    const int n = n0 + tid;
+    s_bias[tid] = (g.bias && n < N) ? g.bias[perm_to_orig(n, g.bias_H)] : 0.f;
+  }
+  f32x4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int buf = 0;
+  if (kbeg < kend) {
+    fetch(kbeg);
+    stage(0);
+  }
+  __syncthreads();
+  for (int k0 = kbeg; k0 < kend; k0 += BKW) {
+    const bool more = k0 + BKW < kend;
+    if (more) fetch(k0 + BKW);                      // next slice in flight during this one
+    const bf16_t* as = As + buf * BMW * LDW;
+    const bf16_t* bs = Bs + buf * BNW * LDW;
+#pragma unroll
+    for (int kc = 0; kc < BKW / 32; ++kc) {
+      bf16x8 a8[8], b8[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a8[i] = *(const bf16x8*)&as[(wm * 128 + i * 16 + l16) * LDW + kc * 32 + 8 * lq];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) b8[j] = *(const bf16x8*)&bs[(wn * 128 + j * 16 + l16) * LDW + kc * 32 + 8 * lq];
+      // C^T = B^T A^T: a lane holds row l16, columns 4*lq .. 4*lq+3 of each 16 x 16 tile
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = mfma_bf16_16x16x32(b8[j], a8[i], acc[i][j]);
+    }
+    if (more) stage(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+  // epilogue through LDS (the K loop's buffers are free now): the block's rows are written
+  // out in two halves of 128; the waves of one half put their tiles in LDS, then every wave
+  // stores whole rows, 64 lanes x 16 bytes = one contiguous 1 KB row per instruction
+  // (non-temporal: the output is streamed out)
+  constexpr int OLD = BNW + 4;                     // LDS row stride of the staged output (floats)
+  static_assert((size_t)128 * OLD * 4 <= kGemmWideLds, "half the output tile fits the slice buffers");
+  float* os = reinterpret_cast<float*>(gsm);
+  const bool cvec = (g.ldc % 4) == 0 && (((uintptr_t)C) & 15u) == 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (wm == h) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          *(f32x4*)&os[(i * 16 + l16) * OLD + wn * 128 + j * 16 + 4 * lq] = acc[i][j];
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int it = 0; it < 32; ++it) {
+      const int idx = tid + 256 * it, r = idx >> 6, c = (idx & 63) * 4;
+      const int m = m0 + h * 128 + r, n = n0 + c;
+      if (m >= M) continue;
+      const f32x4 v = *(const f32x4*)&os[r * OLD + c];
+      const float4 bv = *(const float4*)&s_bias[c];
+      const f32x4 o = f32x4{v[0] + bv.x, v[1] + bv.y, v[2] + bv.z, v[3] + bv.w};
+      float* cp = C + (size_t)m * g.ldc + n;
+      if (cvec && n + 3 < N) {
+        __builtin_nontemporal_store(o, (f32x4*)cp);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (n + q < N) cp[q] = o[q];
+      }
+    }
+    __syncthreads();
+  }
+}
+
 #define INST(P, A, B) template __global__ void k_gemm<P, A, B>(GemmArgs);
 INST(0, GEMM_MK, GEMM_KN)
 INST(0, GEMM_MK, GEMM_NK)
