@@ -5,7 +5,10 @@
 // K per chunk of the register-resident U slice: 16 (fp32 MFMA, 4 k per lane x 4 steps)
 // or 32 (bf16 MFMA, 8 k per lane).
 constexpr int rec_kc(int prec) { return prec ? 32 : 16; }
-constexpr int rec_lds_ld(int prec, int ks) { return ks * rec_kc(prec) + (prec ? 8 : 4); }
+// Padding of a staged row (elements): keeps rows 16-byte aligned and moves consecutive rows
+// to other LDS banks for the fragment reads (lane l16 reads row l16).
+constexpr int rec_lds_pad(int prec) { return prec ? 8 : 4; }
+constexpr int rec_lds_ld(int prec, int ks) { return ks * rec_kc(prec) + rec_lds_pad(prec); }
 // Row tiles staged in LDS per pass: as many as fit in about 68 KB, so two workgroups
 // can share a CU when the configuration needs it.
 constexpr int rec_ntb(int prec, int nt, int ks) {
@@ -74,11 +77,13 @@ constexpr bool rec_pipe_built(int prec, int nt, int ks) {
   return prec == 0 ? (ks == 16 || (ks == 32 && nt <= 4)) : ks == 16;
 }
 
-// Wide forward (bf16, H > 512): three 16-row tile buffers of K = 32*KS bf16 columns, the
+// Wide forward (bf16, H > 512): row padding of its staged tiles (elements), then the LDS of
+// three 16-row tile buffers of K = 32*KS bf16 columns, the
 // per-tile recurrence state (NT tiles x 4 floats x 256 lanes) and three input-projection
 // slots (2 float4 x 256 lanes).
+constexpr int rec_wide_pad = 8;
 constexpr size_t rec_wide_lds_bytes(int ks, int nt) {
-  return (size_t)3 * 16 * (ks * 32 + 8) * 2 + (size_t)nt * 4 * 256 * 4 + (size_t)3 * 2 * 256 * 16;
+  return (size_t)3 * 16 * (ks * 32 + rec_wide_pad) * 2 + (size_t)nt * 4 * 256 * 4 + (size_t)3 * 2 * 256 * 16;
 }
 
 hipError_t launch_fwd(const struct RecArgs& a, const struct FxArgs& f, int prec, int NT, int KS, dim3 grid,

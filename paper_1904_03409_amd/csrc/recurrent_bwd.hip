@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(bwd_threads(OCC), OCC == 2 ? 1 : OCC) k_bwd(Re
   constexpr int LB = PAIRS < 2 ? PAIRS : 2;
   static_assert(PAIRS % LB == 0, "whole load batches");
   // staged dA rows (direct path): per wave 16 compacted rows of its H gate columns
-  constexpr int QLD = KS * KC + (PREC ? 8 : 4);         // row stride (elements), 16-byte pad
+  constexpr int QLD = rec_lds_ld(PREC, KS);             // row stride (elements), padded
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ float red[LEAN ? 1 : 4][LEAN ? 1 : BG][17];
   // lean: the wave partials of a tile (two tiles in turn) and the per-(row, unit) sums

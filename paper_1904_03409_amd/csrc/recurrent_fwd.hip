@@ -30,7 +30,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd(RecArgs a, FxArgs f) {
   constexpr int KC = PREC ? 32 : 16;               // K per chunk
   constexpr int KP = KS * KC;                      // K capacity of the U registers
   constexpr int ESZ = PREC ? 2 : 4;                // bytes per staged element
-  constexpr int LDS_LD = KP + (PREC ? 8 : 4);      // LDS row stride (elements): 16-byte pad
+  constexpr int LDS_LD = rec_lds_ld(PREC, KS);     // LDS row stride (elements), padded
   constexpr int ROWS_B = NTB * 16;                 // rows staged per pass
   constexpr int NPASS = NT / NTB;
   constexpr int BG = NT * 16;                      // rows per group

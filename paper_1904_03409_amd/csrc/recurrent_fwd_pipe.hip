@@ -98,7 +98,7 @@ __global__ void __launch_bounds__(256, OCC) k_fwd_pipe(RecArgs a) {
   constexpr int KC = PREC ? 32 : 16;               // K per chunk
   constexpr int KP = KS * KC;                      // K capacity of the U registers
   constexpr int ESZ = PREC ? 2 : 4;
-  constexpr int LDS_LD = KP + (PREC ? 8 : 4);      // LDS row stride (elements): 16-byte pad
+  constexpr int LDS_LD = rec_lds_ld(PREC, KS);     // LDS row stride (elements), padded
   constexpr int SEG = KP * ESZ / 1024;             // 1 KB segments per row
   constexpr int BUF = 16 * LDS_LD;                 // elements per tile buffer
   constexpr int BG = NT * 16;                      // rows per group

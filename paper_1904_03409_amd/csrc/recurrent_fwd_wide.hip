@@ -62,7 +62,7 @@ template <int NT, int KS>
 __global__ void __launch_bounds__(256, 1) k_fwd_wide(RecArgs a) {
   constexpr int KC = 32;                          // K per MFMA chunk (bf16)
   constexpr int KP = KS * KC;                     // K capacity of the U registers
-  constexpr int LDS_LD = KP + 8;                  // LDS row stride (elements): 16-byte pad
+  constexpr int LDS_LD = KP + rec_wide_pad;       // LDS row stride (elements), padded
   constexpr int SEG = KP * 2 / 1024;              // 1 KB segments per staged row
   constexpr int BUF = 16 * LDS_LD;                // elements per tile buffer
   constexpr int NBUF = 3, DIST = 2;               // tile buffers; copies run DIST passes ahead
