@@ -171,7 +171,9 @@ typedef struct {
   int32_t fwd_kernel;      /* 0 plain, 1 pipelined (two LDS tile buffers), 2 wide (bf16, H > 512) */
   int32_t fwd_tiles;       /* forward: 16-row tiles per group */
   int32_t k_chunk_cap;     /* K chunks compiled into the kernels (power of two >= k_chunks) */
-  int32_t occupancy;       /* workgroups per CU the recurrent kernels are compiled for */
+  int32_t occupancy;       /* 2: the recurrent kernels are compiled for 256 registers per lane
+                              (two 256-thread workgroups per CU in the forward, one 512-thread
+                              workgroup in the backward), else 1 */
   int32_t bwd_groups;      /* backward: batch groups */
   int32_t bwd_tiles;       /* backward: 16-row tiles per group */
   int32_t bwd_direct;      /* backward: dA rows staged in LDS by DMA (1) or read into registers (0) */

@@ -32,8 +32,10 @@ constexpr bool rec_fx_fits(int rows, int kx) { return kx <= 8 && rows > 0; }
 constexpr size_t rec_bwd_lds_bytes(int prec, int ks) { return (size_t)4 * 16 * rec_lds_ld(prec, ks) * (prec ? 2 : 4); }
 constexpr size_t rec_bwd_static_lds(int nt) { return (size_t)4 * nt * 16 * 17 * 4 + 16 * 16 * 4 * 4 + 5 * nt * 16 * 4 + 64; }
 
-// Workgroups per CU the kernel is compiled for: 2 for the bf16 H > 512 case (64
-// workgroups per group), 1 otherwise.
+// Register budget of the kernels for the bf16 K = 32 chunk case (H > 512): 256 registers per
+// lane, as for two 256-thread workgroups per CU; the plain forward runs two workgroups of 16
+// units per CU, the backward one 512-thread workgroup of 32 units. 1 (the whole register file
+// for one 256-thread workgroup) otherwise.
 constexpr int rec_occ(int prec, int ks) { return (prec == 1 && ks == 32) ? 2 : 1; }
 // Backward instantiations that contain the direct-staging path (LDS DMA of the dA rows with
 // hand-counted vmcnt waits): whole 1 KB row segments, at most two per row, one workgroup per

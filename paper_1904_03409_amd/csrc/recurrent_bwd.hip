@@ -14,15 +14,17 @@
 //         parent (depth p-1) becomes the top: (Gh, Gc) = S[p-1] + (dA U^T, dc f).
 // S[d] of a state that stays on the stack to the end is 0 (zeroed before the sweep); every
 // other S[d] read was stored by the pop of the state above it, at a later step. The most
-// recent store is forwarded in registers, older ones are prefetched a step ahead; no
-// accumulator is read and written in the same step.
+// recent store is forwarded in registers, older ones are prefetched a step ahead (the lean
+// variant below loads the slot at the step instead); no accumulator is read and written in
+// the same step.
 //
 // Same work split as the forward: group of 16*NT rows on one XCC, workgroup w owns
-// hidden units [16w, 16w+16). dA U^T needs all 4H gate columns, so dA is exchanged
+// hidden units [16w, 16w+16) (the lean variant: [32w, 32w+32)). dA U^T needs all 4H gate
+// columns, so dA is exchanged
 // through L2, with a group barrier per step (each workgroup stores its push rows' dA, arrives,
 // waits for the others, then reads every push row of the group). Wave q contracts
-// gate columns [qH, (q+1)H) against its register-resident slice of U and the four partial
-// sums are added in LDS in a fixed order. Every gradient element is owned by one thread,
+// gate columns [qH, (q+1)H) (lean: the q-th eighth of the 4H) against its register-resident
+// slice of U and the wave partial sums are added in LDS in a fixed order. Every gradient element is owned by one thread,
 // so there are no atomics. Workgroup barriers that only order LDS accesses do not wait for
 // outstanding global loads.
 //
