@@ -137,17 +137,26 @@ def executed_flops(wl):
     return out
 
 
+def strip_comments(src: str) -> str:
+    """C++ source without its comments and with runs of white space collapsed (string
+    literals in the library's sources hold no comment markers)."""
+    import re
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def kernel_sources_sha1():
-    """Hash of every HIP source and header of the library: a stored counter reading is
-    valid only for the kernels it was taken from."""
+    """Hash of the code (comments and layout left out) of every HIP source and header of the
+    library: a stored counter reading is valid only for the kernels it was taken from."""
     import glob
     import hashlib
     h = hashlib.sha1()
     for f in sorted(glob.glob(os.path.join(ROOT, "paper_1904_03409_amd", "csrc", "*"))):
         if f.endswith((".hip", ".h")):
             h.update(os.path.basename(f).encode())
-            with open(f, "rb") as fh:
-                h.update(fh.read())
+            with open(f, encoding="utf-8") as fh:
+                h.update(strip_comments(fh.read()).encode())
     return h.hexdigest()
 
 

@@ -33,3 +33,13 @@ def test_sweep_workloads_have_fixed_length_and_hold_padding():
     # without the override the recipe is unchanged
     a, b = wk.make("parser"), wk.make("parser", T=None)
     assert a.T == b.T and np.array_equal(a.ops, b.ops) and np.array_equal(a.x, b.x)
+
+
+def test_kernel_hash_ignores_comments_not_code():
+    """Stored counter readings stay valid across comment edits, not across code edits."""
+    from bench import strip_comments
+    a = "int f(int x) { return x + 1; } // add one\n/* block\n comment */ int g;"
+    b = "int f(int x) {\n  return x + 1;   // different words\n}\nint g;"
+    c = "int f(int x) { return x + 2; } int g;"
+    assert strip_comments(a) == strip_comments(b)
+    assert strip_comments(a) != strip_comments(c)
