@@ -95,6 +95,14 @@ typedef struct {
                               each step (forward: loop top, h_prev staged, MFMA done, epilogue
                               done; backward: loop top, epilogue done, row list ready, dh
                               scattered). For profiling only. */
+  int32_t defer_status;    /* 0: each call ends with a read-back of its control words (one host
+                              synchronisation) and returns the call's own status. 1: the call
+                              returns SLSTM_OK once its kernels are queued (host-side argument
+                              errors are still returned at once), and the error words of the
+                              work space are not reset, so they keep the first op error and any
+                              time-out or index error of every deferred call since the last call
+                              made with 0; stacklstm_sync_status reads them. Calls with 0 reset
+                              them (make the first call on a new work space with 0). */
 } slstm_dims;
 
 #define SLSTM_PHASE_EVENTS 10

@@ -12,7 +12,7 @@
 #include "rec_config.h"
 #include "recurrent.h"
 
-__global__ void k_init_ctl(uint32_t* ctl);
+__global__ void k_init_ctl(uint32_t* ctl, int keep_errors);
 template <bool LDS>
 __global__ void k_scan(const int8_t* ops, int T, int B, int cap, int32_t* ptr, int32_t* top, int32_t* depth_end,
                        int32_t* gstack, uint32_t* ctl);
@@ -23,7 +23,7 @@ __global__ void k_gather_top4(const int32_t* top, const float* hcell, const floa
 __global__ void k_permute_w(const float* W, float* Wp32, bf16_t* Wp16, bf16_t* WpT16, int I, int H);
 __global__ void k_fill_f32(float* p, size_t n, float v);
 __global__ void k_zero_u32(uint32_t* p, int n);
-__global__ void k_zero_ctl_bwd(uint32_t* ctl);
+__global__ void k_zero_ctl_bwd(uint32_t* ctl, int keep_errors);
 __global__ void k_fill_pattern(unsigned char* p, size_t bytes, uint32_t v);
 __global__ void k_h0_bf16(const float* h0, bf16_t* hx, size_t n);
 __global__ void k_to_bf16x8(const float* in, bf16_t* out, size_t n8);
@@ -304,6 +304,13 @@ int read_status(const uint32_t* ctl, hipStream_t st) {
   return SLSTM_OK;
 }
 
+// The status a call returns: its control words read back (one host synchronisation), or,
+// for a deferred call, OK once its kernels are queued (sync_status reads the words later).
+int call_status(const slstm_dims* d, const uint32_t* ctl, hipStream_t st) {
+  if (hipGetLastError() != hipSuccess) return SLSTM_EDEVICE;
+  return d->defer_status ? SLSTM_OK : read_status(ctl, st);
+}
+
 // Backward direct staging: a variant built with it, whole 1 KB row segments, K range equal
 // to the register capacity, and the LDS slice plus static LDS within one CU (one workgroup
 // per CU).
@@ -408,7 +415,7 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   // a1: op validation, pointer scan and producer trace. One thread per element; its stack of
   // T + 1 step indices in LDS when a few elements' stacks fit in 64 KB, else in the work space
   mark(d, 0, st);
-  hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl);
+  hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(256), 0, st, ctl, d->defer_status ? 1 : 0);
   {
     const int cap = (T + 1) | 1;                  // odd: neighbouring stacks start in other banks
     int R = (int)std::min<size_t>(64, 65536 / ((size_t)cap * 4));
@@ -423,7 +430,7 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   }
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 1, st);
-  if (T == 0) return read_status(ctl, st);
+  if (T == 0) return call_status(d, ctl, st);
 
   // a2: XW = x W + b for all steps on the library's MFMA GEMM, columns gate-interleaved
   // (Wp = W with permuted columns; bf16 mode: Wp and its transpose in bf16), bias added in
@@ -508,7 +515,7 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
   }
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 4, st);
-  return read_status(ctl, st);
+  return call_status(d, ctl, st);
 }
 
 bool fwd_args_ok(const slstm_dims* d, const float* x, const int8_t* ops, const float* W, const float* U,
@@ -594,7 +601,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
   const int T = d->T, B = d->B, I = d->I, H = d->H;
   const bool bf = p.prec == SLSTM_BF16_GEMM;
   // the backward's control words (slot and barrier counters, wait and index flags) start at 0
-  hipLaunchKernelGGL(k_zero_ctl_bwd, dim3(1), dim3(256), 0, st, ctl);
+  hipLaunchKernelGGL(k_zero_ctl_bwd, dim3(1), dim3(256), 0, st, ctl, d->defer_status ? 1 : 0);
   if (T == 0) {
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)I * 4 * H)), dim3(256), 0, st, dW, (size_t)I * 4 * H, 0.f);
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)H * 4 * H)), dim3(256), 0, st, dU, (size_t)H * 4 * H, 0.f);
@@ -602,7 +609,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, dh0, (size_t)B * H, 0.f);
     hipLaunchKernelGGL(k_fill_f32, dim3(grid1d((size_t)B * H)), dim3(256), 0, st, dc0, (size_t)B * H, 0.f);
     if ((rc = hip_status(hipGetLastError()))) return rc;
-    return read_status(ctl, st);
+    return call_status(d, ctl, st);
   }
 
   // a8: persistent reverse loop
@@ -709,7 +716,7 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                      I);
   if ((rc = hip_status(hipGetLastError()))) return rc;
   mark(d, 9, st);
-  return read_status(ctl, st);
+  return call_status(d, ctl, st);
 }
 
 int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream) {

@@ -6,8 +6,15 @@
 // earliest failing step decides the code.
 #include "common.h"
 
-__global__ void __launch_bounds__(256) k_init_ctl(uint32_t* ctl) {
-  for (int i = threadIdx.x; i < CTL_WORDS; i += blockDim.x) ctl[i] = (i == CTL_STATUS) ? kStatusOk : 0u;
+// Control words of a forward call at 0 (status: no error). With keep_errors (a deferred
+// call) the error words keep what earlier calls on the work space set: the lowest failing
+// element's op status, the time-out and the index flag.
+__global__ void __launch_bounds__(256) k_init_ctl(uint32_t* ctl, int keep_errors) {
+  for (int i = threadIdx.x; i < CTL_WORDS; i += blockDim.x) {
+    const bool err = i == CTL_STATUS || i == CTL_TIMEOUT || i == CTL_BADIDX;
+    if (keep_errors && err) continue;
+    ctl[i] = (i == CTL_STATUS) ? kStatusOk : 0u;
+  }
 }
 
 // Op validation, pointer scan and producer trace in one pass (section 3: the unified update
@@ -181,14 +188,17 @@ __global__ void __launch_bounds__(256) k_to_bf16x8(const float* __restrict__ in,
 
 // Clears the backward's control words: slot counters, group barrier counters, the wait flags
 // and the index flag (the op status of the forward stays: the backward reports only its own).
-__global__ void __launch_bounds__(256) k_zero_ctl_bwd(uint32_t* __restrict__ ctl) {
+// (keep_errors: a deferred call; the error words stay as earlier calls left them)
+__global__ void __launch_bounds__(256) k_zero_ctl_bwd(uint32_t* __restrict__ ctl, int keep_errors) {
   for (int i = threadIdx.x; i < 16; i += blockDim.x) ctl[CTL_XCC_SLOT_B + i] = 0u;
   for (int i = threadIdx.x; i < 16 * MAX_GROUPS; i += blockDim.x) ctl[CTL_BAR_B + i] = 0u;
   if (threadIdx.x == 0) {
-    ctl[CTL_STATUS] = kStatusOk;
     ctl[CTL_ABORT] = 0u;
-    ctl[CTL_TIMEOUT] = 0u;
-    ctl[CTL_BADIDX] = 0u;
+    if (!keep_errors) {
+      ctl[CTL_STATUS] = kStatusOk;
+      ctl[CTL_TIMEOUT] = 0u;
+      ctl[CTL_BADIDX] = 0u;
+    }
   }
 }
 

@@ -36,7 +36,7 @@ class StackLSTMError(RuntimeError):
 class slstm_dims(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32), ("I", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("precision", ctypes.c_int32), ("spin_limit", ctypes.c_int32), ("phase_events", ctypes.c_void_p),
-                ("step_clock", ctypes.c_void_p)]
+                ("step_clock", ctypes.c_void_p), ("defer_status", ctypes.c_int32)]
 
 SLSTM_PHASE_EVENTS = 10
 
@@ -84,8 +84,9 @@ def _status_string(code: int) -> str:
         return "?"
 
 
-def make_dims(T: int, B: int, I: int, H: int, precision: int = SLSTM_FP32, spin_limit: int = 0) -> slstm_dims:
-    return slstm_dims(int(T), int(B), int(I), int(H), int(precision), int(spin_limit), None, None)
+def make_dims(T: int, B: int, I: int, H: int, precision: int = SLSTM_FP32, spin_limit: int = 0,
+              defer_status: int = 0) -> slstm_dims:
+    return slstm_dims(int(T), int(B), int(I), int(H), int(precision), int(spin_limit), None, None, int(defer_status))
 
 
 def _ptr(t: Optional[torch.Tensor], dtype=None, what="tensor"):

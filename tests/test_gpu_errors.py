@@ -133,3 +133,39 @@ def test_corrupted_top_reported(precision):
                          r.dc_top, r.dx, r.dW, r.dU, r.db, r.dh0, r.dc0, check=False)
     assert rc == 0
     assert s.stacklstm_sync_status(r.workspace) == 0
+
+
+def test_deferred_status():
+    """Deferred calls return OK without a read-back; they give the same results as ordinary
+    calls, keep the first error of any of them for stacklstm_sync_status, and an ordinary call
+    resets it."""
+    need_gpu()
+    from paper_1904_03409_amd.stacklstm import DeviceRun, stacklstm_sync_status
+    wl = wk.custom(T=12, B=40, I=8, H=32, seed=3)
+    ref = DeviceRun.from_workload(wl)
+    assert ref.forward(check=False) == 0 and ref.backward(check=False) == 0
+    want = ref.results()
+    r = DeviceRun.from_workload(wl)
+    assert r.forward(check=False) == 0 and r.backward(check=False) == 0   # resets the error words
+    r.dims.defer_status = 1
+    for _ in range(2):
+        assert r.forward(check=False) == 0 and r.backward(check=False) == 0
+    torch.cuda.synchronize()
+    assert stacklstm_sync_status(r.workspace) == 0
+    got = r.results()
+    for k in want:
+        assert np.array_equal(want[k], got[k]), k
+    # an invalid op in a deferred call, then valid deferred calls: still reported
+    bad_ops = wl.ops.copy()
+    bad_ops[4, 7] = 5
+    rb = DeviceRun.from_workload(wk.custom(T=12, B=40, I=8, H=32, seed=3, ops=bad_ops))
+    assert rb.forward(check=False) == 2                                      # ordinary call: its own status
+    rb.dims.defer_status = 1
+    assert rb.forward(check=False) == 0 and rb.backward(check=False) == 0
+    rb.ops.copy_(torch.from_numpy(wl.ops).to(rb.ops.device))
+    assert rb.forward(check=False) == 0 and rb.backward(check=False) == 0
+    torch.cuda.synchronize()
+    assert stacklstm_sync_status(rb.workspace) == 2
+    rb.dims.defer_status = 0
+    assert rb.forward(check=False) == 0                                      # resets: valid ops now
+    assert stacklstm_sync_status(rb.workspace) == 0
