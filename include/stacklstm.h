@@ -162,8 +162,9 @@ int stacklstm_bwd(const slstm_dims* d, const float* x, const int8_t* ops, const 
                   void* workspace, size_t ws_bytes, const float* dh_top, const float* dc_top, float* dx, float* dW,
                   float* dU, float* db, float* dh0, float* dc0, void* stream);
 
-/* Synchronises `stream` and reports again the status of the last call on `workspace`
- * (what that call returned from its read-back, for calls whose return value was lost). */
+/* Synchronises `stream` and reports the status held by the error words of `workspace`: that
+ * of the last ordinary call (what it returned from its read-back, for calls whose return value
+ * was lost), together with the first error of every deferred call made since (defer_status). */
 int stacklstm_sync_status(const void* workspace, size_t ws_bytes, void* stream);
 
 /* Static text for a status code. */
