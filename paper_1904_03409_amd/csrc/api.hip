@@ -234,9 +234,13 @@ Layout layout(const slstm_dims* d) {
   L.dh = o; o += align256((T + 1) * B * H * 4);
   L.dc = o; o += align256((T + 1) * B * H * 4);
   L.dbp = o; o += align256((size_t)MAX_GROUPS * 4 * H * 4);
-  // split-K partials of dW / dU, and the K-slice partials of dx (at most the rows of the grid's
-  // whole tiles: padded T*B x I)
-  L.part = o; o += align256(std::max((size_t)64 * std::max(I, H) * 4 * H, (T * B + 127) / 128 * 128 * I) * 4);
+  // split-K partials of dW / dU (at most min(64, ceil(T*B / 64)) slices: the split counts never
+  // exceed the GEMM's 64-row K steps over the T*B rows), the K-slice partials of dx (at most the
+  // rows of the grid's whole tiles: padded T*B x I), and the fp32 backward's gate-split partial
+  // sums (two step buffers of the groups' rows, at most B + 127, x H/16 workgroups x H)
+  const size_t max_splits = std::min<size_t>(64, std::max<size_t>(1, (T * B + 63) / 64));
+  L.part = o; o += align256(std::max({max_splits * std::max(I, H) * 4 * H, (T * B + 127) / 128 * 128 * I,
+                                      bf ? 0 : 2 * (B + 127) * ((H + 15) / 16) * H}) * 4);
   L.prow = o; o += align256(std::max<size_t>(T * B * 4, 16));         // push-row list
   L.total = o;
   return L;

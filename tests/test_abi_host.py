@@ -40,6 +40,9 @@ def test_host_only_entry_points():
     assert s.stacklstm_workspace_bytes(s.make_dims(8, 4, 3, 2000, s.SLSTM_FP32)) == 0    # H > 512 in fp32
     assert s.stacklstm_workspace_bytes(s.make_dims(8, 4, 3, 1024, s.SLSTM_BF16_GEMM)) > 0
     assert s.stacklstm_workspace_bytes(s.make_dims(8, 0, 3, 16, s.SLSTM_FP32)) == 0      # B < 1
+    # the post-loop split-K partials are sized by the slices T*B rows allow (here one), not by
+    # the 64-slice cap: a small problem at H = 1024 needs tens of MB, not a GB
+    assert s.stacklstm_workspace_bytes(s.make_dims(8, 4, 3, 1024, s.SLSTM_BF16_GEMM)) < (64 << 20)
     for code in range(9):
         assert s._status_string(code) not in ("", "?", "unknown status")
     assert s._status_string(99) == "unknown status"
