@@ -2,9 +2,9 @@
 
 Every kernel's resource usage is read from the compiler's resource report, and the build
 fails if a kernel that counts its own outstanding vector-memory operations (the wide
-forward, and the backward variants built with direct dA staging) uses scratch memory:
-spill loads and stores share that counter, so a counted wait would no longer wait for the
-loads it counts.
+forward, the LDS-DMA ring GEMM, and the backward variants built with direct dA staging) uses
+scratch memory: spill loads and stores share that counter, so a counted wait would no longer
+wait for the loads it counts.
 
 The device assembly of every source is kept (-save-temps) and scanned for one hazard the
 compiler has been seen to miss: an MFMA chain at the end of a basic block whose results are
@@ -43,7 +43,7 @@ def bwd_direct_built(prec: int, nt: int, ks: int) -> bool:
 
 def counted_waits(name: str) -> bool:
     """Kernels (mangled names) whose code counts outstanding vector-memory operations."""
-    if name.startswith("_Z10k_fwd_wide"):
+    if name.startswith("_Z10k_fwd_wide") or name.startswith("_Z11k_gemm_ring"):
         return True
     # k_bwd<prec, NT, KS, OCC, GS>: the gate-split variants (GS = true) have no direct staging
     m = re.match(r"_Z5k_bwdILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELb([01])E", name)

@@ -35,6 +35,7 @@ __global__ void k_transpose_bf16(const void* src, int src_f32, int ld, int cols,
                                  const uint32_t* count, int ldo, const int32_t* gtop, int B, bf16_t* out, uint32_t* ctl);
 template <int PREC, int AL, int BL> __global__ void k_gemm(GemmArgs g);
 __global__ void k_gemm_wide(GemmArgs g);
+__global__ void k_gemm_ring(GemmArgs g);
 __global__ void k_reduce_splits(const float* P, int splits, size_t split_stride, int M, int N, int unperm_H,
                                 float* out);
 __global__ void k_scatter_splits(const float* P, const int32_t* rows, const uint32_t* count, size_t max_rows, int N,
@@ -469,8 +470,15 @@ int fwd_impl(const slstm_dims* d, const Plan& p, const Layout& L, const float* x
       g.A = x16;
       al = GEMM_MK;
     }
-    // (bf16 operands: the wide-tile GEMM when its 256 x 256 tiles alone fill the chip)
-    if (gemm_wide_ok(p.prec, al, GEMM_NK, g) && wide_tiles(g.M, g.N) >= 256) {
+    // (bf16 operands: the wide-tile GEMM when its 256 x 256 tiles alone fill the chip; fp32:
+    // the LDS-DMA ring GEMM when its operands allow 16-byte DMAs with 32-bit offsets)
+    const bool ring = !bf && g.K % 4 == 0 && g.N % 4 == 0 && al16(x) && (size_t)g.M * g.lda * 4 < ((size_t)1 << 32) &&
+                      (size_t)g.K * g.ldb * 4 < ((size_t)1 << 32);
+    if (ring) {
+      hipLaunchKernelGGL(k_gemm_ring, dim3((g.N + kGemmBN - 1) / kGemmBN, (g.M + kGemmBM - 1) / kGemmBM), dim3(256), 0, st,
+                         g);
+      if ((rc = hip_status(hipGetLastError()))) return rc;
+    } else if (gemm_wide_ok(p.prec, al, GEMM_NK, g) && wide_tiles(g.M, g.N) >= 256) {
       if ((rc = launch_gemm_wide(g, 1, st))) return rc;
     } else if ((rc = launch_gemm(p.prec, al, bf ? GEMM_NK : GEMM_KN, g, 1, st))) {
       return rc;

@@ -550,3 +550,147 @@ INST(0, GEMM_MK, GEMM_NK)
 INST(0, GEMM_KM, GEMM_KN)
 INST(1, GEMM_MK, GEMM_NK)
 INST(1, GEMM_MK_F32, GEMM_NK)
+
+// fp32 GEMM for A stored MK and B stored KN (the input projection x Wp + b): the tiles, waves,
+// MFMAs and epilogue of k_gemm<0, MK, KN>, but the operand slices (16 deep) go from global
+// memory straight into a ring of kRingStages LDS stages by LDS DMA, issued that many slices
+// less one ahead.
+// k_gemm stages one slice in registers, one slice ahead, and a second register stage does
+// not fit its register budget. A DMA writes one contiguous kilobyte of LDS per wave
+// instruction, so the lanes fetch the 16-byte chunks that a swizzled layout puts at their
+// slots: A row m holds its chunk c at slot c ^ ((m >> 2) & 3), B row k holds column n at
+// n ^ 16 (k & 3), and the fragment reads of a wave then fall in 64 distinct banks. Every
+// wave issues four DMAs per slice, also past the last slice (out of range: zeros), so
+// "this slice has landed" is always the wait for all but the later slices' DMAs.
+// Requires K and N multiples of 4, A 16-byte aligned, and A, B under 4 GB.
+namespace {
+constexpr int kRingK = 16;                                  // K per slice
+constexpr int kRingStages = 4;
+constexpr int kRingStage = BM * kRingK + kRingK * BN;       // floats per stage: A, then B
+__device__ __forceinline__ int ring_a(int m, int k) { return m * kRingK + ((((k >> 2) ^ (m >> 2)) & 3) << 2) + (k & 3); }
+__device__ __forceinline__ int ring_b(int k, int n) { return BM * kRingK + k * BN + (n ^ ((k & 3) << 4)); }
+}  // namespace
+
+__global__ void __launch_bounds__(256, 2) k_gemm_ring(GemmArgs g) {
+  constexpr int OLD = BN + 4;                       // row stride of the staged output (floats)
+  constexpr size_t RING_BYTES = (size_t)kRingStages * kRingStage * 4;
+  constexpr size_t OUT_BYTES = (size_t)BM * OLD * 4;
+  __shared__ __align__(16) float rs_s[(RING_BYTES > OUT_BYTES ? RING_BYTES : OUT_BYTES) / 4];
+  // block -> tile: the XCD-contiguous, m-grouped order of k_gemm
+  constexpr int GM = 8;
+  const int NTL = (int)gridDim.x, MTL = (int)gridDim.y;
+  const int nblk = NTL * MTL;
+  int lid = (int)blockIdx.x + NTL * (int)blockIdx.y;
+  {
+    const int full = nblk & ~7;
+    if (lid < full) lid = (lid & 7) * (full >> 3) + (lid >> 3);
+  }
+  const int gidx = lid / (GM * NTL);
+  const int gm = min(GM, MTL - gidx * GM);
+  const int r = lid - gidx * GM * NTL;
+  const int m0 = (gidx * GM + r % gm) * BM, n0 = (r / gm) * BN;
+  const int M = g.M, N = g.N, K = g.K;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int l16 = lane & 15, lq = lane >> 4;
+  const float* A = (const float*)g.A;
+  const float* Bp = (const float*)g.Bm;
+  const rsrc_t ra = make_rsrc(A, (size_t)M * g.lda * 4);
+  const rsrc_t rb = make_rsrc(Bp, (size_t)K * g.ldb * 4);
+
+  // slice s into stage s % 4: wave w copies A rows [32w, 32w+32) (two DMAs of 16 rows) and B
+  // rows [4w, 4w+4) (two DMAs of 2 rows)
+  auto issue = [&](int s) {
+    float* st = rs_s + (s % kRingStages) * kRingStage;
+    const int k0 = s * kRingK;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int r0 = 32 * wave + 16 * q, rr = r0 + (lane >> 2), c = (lane & 3) ^ ((rr >> 2) & 3);
+      const bool ok = m0 + rr < M && k0 + 4 * c < K;
+      bdma16(ra, ok ? (uint32_t)(((size_t)(m0 + rr) * g.lda + k0 + 4 * c) * 4) : kOOB, 0u, lds_addr(st + r0 * kRingK));
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int kk0 = 4 * wave + 2 * q, kk = kk0 + (lane >> 5), n = ((lane & 31) * 4) ^ ((kk & 3) << 4);
+      const bool ok = k0 + kk < K && n0 + n < N;
+      bdma16(rb, ok ? (uint32_t)(((size_t)(k0 + kk) * g.ldb + n0 + n) * 4) : kOOB, 0u,
+             lds_addr(st + BM * kRingK + kk0 * BN));
+    }
+  };
+
+  // epilogue operands, loaded before the DMAs (loads and DMAs share one in-order counter)
+  float bias[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = n0 + wn * 64 + j * 16 + 4 * lq + q;
+      bias[j][q] = (g.bias && n < N) ? g.bias[perm_to_orig(n, g.bias_H)] : 0.f;
+    }
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int ns = (K + kRingK - 1) / kRingK;
+#pragma unroll
+  for (int s = 0; s < kRingStages - 1; ++s) issue(s);
+  for (int s = 0; s < ns; ++s) {
+    // this wave's part of slice s has landed (the later slices' DMAs may still be in flight)
+    wait_vm<4 * (kRingStages - 2)>();
+    // every wave's part has, and every wave is done with the stage slice s-1 used
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    issue(s + kRingStages - 1);
+    const float* st = rs_s + (s % kRingStages) * kRingStage;
+    // one MFMA k-step covers k = 4*kc + lq; the fragments of step kc+1 are read before the
+    // MFMAs of step kc
+    float av[2][4], bv[2][4];
+    auto rd = [&](int kc, float (&a4)[4], float (&b4)[4]) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a4[i] = st[ring_a(wm * 64 + i * 16 + l16, 4 * kc + lq)];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b4[j] = st[ring_b(4 * kc + lq, wn * 64 + j * 16 + l16)];
+    };
+    rd(0, av[0], bv[0]);
+#pragma unroll
+    for (int kc = 0; kc < kRingK / 4; ++kc) {
+      const int cur = kc & 1;
+      if (kc + 1 < kRingK / 4) rd(kc + 1, av[cur ^ 1], bv[cur ^ 1]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32_16x16x4(bv[cur][j], av[cur][i], acc[i][j]);
+    }
+  }
+  wait_vm<0>();                                     // the DMAs past the last slice (zeros)
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  // epilogue as k_gemm's: the tile (bias added) through LDS, whole rows stored non-temporally
+  float* os = rs_s;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *(f32x4*)&os[(wm * 64 + i * 16 + l16) * OLD + wn * 64 + j * 16 + 4 * lq] =
+          f32x4{acc[i][j][0] + bias[j][0], acc[i][j][1] + bias[j][1], acc[i][j][2] + bias[j][2],
+                acc[i][j][3] + bias[j][3]};
+  __syncthreads();
+  float* C = g.C;
+  const bool cvec = (g.ldc % 4) == 0 && (((uintptr_t)C) & 15u) == 0;
+#pragma unroll 4
+  for (int it = 0; it < BM * BN / 4 / 256; ++it) {
+    const int idx = (int)threadIdx.x + 256 * it, rw = idx / (BN / 4), c = (idx % (BN / 4)) * 4;
+    const int m = m0 + rw, n = n0 + c;
+    if (m >= M) continue;
+    const f32x4 v = *(const f32x4*)&os[rw * OLD + c];
+    float* cp = C + (size_t)m * g.ldc + n;
+    if (cvec && n + 3 < N) {
+      __builtin_nontemporal_store(v, (f32x4*)cp);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (n + q < N) cp[q] = v[q];
+    }
+  }
+}
