@@ -554,15 +554,14 @@ INST(1, GEMM_MK_F32, GEMM_NK)
 // fp32 GEMM for A stored MK and B stored KN (the input projection x Wp + b): the tiles, waves,
 // MFMAs and epilogue of k_gemm<0, MK, KN>, but the operand slices (16 deep) go from global
 // memory straight into a ring of kRingStages LDS stages by LDS DMA, issued that many slices
-// less one ahead.
-// k_gemm stages one slice in registers, one slice ahead, and a second register stage does
-// not fit its register budget. A DMA writes one contiguous kilobyte of LDS per wave
+// less one ahead (k_gemm stages one slice in registers, one slice ahead, and a second register
+// stage does not fit its register budget). A DMA writes one contiguous kilobyte of LDS per wave
 // instruction, so the lanes fetch the 16-byte chunks that a swizzled layout puts at their
 // slots: A row m holds its chunk c at slot c ^ ((m >> 2) & 3), B row k holds column n at
 // n ^ 16 (k & 3), and the fragment reads of a wave then fall in 64 distinct banks. Every
 // wave issues four DMAs per slice, also past the last slice (out of range: zeros), so
 // "this slice has landed" is always the wait for all but the later slices' DMAs.
-// Requires K and N multiples of 4, A 16-byte aligned, and A, B under 4 GB.
+// Requires K and N multiples of 4, A and B 16-byte aligned, and A, B under 4 GB.
 namespace {
 constexpr int kRingK = 16;                                  // K per slice
 constexpr int kRingStages = 4;
